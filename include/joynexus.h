@@ -1,0 +1,237 @@
+/*
+ * joynexus.h -- C ABI of the MI355X (gfx950) group-batched step.
+ *
+ * The step follows the multi-tenant group batching of JoyNexus
+ * (Sec. 4.3 "Multi-Tenant Group Batching", its figure of the pipeline;
+ * App. A.3 "Inference Queue Composition"; Sec. 5.2 "Multi-Tenant
+ * Group-Batched Execution"):
+ *
+ *   jn_pack_group          canonicalize + pad: concatenate compatible tenant
+ *                          requests into one physical batch and record the
+ *                          slices that partition it again
+ *   jn_backbone_forward    one frozen shared-backbone forward over that batch
+ *                          (the "encode" of App. A.3), attention confined to
+ *                          each sample
+ *   jn_tenant_heads_fwd_bwd split the shared features by tenant; per tenant:
+ *                          action-head forward, loss, weight gradients (the
+ *                          tenant-private decode / loss / backward of Sec. 5.2;
+ *                          nothing is averaged across tenants)
+ *   jn_unpack              scatter packed rows back to the requests' own
+ *                          padded buffers (the "split" by slices, App. A.3)
+ *
+ * Conventions
+ *   - bf16 is the IEEE-754 binary32 upper half (bfloat16), stored as 2 bytes.
+ *   - Every device buffer is owned by the caller.  The library allocates no
+ *     device memory after jn_ctx_create; scratch comes from the caller's
+ *     workspace.  It keeps no pointer after a call returns.
+ *   - Calls are asynchronous on the context's HIP stream.  All validation is
+ *     done before anything is enqueued: a non-OK status means nothing was
+ *     written to any output.  jn_last_error() holds a message for the last
+ *     non-OK status of that context.
+ *   - "host" arrays are read during the call and may be reused on return.
+ *   - One context per stream and per host thread; contexts share nothing.
+ *   - Weight matrices are row-major [out][in].
+ */
+#ifndef JOYNEXUS_H
+#define JOYNEXUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum jn_status {
+  JN_OK = 0,
+  JN_EINVAL = 1,        /* null pointer, bad option or count                    */
+  JN_EINCOMPAT = 2,     /* tenants do not share the backbone's prefix interface */
+  JN_ESHAPE = 3,        /* a length, size or index out of its range             */
+  JN_ENOSPACE = 4,      /* a caller buffer or workspace is too small            */
+  JN_EHIP = 5,          /* the HIP runtime reported an error                    */
+  JN_EUNSUPPORTED = 6   /* a shape the kernels do not implement                 */
+} jn_status;
+
+typedef struct jn_ctx jn_ctx;
+
+/* Create a context bound to `hip_stream` (a hipStream_t, borrowed; NULL = the
+ * null stream) on the current HIP device.  Allocates pinned host staging for
+ * index-map uploads. */
+jn_status jn_ctx_create(jn_ctx** out, void* hip_stream);
+void jn_ctx_destroy(jn_ctx* ctx);
+/* Rebind the context to another stream of the same device. */
+jn_status jn_ctx_set_stream(jn_ctx* ctx, void* hip_stream);
+/* Message for the last non-OK status returned on this context ("" if none). */
+const char* jn_last_error(const jn_ctx* ctx);
+
+/* ---------------------------------------------------------------- pack --- */
+
+/* One inference / training request of one tenant (App. A.3: a request carries
+ * the tenant identity, its schema signature and a batch of observations; here
+ * the observations are already embedded by the tenant's front end). */
+typedef struct jn_request {
+  int32_t tenant;          /* slot in the tenant table                       */
+  int32_t n_samples;       /* >= 1                                           */
+  int32_t max_len;         /* rows per sample in `embeds` (canonical length) */
+  int32_t reserved;
+  const void* embeds;      /* device bf16 [n_samples][max_len][d]            */
+  const int32_t* lengths;  /* host int32 [n_samples]: valid rows, 1..max_len */
+} jn_request;
+
+/* A tenant taking part in the group.  Compatibility is decided at the shared
+ * frozen-prefix boundary, not by tenant identity (App. A.3): every tenant in
+ * the table must carry the same `prefix_sig` and consume features of the
+ * backbone's width. */
+typedef struct jn_tenant {
+  uint64_t prefix_sig;     /* signature of the shared-prefix interface */
+  int32_t d_model;         /* feature width the tenant expects         */
+  int32_t reserved;
+} jn_tenant;
+
+typedef struct jn_pack_opts {
+  int32_t d_model;         /* backbone width d (row width of embeds)            */
+  int32_t align;           /* each sample occupies roundup(len, align) rows, >=1 */
+} jn_pack_opts;
+
+typedef struct jn_pack_sizes {
+  int32_t N;               /* samples                                   */
+  int32_t T;               /* packed rows (sum of aligned lengths)      */
+  int32_t max_seqlen;      /* longest valid length                      */
+  int32_t reserved;
+  int64_t map_bytes;       /* size of the index-map buffer to allocate  */
+  int64_t token_bytes;     /* size of the packed-token buffer: T*d*2    */
+} jn_pack_sizes;
+
+/* The physical batch: sizes plus device pointers into the caller's buffers.
+ * Filled by jn_pack_group; read by the later calls.  Map meaning (all int32):
+ *   seqlens[N]            valid rows of sample i
+ *   cu_seqlens[N+1]       first packed row of sample i (aligned prefix sums)
+ *   sample_request[N]     request of sample i (arrival order: requests in the
+ *                         order given, samples in order inside a request)
+ *   sample_local[N]       index of sample i inside its request
+ *   sample_tenant[N]      tenant slot of sample i
+ *   tenant_sample_off[G+1] first tenant-order position of tenant g
+ *   tenant_perm[N]        sample at tenant-order position k (stable by tenant)
+ *   sample_tenant_rank[N] tenant-order position of sample i (inverse of perm)
+ *   token_sample[T]       sample of packed row t, -1 for an alignment row
+ *   token_pos[T]          row of that sample, -1 for an alignment row      */
+typedef struct jn_packed {
+  int32_t R, G, N, T, d, max_seqlen, align, reserved;
+  void* tokens;            /* device bf16 [T][d]; alignment rows are zero */
+  int32_t* seqlens;
+  int32_t* cu_seqlens;
+  int32_t* sample_request;
+  int32_t* sample_local;
+  int32_t* sample_tenant;
+  int32_t* tenant_sample_off;
+  int32_t* tenant_perm;
+  int32_t* sample_tenant_rank;
+  int32_t* token_sample;
+  int32_t* token_pos;
+  void* req_table;         /* library-internal request table [R] (32 B each) */
+} jn_packed;
+
+/* Sizes of the physical batch (host only, touches no device). */
+jn_status jn_pack_plan(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                       const jn_pack_opts* opts, jn_pack_sizes* out);
+
+/* The same index maps, computed on the host into `host_maps` (map_bytes from
+ * jn_pack_plan), in the layout jn_pack_group uses on the device:
+ *   seqlens | cu_seqlens | sample_request | sample_local | sample_tenant |
+ *   tenant_sample_off | tenant_perm | sample_tenant_rank | token_sample |
+ *   token_pos | request table (32 B per request, library-internal), each
+ *   array starting on a 256-byte boundary of the buffer.
+ * `out` receives host pointers into `host_maps` (tokens = NULL). */
+jn_status jn_pack_maps_host(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                            const jn_pack_opts* opts, void* host_maps, size_t map_bytes,
+                            jn_packed* out);
+
+/* Build the physical batch on the device: index maps into `maps`
+ * (map_bytes), packed rows into `tokens` (token_bytes).  Row
+ * cu_seqlens[i] + j of `tokens` is row j of sample i for j < seqlens[i];
+ * alignment rows are zero.  Bit-exact copy. */
+jn_status jn_pack_group(jn_ctx* ctx, const jn_request* req, int32_t R, const jn_tenant* ten,
+                        int32_t G, const jn_pack_opts* opts, void* maps, size_t map_bytes,
+                        void* tokens, size_t token_bytes, jn_packed* out);
+
+/* ------------------------------------------------------------ backbone --- */
+
+typedef struct jn_layer {
+  const void* wqkv;        /* bf16 [3d][d]: q rows, then k rows, then v rows;
+                              head h uses rows h*hd .. h*hd+hd-1 of each      */
+  const void* wo;          /* bf16 [d][d]                                     */
+  const void* w_up;        /* bf16 [f][d]                                     */
+  const void* w_gate;      /* bf16 [f][d] for a GeGLU MLP, NULL for GELU MLP  */
+  const void* w_down;      /* bf16 [d][f]                                     */
+  const void* g1;          /* bf16 [d] pre-attention RMSNorm gain             */
+  const void* g2;          /* bf16 [d] pre-MLP RMSNorm gain                   */
+} jn_layer;
+
+/* Frozen shared backbone: pre-RMSNorm transformer blocks
+ *   h = RMS(x) g1; q,k,v = h Wqkv^T; x += Attn(q,k,v) Wo^T;
+ *   h = RMS(x) g2; x += Wdown gelu(Wup h)   or   Wdown (gelu(Wgate h) * Wup h)
+ * then z = RMS(x) gf.  Attention is bidirectional within a sample and never
+ * crosses samples; RMS(x) = x / sqrt(mean(x^2) + eps); gelu is the tanh form.
+ * Arithmetic: bf16 GEMM / attention operands with fp32 accumulation, fp32
+ * residual stream, fp32 norm / softmax statistics, bf16 stored activations. */
+typedef struct jn_backbone {
+  int32_t n_layers, d, n_heads, ffn;
+  float eps;
+  int32_t reserved;
+  const jn_layer* layers;  /* host array [n_layers] of device pointers */
+  const void* gf;          /* bf16 [d] final RMSNorm gain              */
+} jn_backbone;
+
+/* Workspace bytes jn_backbone_forward needs for a batch of T rows. */
+jn_status jn_backbone_workspace_size(const jn_backbone* bb, int32_t T, size_t* bytes);
+
+/* hidden: device bf16 [T][d], written for every row (alignment rows zero). */
+jn_status jn_backbone_forward(jn_ctx* ctx, const jn_backbone* bb, const jn_packed* p,
+                              void* hidden, void* ws, size_t ws_bytes);
+
+/* --------------------------------------------------------------- heads --- */
+
+/* A tenant-private MLP action head: y = W_L gelu(... gelu(W_1 p + b_1) ...) + b_L
+ * with p the mean of the sample's valid rows of the shared feature. */
+typedef struct jn_head {
+  int32_t n_layers;            /* >= 1                                       */
+  int32_t action_dim, chunk;   /* dims[n_layers] == action_dim * chunk       */
+  int32_t reserved;
+  const int32_t* dims;         /* host [n_layers+1], dims[0] == d            */
+  const float* const* W;       /* host [n_layers] of device fp32 [dims[k+1]][dims[k]] */
+  const float* const* b;       /* host [n_layers] of device fp32 [dims[k+1]] */
+} jn_head;
+
+/* Per-tenant inputs and outputs.  Rows follow the tenant's own arrival order
+ * (the order of its samples in the request list). */
+typedef struct jn_head_io {
+  const float* targets;        /* device fp32 [n_g][chunk][action_dim]       */
+  float* actions;              /* out: device fp32 [n_g][chunk*action_dim]   */
+  float* loss;                 /* out: device fp32 [1], mean squared error   */
+  float* const* dW;            /* host [n_layers] of device fp32 outputs [out][in] */
+  float* const* db;            /* host [n_layers] of device fp32 outputs [out]     */
+} jn_head_io;
+
+jn_status jn_heads_workspace_size(const jn_packed* p, const jn_head* heads, int32_t G, size_t* bytes);
+
+/* Pool, then per tenant g (heads[g], io[g]): forward, loss
+ * L_g = mean((y - t)^2), and dL_g/dW, dL_g/db of every head layer (fp32).
+ * No gradient flows into the frozen backbone.  `pooled` (optional, may be
+ * NULL): device fp32 [N][d] receives the pooled features in tenant order. */
+jn_status jn_tenant_heads_fwd_bwd(jn_ctx* ctx, const jn_packed* p, const void* hidden,
+                                  const jn_head* heads, const jn_head_io* io, int32_t G,
+                                  void* ws, size_t ws_bytes, float* pooled);
+
+/* -------------------------------------------------------------- unpack --- */
+
+/* Scatter packed rows back to the requests: for sample i of request r and
+ * j < max_len_r, out[r][s][j] = rows[cu_seqlens[i] + j] if j < seqlens[i],
+ * else zero.  `rows`: device [T][row_bytes]; `req_out`: host array [R] of
+ * device buffers [n_r][max_len_r][row_bytes]; row_bytes a multiple of 4. */
+jn_status jn_unpack(jn_ctx* ctx, const jn_packed* p, const jn_request* req, int32_t R,
+                    const void* rows, size_t row_bytes, void* const* req_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,291 @@
+"""MI355X (gfx950) group-batched step of JoyNexus multi-tenant group batching.
+
+Thin Python binding of ``libjoynexus.so`` (C ABI in ``include/joynexus.h``):
+the functions below carry the C names and only marshal arguments -- every
+step of the path runs in the library's HIP kernels.  PyTorch supplies device
+memory and streams.  Importing this package fails if the library is not
+built; there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+from . import _abi
+from ._abi import (JN_OK, STATUS_NAMES, jn_backbone, jn_head, jn_head_io, jn_layer, jn_pack_opts,
+                   jn_pack_sizes, jn_packed, jn_request, jn_tenant)
+
+_lib = _abi.load()
+
+__all__ = [
+    "JNError", "Context", "Request", "Tenant", "Backbone", "Head", "HeadIO",
+    "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group", "jn_backbone_workspace_size",
+    "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
+    "lib_path",
+]
+
+
+def lib_path() -> str:
+    return _abi.LIB_PATH
+
+
+class JNError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _check(st: int, ctx: "Context" = None, what: str = ""):
+    if st != JN_OK:
+        msg = _lib.jn_last_error(ctx.handle).decode() if ctx is not None else what
+        raise JNError(st, msg or what)
+
+
+def _ptr(t) -> int:
+    """Device pointer of a torch tensor (or an int)."""
+    if t is None:
+        return None
+    return t if isinstance(t, int) else t.data_ptr()
+
+
+class Context:
+    """A library context bound to a HIP stream (default: torch's current stream)."""
+
+    def __init__(self, stream=None):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        h = C.c_void_p()
+        _check(_lib.jn_ctx_create(C.byref(h), C.c_void_p(stream.cuda_stream)), what="jn_ctx_create")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            _lib.jn_ctx_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- marshal ---
+
+class Request:
+    """A tenant request: ``embeds`` device bf16 [n, max_len, d], host lengths."""
+
+    def __init__(self, tenant: int, embeds, lengths, max_len: int = None):
+        self.tenant = int(tenant)
+        self.embeds = embeds
+        self.lengths = np.ascontiguousarray(lengths, dtype=np.int32)
+        self.n = int(self.lengths.shape[0])
+        self.max_len = int(max_len) if max_len is not None else int(embeds.shape[1])
+
+
+class Tenant:
+    def __init__(self, prefix_sig: int, d_model: int):
+        self.prefix_sig = int(prefix_sig)
+        self.d_model = int(d_model)
+
+
+def _requests(reqs: Sequence[Request]):
+    arr = (jn_request * len(reqs))()
+    keep = []
+    for i, r in enumerate(reqs):
+        lens = r.lengths
+        keep.append(lens)
+        arr[i].tenant = r.tenant
+        arr[i].n_samples = r.n
+        arr[i].max_len = r.max_len
+        arr[i].embeds = _ptr(r.embeds) if r.embeds is not None else None
+        arr[i].lengths = lens.ctypes.data_as(C.POINTER(C.c_int32))
+    return arr, keep
+
+
+def _tenants(ten: Sequence[Tenant]):
+    arr = (jn_tenant * len(ten))()
+    for i, t in enumerate(ten):
+        arr[i].prefix_sig = t.prefix_sig
+        arr[i].d_model = t.d_model
+    return arr
+
+
+def _opts(d: int, align: int):
+    o = jn_pack_opts()
+    o.d_model = d
+    o.align = align
+    return o
+
+
+# ---------------------------------------------------------------- pack ------
+
+def jn_pack_plan(reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int = 1) -> jn_pack_sizes:
+    ra, keep = _requests(reqs)
+    ta = _tenants(tenants)
+    out = jn_pack_sizes()
+    o = _opts(d, align)
+    _check(_lib.jn_pack_plan(ra, len(reqs), ta, len(tenants), C.byref(o), C.byref(out)), what="jn_pack_plan")
+    return out
+
+
+def jn_pack_maps_host(reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int = 1) -> dict:
+    """Index maps computed on the host by the library (numpy int32 arrays)."""
+    sz = jn_pack_plan(reqs, tenants, d, align)
+    buf = np.zeros(int(sz.map_bytes), dtype=np.uint8)
+    ra, keep = _requests(reqs)
+    ta = _tenants(tenants)
+    out = jn_packed()
+    o = _opts(d, align)
+    _check(_lib.jn_pack_maps_host(ra, len(reqs), ta, len(tenants), C.byref(o),
+                                  buf.ctypes.data_as(C.c_void_p), buf.nbytes, C.byref(out)), what="jn_pack_maps_host")
+    base = buf.ctypes.data
+    res = {"N": out.N, "T": out.T, "max_seqlen": out.max_seqlen}
+    for name in jn_packed.MAP_FIELDS:
+        off = C.cast(getattr(out, name), C.c_void_p).value - base
+        res[name] = buf[off: off + 4 * out.map_len(name)].view(np.int32).copy()
+    return res
+
+
+class Packed:
+    """A packed batch: the C struct plus the tensors it points into."""
+
+    def __init__(self, struct: jn_packed, maps, tokens):
+        self.struct = struct
+        self.maps = maps
+        self.tokens = tokens
+
+    def __getattr__(self, k):
+        return getattr(self.struct, k)
+
+    def map_tensor(self, name: str):
+        """View of one device index map as an int32 tensor."""
+        import torch
+        off = C.cast(getattr(self.struct, name), C.c_void_p).value - self.maps.data_ptr()
+        n = self.struct.map_len(name)
+        return self.maps[off: off + 4 * n].view(torch.int32)
+
+
+def jn_pack_group(ctx: Context, reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int,
+                  maps, tokens) -> Packed:
+    ra, keep = _requests(reqs)
+    ta = _tenants(tenants)
+    out = jn_packed()
+    o = _opts(d, align)
+    _check(_lib.jn_pack_group(ctx.handle, ra, len(reqs), ta, len(tenants), C.byref(o), _ptr(maps),
+                              maps.numel() * maps.element_size(), _ptr(tokens),
+                              tokens.numel() * tokens.element_size(), C.byref(out)), ctx)
+    return Packed(out, maps, tokens)
+
+
+# ------------------------------------------------------------ backbone ------
+
+class Backbone:
+    """Device weights of the frozen backbone (lists of torch bf16 tensors)."""
+
+    def __init__(self, layers: List[dict], gf, n_heads: int, eps: float):
+        self.layers = layers
+        self.gf = gf
+        self.n_heads = int(n_heads)
+        self.eps = float(eps)
+        self.d = int(gf.shape[0])
+        self.ffn = int(layers[0]["w_up"].shape[0])
+        arr = (jn_layer * len(layers))()
+        for i, L in enumerate(layers):
+            arr[i].wqkv = _ptr(L["wqkv"])
+            arr[i].wo = _ptr(L["wo"])
+            arr[i].w_up = _ptr(L["w_up"])
+            arr[i].w_gate = _ptr(L.get("w_gate"))
+            arr[i].w_down = _ptr(L["w_down"])
+            arr[i].g1 = _ptr(L["g1"])
+            arr[i].g2 = _ptr(L["g2"])
+        self._arr = arr
+        s = jn_backbone()
+        s.n_layers = len(layers)
+        s.d = self.d
+        s.n_heads = self.n_heads
+        s.ffn = self.ffn
+        s.eps = self.eps
+        s.layers = C.cast(arr, C.POINTER(jn_layer))
+        s.gf = _ptr(gf)
+        self.struct = s
+
+
+def jn_backbone_workspace_size(bb: Backbone, T: int) -> int:
+    n = C.c_size_t()
+    _check(_lib.jn_backbone_workspace_size(C.byref(bb.struct), T, C.byref(n)), what="jn_backbone_workspace_size")
+    return int(n.value)
+
+
+def jn_backbone_forward(ctx: Context, bb: Backbone, packed: Packed, hidden, ws):
+    _check(_lib.jn_backbone_forward(ctx.handle, C.byref(bb.struct), C.byref(packed.struct), _ptr(hidden),
+                                    _ptr(ws), ws.numel() * ws.element_size()), ctx)
+
+
+# --------------------------------------------------------------- heads ------
+
+class Head:
+    """A tenant's MLP head: lists of device fp32 W [out, in] and b [out]."""
+
+    def __init__(self, W: list, b: list, action_dim: int, chunk: int):
+        self.W, self.b = W, b
+        self.dims = np.array([int(W[0].shape[1])] + [int(w.shape[0]) for w in W], dtype=np.int32)
+        s = jn_head()
+        s.n_layers = len(W)
+        s.action_dim = int(action_dim)
+        s.chunk = int(chunk)
+        self._W = (C.c_void_p * len(W))(*[_ptr(w) for w in W])
+        self._b = (C.c_void_p * len(b))(*[_ptr(x) for x in b])
+        s.dims = self.dims.ctypes.data_as(C.POINTER(C.c_int32))
+        s.W = C.cast(self._W, C.POINTER(C.c_void_p))
+        s.b = C.cast(self._b, C.POINTER(C.c_void_p))
+        self.struct = s
+
+
+class HeadIO:
+    """A tenant's targets and outputs (device fp32 tensors)."""
+
+    def __init__(self, targets, actions, loss, dW: list, db: list):
+        self.targets, self.actions, self.loss, self.dW, self.db = targets, actions, loss, dW, db
+        s = jn_head_io()
+        s.targets = _ptr(targets)
+        s.actions = _ptr(actions)
+        s.loss = _ptr(loss)
+        self._dW = (C.c_void_p * len(dW))(*[_ptr(w) for w in dW])
+        self._db = (C.c_void_p * len(db))(*[_ptr(x) for x in db])
+        s.dW = C.cast(self._dW, C.POINTER(C.c_void_p))
+        s.db = C.cast(self._db, C.POINTER(C.c_void_p))
+        self.struct = s
+
+
+def _head_arrays(heads: Sequence[Head], ios: Sequence[HeadIO] = None):
+    ha = (jn_head * len(heads))(*[h.struct for h in heads])
+    ia = (jn_head_io * len(ios))(*[x.struct for x in ios]) if ios is not None else None
+    return ha, ia
+
+
+def jn_heads_workspace_size(packed: Packed, heads: Sequence[Head]) -> int:
+    ha, _ = _head_arrays(heads)
+    n = C.c_size_t()
+    _check(_lib.jn_heads_workspace_size(C.byref(packed.struct), ha, len(heads), C.byref(n)),
+           what="jn_heads_workspace_size")
+    return int(n.value)
+
+
+def jn_tenant_heads_fwd_bwd(ctx: Context, packed: Packed, hidden, heads: Sequence[Head], ios: Sequence[HeadIO],
+                            ws, pooled=None):
+    ha, ia = _head_arrays(heads, ios)
+    _check(_lib.jn_tenant_heads_fwd_bwd(ctx.handle, C.byref(packed.struct), _ptr(hidden), ha, ia, len(heads),
+                                        _ptr(ws), ws.numel() * ws.element_size(), _ptr(pooled)), ctx)
+
+
+# -------------------------------------------------------------- unpack ------
+
+def jn_unpack(ctx: Context, packed: Packed, reqs: Sequence[Request], rows, row_bytes: int, outs: Sequence):
+    ra, keep = _requests(reqs)
+    oa = (C.c_void_p * len(outs))(*[_ptr(o) for o in outs])
+    _check(_lib.jn_unpack(ctx.handle, C.byref(packed.struct), ra, len(reqs), _ptr(rows), int(row_bytes), oa), ctx)

@@ -1,0 +1,120 @@
+"""ctypes mirror of ``include/joynexus.h`` (argument marshalling only).
+
+Every function of the C ABI is exposed under its own name; device buffers
+are passed as raw pointers (``tensor.data_ptr()``), host arrays as ctypes
+arrays.  Nothing here computes any part of the step.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libjoynexus.so")
+
+JN_OK, JN_EINVAL, JN_EINCOMPAT, JN_ESHAPE, JN_ENOSPACE, JN_EHIP, JN_EUNSUPPORTED = range(7)
+STATUS_NAMES = {0: "JN_OK", 1: "JN_EINVAL", 2: "JN_EINCOMPAT", 3: "JN_ESHAPE", 4: "JN_ENOSPACE",
+                5: "JN_EHIP", 6: "JN_EUNSUPPORTED"}
+
+EXPORTS = (
+    "jn_ctx_create", "jn_ctx_destroy", "jn_ctx_set_stream", "jn_last_error",
+    "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group",
+    "jn_backbone_workspace_size", "jn_backbone_forward",
+    "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
+)
+
+
+class jn_request(C.Structure):
+    _fields_ = [("tenant", C.c_int32), ("n_samples", C.c_int32), ("max_len", C.c_int32),
+                ("reserved", C.c_int32), ("embeds", C.c_void_p), ("lengths", C.POINTER(C.c_int32))]
+
+
+class jn_tenant(C.Structure):
+    _fields_ = [("prefix_sig", C.c_uint64), ("d_model", C.c_int32), ("reserved", C.c_int32)]
+
+
+class jn_pack_opts(C.Structure):
+    _fields_ = [("d_model", C.c_int32), ("align", C.c_int32)]
+
+
+class jn_pack_sizes(C.Structure):
+    _fields_ = [("N", C.c_int32), ("T", C.c_int32), ("max_seqlen", C.c_int32), ("reserved", C.c_int32),
+                ("map_bytes", C.c_int64), ("token_bytes", C.c_int64)]
+
+
+_I32P = C.POINTER(C.c_int32)
+
+
+class jn_packed(C.Structure):
+    _fields_ = [("R", C.c_int32), ("G", C.c_int32), ("N", C.c_int32), ("T", C.c_int32), ("d", C.c_int32),
+                ("max_seqlen", C.c_int32), ("align", C.c_int32), ("reserved", C.c_int32),
+                ("tokens", C.c_void_p),
+                ("seqlens", _I32P), ("cu_seqlens", _I32P), ("sample_request", _I32P), ("sample_local", _I32P),
+                ("sample_tenant", _I32P), ("tenant_sample_off", _I32P), ("tenant_perm", _I32P),
+                ("sample_tenant_rank", _I32P), ("token_sample", _I32P), ("token_pos", _I32P),
+                ("req_table", C.c_void_p)]
+
+    MAP_FIELDS = ("seqlens", "cu_seqlens", "sample_request", "sample_local", "sample_tenant",
+                  "tenant_sample_off", "tenant_perm", "sample_tenant_rank", "token_sample", "token_pos")
+
+    def map_len(self, name: str) -> int:
+        return {"cu_seqlens": self.N + 1, "tenant_sample_off": self.G + 1,
+                "token_sample": self.T, "token_pos": self.T}.get(name, self.N)
+
+
+class jn_layer(C.Structure):
+    _fields_ = [("wqkv", C.c_void_p), ("wo", C.c_void_p), ("w_up", C.c_void_p), ("w_gate", C.c_void_p),
+                ("w_down", C.c_void_p), ("g1", C.c_void_p), ("g2", C.c_void_p)]
+
+
+class jn_backbone(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d", C.c_int32), ("n_heads", C.c_int32), ("ffn", C.c_int32),
+                ("eps", C.c_float), ("reserved", C.c_int32), ("layers", C.POINTER(jn_layer)), ("gf", C.c_void_p)]
+
+
+class jn_head(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("action_dim", C.c_int32), ("chunk", C.c_int32), ("reserved", C.c_int32),
+                ("dims", _I32P), ("W", C.POINTER(C.c_void_p)), ("b", C.POINTER(C.c_void_p))]
+
+
+class jn_head_io(C.Structure):
+    _fields_ = [("targets", C.c_void_p), ("actions", C.c_void_p), ("loss", C.c_void_p),
+                ("dW", C.POINTER(C.c_void_p)), ("db", C.POINTER(C.c_void_p))]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Load the built library and declare its prototypes (raises if missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() (hipcc --offload-arch=gfx950)")
+    lib = C.CDLL(path)
+    P, V = C.POINTER, C.c_void_p
+    sig = {
+        "jn_ctx_create": (C.c_int, [P(V), V]),
+        "jn_ctx_destroy": (None, [V]),
+        "jn_ctx_set_stream": (C.c_int, [V, V]),
+        "jn_last_error": (C.c_char_p, [V]),
+        "jn_pack_plan": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                   P(jn_pack_sizes)]),
+        "jn_pack_maps_host": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                        V, C.c_size_t, P(jn_packed)]),
+        "jn_pack_group": (C.c_int, [V, P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                    V, C.c_size_t, V, C.c_size_t, P(jn_packed)]),
+        "jn_backbone_workspace_size": (C.c_int, [P(jn_backbone), C.c_int32, P(C.c_size_t)]),
+        "jn_backbone_forward": (C.c_int, [V, P(jn_backbone), P(jn_packed), V, V, C.c_size_t]),
+        "jn_heads_workspace_size": (C.c_int, [P(jn_packed), P(jn_head), C.c_int32, P(C.c_size_t)]),
+        "jn_tenant_heads_fwd_bwd": (C.c_int, [V, P(jn_packed), V, P(jn_head), P(jn_head_io), C.c_int32, V,
+                                              C.c_size_t, V]),
+        "jn_unpack": (C.c_int, [V, P(jn_packed), P(jn_request), C.c_int32, V, C.c_size_t, P(V)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib

@@ -1,0 +1,756 @@
+// Host side of the C ABI: validation, the pack plan, workspace carving,
+// pinned staging of small tables, and launch sequencing on the context stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "jn_internal.h"
+
+using namespace jnx;
+
+// --------------------------------------------------------------- context ---
+
+namespace {
+constexpr int kSlots = 8;
+struct StageSlot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+}  // namespace
+
+struct jn_ctx {
+  hipStream_t stream = nullptr;
+  int device = 0;
+  std::string err;
+  StageSlot slots[kSlots];
+  int next = 0;
+};
+
+namespace {
+
+jn_status fail(jn_ctx* c, jn_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  return code;
+}
+
+jn_status hip_fail(jn_ctx* c, hipError_t e, const char* what) {
+  return fail(c, JN_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define JN_HIP(ctx, call, what)                         \
+  do {                                                  \
+    hipError_t _e = (call);                             \
+    if (_e != hipSuccess) return hip_fail(ctx, _e, what); \
+  } while (0)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Stage `bytes` of host data in pinned memory and copy it to `dst` on the
+// context stream.  Slots are reused round-robin; a slot is rewritten only
+// after the copy that last read it has completed.
+jn_status stage_copy(jn_ctx* c, void* dst, const void* src, size_t bytes) {
+  if (bytes == 0) return JN_OK;
+  StageSlot& s = c->slots[c->next];
+  c->next = (c->next + 1) % kSlots;
+  if (s.pending) {
+    JN_HIP(c, hipEventSynchronize(s.ev), "hipEventSynchronize(staging)");
+    s.pending = false;
+  }
+  if (s.cap < bytes) {
+    if (s.host) JN_HIP(c, hipHostFree(s.host), "hipHostFree");
+    s.host = nullptr;
+    s.cap = 0;
+    size_t cap = align_up(std::max<size_t>(bytes, 1 << 16), 1 << 16);
+    JN_HIP(c, hipHostMalloc(&s.host, cap, hipHostMallocDefault), "hipHostMalloc(staging)");
+    s.cap = cap;
+  }
+  std::memcpy(s.host, src, bytes);
+  JN_HIP(c, hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, c->stream), "hipMemcpyAsync(H2D)");
+  JN_HIP(c, hipEventRecord(s.ev, c->stream), "hipEventRecord(staging)");
+  s.pending = true;
+  return JN_OK;
+}
+
+// ------------------------------------------------------------------ plan ---
+
+struct MapLayout {
+  size_t seqlens, cu, sreq, sloc, sten, toff, tperm, trank, tsamp, tpos, reqtab, total;
+};
+
+MapLayout map_layout(int64_t N, int64_t T, int64_t G, int64_t R) {
+  MapLayout m{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  m.seqlens = take(4 * N);
+  m.cu = take(4 * (N + 1));
+  m.sreq = take(4 * N);
+  m.sloc = take(4 * N);
+  m.sten = take(4 * N);
+  m.toff = take(4 * (G + 1));
+  m.tperm = take(4 * N);
+  m.trank = take(4 * N);
+  m.tsamp = take(4 * T);
+  m.tpos = take(4 * T);
+  m.reqtab = take(sizeof(ReqEntry) * R);
+  m.total = o;
+  return m;
+}
+
+struct Plan {
+  int32_t N = 0, T = 0, max_seqlen = 0, max_rows = 0, max_req_len = 0;
+  std::vector<int32_t> seqlens, cu, sreq, sloc, sten, toff, tperm, trank;
+  std::vector<int32_t> req_first;
+};
+
+// Validates the request / tenant tables and computes every N- and G-sized
+// map.  Arrival order = request order, samples in order; tenant order is a
+// stable counting sort by tenant slot.
+jn_status make_plan(jn_ctx* c, const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                    const jn_pack_opts* o, Plan* p) {
+  if (!req || !ten || !o || !p) return fail(c, JN_EINVAL, "null argument");
+  if (R < 1) return fail(c, JN_EINVAL, "need at least one request (R=%d)", R);
+  if (G < 1) return fail(c, JN_EINVAL, "need at least one tenant (G=%d)", G);
+  if (o->align < 1 || o->align > 4096) return fail(c, JN_EINVAL, "align %d outside [1, 4096]", o->align);
+  if (o->d_model < 1) return fail(c, JN_EINVAL, "d_model %d < 1", o->d_model);
+  for (int32_t g = 0; g < G; ++g) {
+    if (ten[g].prefix_sig != ten[0].prefix_sig)
+      return fail(c, JN_EINCOMPAT, "tenant %d has a different shared-prefix signature", g);
+    if (ten[g].d_model != o->d_model)
+      return fail(c, JN_EINCOMPAT, "tenant %d expects width %d, backbone has %d", g, ten[g].d_model,
+                  o->d_model);
+  }
+  int64_t N = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (req[r].tenant < 0 || req[r].tenant >= G)
+      return fail(c, JN_ESHAPE, "request %d names tenant %d outside the table of %d", r, req[r].tenant, G);
+    if (req[r].n_samples < 1) return fail(c, JN_ESHAPE, "request %d has no samples", r);
+    if (req[r].max_len < 1) return fail(c, JN_ESHAPE, "request %d has max_len %d", r, req[r].max_len);
+    if (!req[r].embeds || !req[r].lengths) return fail(c, JN_EINVAL, "request %d has a null pointer", r);
+    N += req[r].n_samples;
+  }
+  if (N >= (1ll << 30)) return fail(c, JN_ESHAPE, "too many samples");
+  p->N = (int32_t)N;
+  p->seqlens.resize(N);
+  p->cu.resize(N + 1);
+  p->sreq.resize(N);
+  p->sloc.resize(N);
+  p->sten.resize(N);
+  p->req_first.resize(R);
+  int64_t i = 0, T = 0;
+  int32_t mx = 0, mreq = 0;
+  p->cu[0] = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    p->req_first[r] = (int32_t)i;
+    mreq = std::max(mreq, req[r].max_len);
+    for (int32_t s = 0; s < req[r].n_samples; ++s, ++i) {
+      int32_t L = req[r].lengths[s];
+      if (L < 1 || L > req[r].max_len)
+        return fail(c, JN_ESHAPE, "request %d sample %d: length %d outside [1, %d]", r, s, L, req[r].max_len);
+      int64_t rows = (int64_t)(L + o->align - 1) / o->align * o->align;
+      T += rows;
+      if (T >= (1ll << 31) - 1) return fail(c, JN_ESHAPE, "packed batch overflows int32 row indices");
+      p->seqlens[i] = L;
+      p->cu[i + 1] = (int32_t)T;
+      p->sreq[i] = r;
+      p->sloc[i] = s;
+      p->sten[i] = req[r].tenant;
+      mx = std::max(mx, L);
+    }
+  }
+  p->T = (int32_t)T;
+  p->max_seqlen = mx;
+  p->max_rows = (int32_t)((int64_t)(mx + o->align - 1) / o->align * o->align);
+  p->max_req_len = mreq;
+  p->toff.assign(G + 1, 0);
+  for (int64_t k = 0; k < N; ++k) p->toff[p->sten[k] + 1]++;
+  for (int32_t g = 0; g < G; ++g) {
+    if (p->toff[g + 1] == 0) return fail(c, JN_ESHAPE, "tenant %d has no samples in this group", g);
+    p->toff[g + 1] += p->toff[g];
+  }
+  p->tperm.resize(N);
+  p->trank.resize(N);
+  std::vector<int32_t> fill(p->toff.begin(), p->toff.end() - 1);
+  for (int64_t k = 0; k < N; ++k) {
+    int32_t pos = fill[p->sten[k]]++;
+    p->tperm[pos] = (int32_t)k;
+    p->trank[k] = pos;
+  }
+  return JN_OK;
+}
+
+void fill_packed(jn_packed* out, char* base, const MapLayout& m, const Plan& p, int32_t R, int32_t G,
+                 const jn_pack_opts* o) {
+  std::memset(out, 0, sizeof(*out));
+  out->R = R;
+  out->G = G;
+  out->N = p.N;
+  out->T = p.T;
+  out->d = o->d_model;
+  out->max_seqlen = p.max_seqlen;
+  out->align = o->align;
+  out->seqlens = (int32_t*)(base + m.seqlens);
+  out->cu_seqlens = (int32_t*)(base + m.cu);
+  out->sample_request = (int32_t*)(base + m.sreq);
+  out->sample_local = (int32_t*)(base + m.sloc);
+  out->sample_tenant = (int32_t*)(base + m.sten);
+  out->tenant_sample_off = (int32_t*)(base + m.toff);
+  out->tenant_perm = (int32_t*)(base + m.tperm);
+  out->sample_tenant_rank = (int32_t*)(base + m.trank);
+  out->token_sample = (int32_t*)(base + m.tsamp);
+  out->token_pos = (int32_t*)(base + m.tpos);
+  out->req_table = base + m.reqtab;
+}
+
+// Host image of the maps region [0, m.tsamp) (the N/G-sized arrays).
+std::vector<char> host_head_image(const MapLayout& m, const Plan& p) {
+  std::vector<char> img(m.tsamp, 0);
+  auto put = [&](size_t off, const std::vector<int32_t>& v) {
+    if (!v.empty()) std::memcpy(img.data() + off, v.data(), 4 * v.size());
+  };
+  put(m.seqlens, p.seqlens);
+  put(m.cu, p.cu);
+  put(m.sreq, p.sreq);
+  put(m.sloc, p.sloc);
+  put(m.sten, p.sten);
+  put(m.toff, p.toff);
+  put(m.tperm, p.tperm);
+  put(m.trank, p.trank);
+  return img;
+}
+
+bool valid_packed(const jn_packed* p) {
+  return p && p->N > 0 && p->T > 0 && p->G > 0 && p->R > 0 && p->d > 0 && p->seqlens && p->cu_seqlens &&
+         p->sample_request && p->sample_local && p->tenant_sample_off && p->sample_tenant_rank &&
+         p->req_table;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ ABI ----
+
+extern "C" {
+
+jn_status jn_ctx_create(jn_ctx** out, void* hip_stream) {
+  if (!out) return JN_EINVAL;
+  *out = nullptr;
+  jn_ctx* c = new (std::nothrow) jn_ctx();
+  if (!c) return JN_EINVAL;
+  c->stream = (hipStream_t)hip_stream;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return JN_EHIP;
+  }
+  for (auto& s : c->slots) {
+    if (hipEventCreateWithFlags(&s.ev, hipEventDisableTiming) != hipSuccess) {
+      jn_ctx_destroy(c);
+      return JN_EHIP;
+    }
+  }
+  *out = c;
+  return JN_OK;
+}
+
+void jn_ctx_destroy(jn_ctx* c) {
+  if (!c) return;
+  for (auto& s : c->slots) {
+    if (s.pending) hipEventSynchronize(s.ev);
+    if (s.host) hipHostFree(s.host);
+    if (s.ev) hipEventDestroy(s.ev);
+  }
+  delete c;
+}
+
+jn_status jn_ctx_set_stream(jn_ctx* c, void* hip_stream) {
+  if (!c) return JN_EINVAL;
+  c->stream = (hipStream_t)hip_stream;
+  return JN_OK;
+}
+
+const char* jn_last_error(const jn_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+jn_status jn_pack_plan(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                       const jn_pack_opts* o, jn_pack_sizes* out) {
+  if (!out) return JN_EINVAL;
+  Plan p;
+  jn_status st = make_plan(nullptr, req, R, ten, G, o, &p);
+  if (st != JN_OK) return st;
+  MapLayout m = map_layout(p.N, p.T, G, R);
+  std::memset(out, 0, sizeof(*out));
+  out->N = p.N;
+  out->T = p.T;
+  out->max_seqlen = p.max_seqlen;
+  out->map_bytes = (int64_t)m.total;
+  out->token_bytes = (int64_t)p.T * o->d_model * 2;
+  return JN_OK;
+}
+
+jn_status jn_pack_maps_host(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                            const jn_pack_opts* o, void* host_maps, size_t map_bytes, jn_packed* out) {
+  if (!host_maps || !out) return JN_EINVAL;
+  Plan p;
+  jn_status st = make_plan(nullptr, req, R, ten, G, o, &p);
+  if (st != JN_OK) return st;
+  MapLayout m = map_layout(p.N, p.T, G, R);
+  if (map_bytes < m.total) return JN_ENOSPACE;
+  std::vector<char> img = host_head_image(m, p);
+  char* base = (char*)host_maps;
+  std::memset(base, 0, m.total);
+  std::memcpy(base, img.data(), img.size());
+  int32_t* ts = (int32_t*)(base + m.tsamp);
+  int32_t* tp = (int32_t*)(base + m.tpos);
+  for (int32_t i = 0; i < p.N; ++i) {
+    for (int32_t t = p.cu[i]; t < p.cu[i + 1]; ++t) {
+      int32_t j = t - p.cu[i];
+      ts[t] = j < p.seqlens[i] ? i : -1;
+      tp[t] = j < p.seqlens[i] ? j : -1;
+    }
+  }
+  ReqEntry* rt = (ReqEntry*)(base + m.reqtab);
+  for (int32_t r = 0; r < R; ++r) rt[r] = ReqEntry{req[r].embeds, nullptr, req[r].max_len, req[r].n_samples, p.req_first[r], 0};
+  fill_packed(out, base, m, p, R, G, o);
+  return JN_OK;
+}
+
+jn_status jn_pack_group(jn_ctx* c, const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                        const jn_pack_opts* o, void* maps, size_t map_bytes, void* tokens,
+                        size_t token_bytes, jn_packed* out) {
+  if (!c) return JN_EINVAL;
+  if (!maps || !tokens || !out) return fail(c, JN_EINVAL, "null output buffer");
+  Plan p;
+  jn_status st = make_plan(c, req, R, ten, G, o, &p);
+  if (st != JN_OK) return st;
+  MapLayout m = map_layout(p.N, p.T, G, R);
+  if (map_bytes < m.total) return fail(c, JN_ENOSPACE, "map buffer %zu B < %zu B", map_bytes, m.total);
+  size_t need_tok = (size_t)p.T * o->d_model * 2;
+  if (token_bytes < need_tok) return fail(c, JN_ENOSPACE, "token buffer %zu B < %zu B", token_bytes, need_tok);
+  if (o->d_model % 8 != 0) return fail(c, JN_EUNSUPPORTED, "d_model %d not a multiple of 8", o->d_model);
+  for (int32_t r = 0; r < R; ++r)
+    if (((uintptr_t)req[r].embeds) % 16 != 0) return fail(c, JN_EUNSUPPORTED, "request %d embeds not 16-byte aligned", r);
+  if (((uintptr_t)tokens) % 16 != 0) return fail(c, JN_EUNSUPPORTED, "token buffer not 16-byte aligned");
+
+  std::vector<char> img = host_head_image(m, p);
+  std::vector<ReqEntry> rt(R);
+  for (int32_t r = 0; r < R; ++r) rt[r] = ReqEntry{req[r].embeds, nullptr, req[r].max_len, req[r].n_samples, p.req_first[r], 0};
+  char* base = (char*)maps;
+  st = stage_copy(c, base, img.data(), img.size());
+  if (st != JN_OK) return st;
+  st = stage_copy(c, base + m.reqtab, rt.data(), sizeof(ReqEntry) * R);
+  if (st != JN_OK) return st;
+  jn_packed tmp;
+  fill_packed(&tmp, base, m, p, R, G, o);
+  tmp.tokens = tokens;
+  JN_HIP(c, launch_pack(c->stream, (const ReqEntry*)tmp.req_table, tmp.sample_request, tmp.sample_local,
+                        tmp.seqlens, tmp.cu_seqlens, p.N, o->d_model, o->align, p.max_rows, tokens,
+                        tmp.token_sample, tmp.token_pos),
+         "pack kernel");
+  *out = tmp;
+  return JN_OK;
+}
+
+// -------------------------------------------------------------- backbone ---
+
+namespace {
+
+struct BbLayout {
+  size_t x, h, qkv, att, mid, total;
+};
+
+BbLayout bb_layout(const jn_backbone* bb, int64_t T) {
+  BbLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  int64_t d = bb->d, f = bb->ffn;
+  L.x = take(4 * T * d);
+  L.h = take(2 * T * d);
+  L.qkv = take(2 * T * 3 * d);
+  L.att = take(2 * T * d);
+  L.mid = take(2 * T * f);
+  L.total = o;
+  return L;
+}
+
+jn_status check_backbone(jn_ctx* c, const jn_backbone* bb) {
+  if (!bb || !bb->layers || !bb->gf) return fail(c, JN_EINVAL, "null backbone");
+  if (bb->n_layers < 1 || bb->d < 1 || bb->n_heads < 1 || bb->ffn < 1)
+    return fail(c, JN_EINVAL, "backbone sizes must be positive");
+  if (bb->d % bb->n_heads != 0) return fail(c, JN_EINVAL, "d %% n_heads != 0");
+  int hd = bb->d / bb->n_heads;
+  if (hd != 32 && hd != 64 && hd != 128 && hd != 256)
+    return fail(c, JN_EUNSUPPORTED, "head dim %d not in {32,64,128,256}", hd);
+  if (bb->d % 128 != 0) return fail(c, JN_EUNSUPPORTED, "d %d not a multiple of 128", bb->d);
+  if (bb->ffn % 128 != 0) return fail(c, JN_EUNSUPPORTED, "ffn %d not a multiple of 128", bb->ffn);
+  if (!(bb->eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
+  bool glu = bb->layers[0].w_gate != nullptr;
+  for (int l = 0; l < bb->n_layers; ++l) {
+    const jn_layer& L = bb->layers[l];
+    if (!L.wqkv || !L.wo || !L.w_up || !L.w_down || !L.g1 || !L.g2)
+      return fail(c, JN_EINVAL, "layer %d has a null weight", l);
+    if ((L.w_gate != nullptr) != glu) return fail(c, JN_EINVAL, "layer %d mixes GELU and GeGLU MLPs", l);
+    const void* ps[] = {L.wqkv, L.wo, L.w_up, L.w_down, L.w_gate};
+    for (const void* q : ps)
+      if (q && ((uintptr_t)q) % 16 != 0) return fail(c, JN_EUNSUPPORTED, "layer %d weight not 16-byte aligned", l);
+  }
+  return JN_OK;
+}
+
+}  // namespace
+
+jn_status jn_backbone_workspace_size(const jn_backbone* bb, int32_t T, size_t* bytes) {
+  if (!bb || !bytes || T < 0) return JN_EINVAL;
+  *bytes = bb_layout(bb, T).total;
+  return JN_OK;
+}
+
+jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed* p, void* hidden, void* ws,
+                              size_t ws_bytes) {
+  if (!c) return JN_EINVAL;
+  jn_status st = check_backbone(c, bb);
+  if (st != JN_OK) return st;
+  if (!valid_packed(p) || !p->tokens) return fail(c, JN_EINVAL, "invalid packed batch");
+  if (p->d != bb->d) return fail(c, JN_EINCOMPAT, "packed width %d != backbone width %d", p->d, bb->d);
+  if (!hidden || !ws) return fail(c, JN_EINVAL, "null hidden or workspace");
+  BbLayout L = bb_layout(bb, p->T);
+  if (ws_bytes < L.total) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, L.total);
+  if (((uintptr_t)ws) % 256 != 0 || ((uintptr_t)hidden) % 16 != 0)
+    return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte and hidden 16-byte aligned");
+
+  const int32_t T = p->T, d = bb->d, f = bb->ffn;
+  char* w = (char*)ws;
+  float* x = (float*)(w + L.x);
+  void* h = w + L.h;
+  void* qkv = w + L.qkv;
+  void* att = w + L.att;
+  void* mid = w + L.mid;
+  const bool glu = bb->layers[0].w_gate != nullptr;
+  hipStream_t s = c->stream;
+  for (int l = 0; l < bb->n_layers; ++l) {
+    const jn_layer& Ly = bb->layers[l];
+    if (l == 0)
+      JN_HIP(c, launch_rmsnorm_bf16in(s, p->tokens, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
+    else
+      JN_HIP(c, launch_rmsnorm_f32in(s, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
+    JN_HIP(c, launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0), "gemm qkv");
+    JN_HIP(c, launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, p->max_seqlen,
+                               p->align),
+           "attention");
+    JN_HIP(c, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0), "gemm o");
+    JN_HIP(c, launch_rmsnorm_f32in(s, x, Ly.g2, h, T, d, bb->eps), "rmsnorm");
+    if (glu)
+      JN_HIP(c, launch_gemm(s, EPI_GEGLU_BF16, h, d, Ly.w_gate, Ly.w_up, d, mid, f, T, f, d, 0), "gemm geglu");
+    else
+      JN_HIP(c, launch_gemm(s, EPI_GELU_BF16, h, d, Ly.w_up, nullptr, d, mid, f, T, f, d, 0), "gemm up");
+    JN_HIP(c, launch_gemm(s, EPI_RESID_F32, mid, f, Ly.w_down, nullptr, f, x, d, T, d, f, 0), "gemm down");
+  }
+  JN_HIP(c, launch_rmsnorm_f32in(s, x, bb->gf, hidden, T, d, bb->eps), "final rmsnorm");
+  return JN_OK;
+}
+
+// ----------------------------------------------------------------- heads ---
+
+namespace {
+
+struct HeadPlan {
+  int maxL = 0;
+  std::vector<int64_t> width;      // per layer index k: max output width
+  size_t P = 0, Z0 = 0, total = 0; // offsets
+  std::vector<size_t> Z, H, dZ;    // per k
+  size_t descs = 0, tiles = 0;
+  std::vector<HeadGemm> dv;
+  std::vector<HeadTile> tv;
+  std::vector<LossDesc> lv;
+  size_t losses = 0;
+  // launch ranges into tv
+  std::vector<std::pair<int32_t, int32_t>> fwd, bwd;
+};
+
+constexpr int kHT = 64;  // fp32 head GEMM tile
+
+jn_status check_heads(jn_ctx* c, const jn_packed* p, const jn_head* heads, int32_t G) {
+  if (!heads) return fail(c, JN_EINVAL, "null heads");
+  if (G != p->G) return fail(c, JN_EINVAL, "G=%d but the packed batch has %d tenants", G, p->G);
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_head& H = heads[g];
+    if (H.n_layers < 1 || !H.dims || !H.W || !H.b) return fail(c, JN_EINVAL, "head %d incomplete", g);
+    if (H.dims[0] != p->d) return fail(c, JN_EINCOMPAT, "head %d input %d != feature width %d", g, H.dims[0], p->d);
+    for (int k = 0; k <= H.n_layers; ++k)
+      if (H.dims[k] < 1) return fail(c, JN_EINVAL, "head %d dims[%d] < 1", g, k);
+    if ((int64_t)H.action_dim * H.chunk != H.dims[H.n_layers])
+      return fail(c, JN_EINVAL, "head %d output %d != action_dim*chunk", g, H.dims[H.n_layers]);
+    for (int k = 0; k < H.n_layers; ++k)
+      if (!H.W[k] || !H.b[k]) return fail(c, JN_EINVAL, "head %d layer %d null weight", g, k);
+  }
+  return JN_OK;
+}
+
+// Workspace layout: pooled P [N][d] | per layer k: Z_k, H_k, dZ_k [N][width_k] |
+// loss descriptors | gemm descriptors | tiles.  Tenant g's rows of every
+// [N][*] buffer are its tenant-order rows [off_g, off_g + n_g).
+void head_layout(const jn_packed* p, const jn_head* heads, int32_t G, HeadPlan* hp, bool with_descs) {
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  const int64_t N = p->N;
+  hp->maxL = 0;
+  for (int32_t g = 0; g < G; ++g) hp->maxL = std::max(hp->maxL, heads[g].n_layers);
+  hp->width.assign(hp->maxL, 0);
+  for (int32_t g = 0; g < G; ++g)
+    for (int k = 0; k < heads[g].n_layers; ++k) hp->width[k] = std::max<int64_t>(hp->width[k], heads[g].dims[k + 1]);
+  hp->P = take(4 * N * p->d);
+  hp->Z.resize(hp->maxL);
+  hp->H.resize(hp->maxL);
+  hp->dZ.resize(hp->maxL);
+  for (int k = 0; k < hp->maxL; ++k) {
+    hp->Z[k] = take(4 * N * hp->width[k]);
+    hp->H[k] = take(4 * N * hp->width[k]);
+    hp->dZ[k] = take(4 * N * hp->width[k]);
+  }
+  if (!with_descs) {
+    // descriptor counts are bounded by G * 2 * maxL; tiles computed exactly below
+  }
+  // tile counts: fwd M-dynamic (ceil(N/64) upper bound), bwd wgrad + dgrad
+  const int64_t tm_dyn = (N + kHT - 1) / kHT;
+  int64_t ntiles = 0, ndesc = 0;
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_head& Hh = heads[g];
+    for (int k = 0; k < Hh.n_layers; ++k) {
+      int64_t in = Hh.dims[k], out = Hh.dims[k + 1];
+      ntiles += tm_dyn * ((out + kHT - 1) / kHT);                        // fwd
+      ntiles += ((out + kHT - 1) / kHT) * ((in + kHT - 1) / kHT);         // wgrad
+      if (k > 0) ntiles += tm_dyn * ((in + kHT - 1) / kHT);               // dgrad
+      ndesc += (k > 0) ? 3 : 2;
+    }
+  }
+  hp->losses = take(sizeof(LossDesc) * G);
+  hp->descs = take(sizeof(HeadGemm) * ndesc);
+  hp->tiles = take(sizeof(HeadTile) * ntiles);
+  hp->total = o;
+}
+
+}  // namespace
+
+jn_status jn_heads_workspace_size(const jn_packed* p, const jn_head* heads, int32_t G, size_t* bytes) {
+  if (!bytes || !valid_packed(p)) return JN_EINVAL;
+  jn_status st = check_heads(nullptr, p, heads, G);
+  if (st != JN_OK) return st;
+  HeadPlan hp;
+  head_layout(p, heads, G, &hp, false);
+  *bytes = hp.total;
+  return JN_OK;
+}
+
+jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_head* heads,
+                                  const jn_head_io* io, int32_t G, void* ws, size_t ws_bytes, float* pooled) {
+  if (!c) return JN_EINVAL;
+  if (!valid_packed(p)) return fail(c, JN_EINVAL, "invalid packed batch");
+  if (!hidden || !io || !ws) return fail(c, JN_EINVAL, "null hidden, io or workspace");
+  jn_status st = check_heads(c, p, heads, G);
+  if (st != JN_OK) return st;
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_head_io& I = io[g];
+    if (!I.targets || !I.actions || !I.loss || !I.dW || !I.db) return fail(c, JN_EINVAL, "io %d incomplete", g);
+    for (int k = 0; k < heads[g].n_layers; ++k)
+      if (!I.dW[k] || !I.db[k]) return fail(c, JN_EINVAL, "io %d layer %d null gradient", g, k);
+  }
+  HeadPlan hp;
+  head_layout(p, heads, G, &hp, true);
+  if (ws_bytes < hp.total) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, hp.total);
+  if (((uintptr_t)ws) % 256 != 0) return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte aligned");
+
+  char* w = (char*)ws;
+  float* P = pooled ? pooled : (float*)(w + hp.P);
+  const int64_t N = p->N, d = p->d;
+  const int32_t tm_dyn = (int32_t)((N + kHT - 1) / kHT);
+  auto Zk = [&](int k) { return (float*)(w + hp.Z[k]); };
+  auto Hk = [&](int k) { return (float*)(w + hp.H[k]); };
+  auto dZk = [&](int k) { return (float*)(w + hp.dZ[k]); };
+
+  std::vector<HeadGemm> descs;
+  std::vector<HeadTile> tiles;
+  std::vector<std::pair<int32_t, int32_t>> fwd_rng, bwd_rng;
+  // forward, one launch per layer index
+  for (int k = 0; k < hp.maxL; ++k) {
+    int32_t t0 = (int32_t)tiles.size();
+    for (int32_t g = 0; g < G; ++g) {
+      const jn_head& Hh = heads[g];
+      if (k >= Hh.n_layers) continue;
+      const int64_t in = Hh.dims[k], out = Hh.dims[k + 1];
+      const float* X = (k == 0) ? P : Hk(k - 1);
+      const int64_t ldx = (k == 0) ? d : hp.width[k - 1];
+      HeadGemm D{};
+      D.A = X;
+      D.sam = ldx;
+      D.sak = 1;
+      D.B = Hh.W[k];
+      D.sbk = 1;
+      D.sbn = in;
+      D.C = Zk(k);
+      D.ldc = hp.width[k];
+      D.bias = Hh.b[k];
+      D.Cact = (k + 1 < Hh.n_layers) ? Hk(k) : nullptr;
+      D.bumpA = ldx;
+      D.bumpB = 0;
+      D.bumpC = hp.width[k];
+      D.M = -1;
+      D.N = (int32_t)out;
+      D.K = (int32_t)in;
+      D.tenant = g;
+      D.tiles_n = (int32_t)((out + kHT - 1) / kHT);
+      int32_t di = (int32_t)descs.size();
+      descs.push_back(D);
+      for (int32_t tm = 0; tm < tm_dyn; ++tm)
+        for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
+    }
+    fwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+  }
+  // loss: y = Z_{L-1} rows, dY -> dZ_{L-1}
+  std::vector<LossDesc> losses(G);
+  for (int32_t g = 0; g < G; ++g) {
+    const int L = heads[g].n_layers;
+    losses[g] = LossDesc{Zk(L - 1), io[g].targets, dZk(L - 1), io[g].loss, io[g].actions,
+                         heads[g].dims[L], hp.width[L - 1], g, 0};
+  }
+  // backward, one launch per step s (tenant g at layer k = L_g - 1 - s)
+  for (int sidx = 0; sidx < hp.maxL; ++sidx) {
+    int32_t t0 = (int32_t)tiles.size();
+    for (int32_t g = 0; g < G; ++g) {
+      const jn_head& Hh = heads[g];
+      const int k = Hh.n_layers - 1 - sidx;
+      if (k < 0) continue;
+      const int64_t in = Hh.dims[k], out = Hh.dims[k + 1];
+      const float* X = (k == 0) ? P : Hk(k - 1);
+      const int64_t ldx = (k == 0) ? d : hp.width[k - 1];
+      // wgrad: dW[out][in] = sum_rows dZ[row][o] X[row][i]; db[o] = sum_rows dZ[row][o]
+      HeadGemm Wg{};
+      Wg.A = dZk(k);
+      Wg.sam = 1;
+      Wg.sak = hp.width[k];
+      Wg.B = X;
+      Wg.sbk = ldx;
+      Wg.sbn = 1;
+      Wg.C = io[g].dW[k];
+      Wg.ldc = in;
+      Wg.db = io[g].db[k];
+      Wg.bumpA = hp.width[k];
+      Wg.bumpB = ldx;
+      Wg.bumpC = 0;
+      Wg.M = (int32_t)out;
+      Wg.N = (int32_t)in;
+      Wg.K = -1;
+      Wg.tenant = g;
+      Wg.tiles_n = (int32_t)((in + kHT - 1) / kHT);
+      int32_t di = (int32_t)descs.size();
+      descs.push_back(Wg);
+      const int32_t tmw = (int32_t)((out + kHT - 1) / kHT);
+      for (int32_t tm = 0; tm < tmw; ++tm)
+        for (int32_t tn = 0; tn < Wg.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
+      if (k > 0) {
+        // dgrad: dZ_{k-1}[row][i] = (sum_o dZ_k[row][o] W[o][i]) * gelu'(Z_{k-1}[row][i])
+        HeadGemm Dg{};
+        Dg.A = dZk(k);
+        Dg.sam = hp.width[k];
+        Dg.sak = 1;
+        Dg.B = Hh.W[k];
+        Dg.sbk = in;
+        Dg.sbn = 1;
+        Dg.C = dZk(k - 1);
+        Dg.ldc = hp.width[k - 1];
+        Dg.Zg = Zk(k - 1);
+        Dg.bumpA = hp.width[k];
+        Dg.bumpB = 0;
+        Dg.bumpC = hp.width[k - 1];
+        Dg.M = -1;
+        Dg.N = (int32_t)in;
+        Dg.K = (int32_t)out;
+        Dg.tenant = g;
+        Dg.tiles_n = (int32_t)((in + kHT - 1) / kHT);
+        int32_t dj = (int32_t)descs.size();
+        descs.push_back(Dg);
+        for (int32_t tm = 0; tm < tm_dyn; ++tm)
+          for (int32_t tn = 0; tn < Dg.tiles_n; ++tn) tiles.push_back(HeadTile{dj, tm, tn, 0});
+      }
+    }
+    bwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+  }
+
+  // one upload of every table: losses | descs | tiles (contiguous in ws)
+  const size_t lbytes = sizeof(LossDesc) * G, dbytes = sizeof(HeadGemm) * descs.size(),
+               tbytes = sizeof(HeadTile) * tiles.size();
+  if (hp.descs + dbytes > hp.tiles || hp.tiles + tbytes > hp.total)
+    return fail(c, JN_ENOSPACE, "internal: head table sizing");
+  std::vector<char> img(hp.total - hp.losses, 0);
+  std::memcpy(img.data(), losses.data(), lbytes);
+  std::memcpy(img.data() + (hp.descs - hp.losses), descs.data(), dbytes);
+  std::memcpy(img.data() + (hp.tiles - hp.losses), tiles.data(), tbytes);
+  st = stage_copy(c, w + hp.losses, img.data(), hp.tiles - hp.losses + tbytes);
+  if (st != JN_OK) return st;
+  const LossDesc* dl = (const LossDesc*)(w + hp.losses);
+  const HeadGemm* dd = (const HeadGemm*)(w + hp.descs);
+  const HeadTile* dt = (const HeadTile*)(w + hp.tiles);
+  hipStream_t s = c->stream;
+
+  JN_HIP(c, launch_pool(s, hidden, p->seqlens, p->cu_seqlens, p->sample_tenant_rank, p->N, p->d, P), "pool");
+  for (auto& r : fwd_rng)
+    if (r.second) JN_HIP(c, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off), "head fwd");
+  JN_HIP(c, launch_mse(s, dl, G, p->tenant_sample_off), "loss");
+  for (auto& r : bwd_rng)
+    if (r.second) JN_HIP(c, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off), "head bwd");
+  return JN_OK;
+}
+
+// ---------------------------------------------------------------- unpack ---
+
+jn_status jn_unpack(jn_ctx* c, const jn_packed* p, const jn_request* req, int32_t R, const void* rows,
+                    size_t row_bytes, void* const* req_out) {
+  if (!c) return JN_EINVAL;
+  if (!valid_packed(p) || !p->token_sample) return fail(c, JN_EINVAL, "invalid packed batch");
+  if (!req || !rows || !req_out) return fail(c, JN_EINVAL, "null argument");
+  if (R != p->R) return fail(c, JN_EINVAL, "R=%d but the packed batch has %d requests", R, p->R);
+  if (row_bytes == 0 || row_bytes % 4 != 0) return fail(c, JN_EUNSUPPORTED, "row_bytes %zu not a positive multiple of 4", row_bytes);
+  if (((uintptr_t)rows) % 4 != 0) return fail(c, JN_EUNSUPPORTED, "rows not 4-byte aligned");
+  std::vector<ReqEntry> rt(R);
+  int64_t n = 0;
+  int32_t mreq = 0;
+  bool vec16 = row_bytes % 16 == 0 && ((uintptr_t)rows) % 16 == 0;
+  for (int32_t r = 0; r < R; ++r) {
+    if (!req_out[r]) return fail(c, JN_EINVAL, "request %d output is null", r);
+    if (((uintptr_t)req_out[r]) % 4 != 0) return fail(c, JN_EUNSUPPORTED, "request %d output not 4-byte aligned", r);
+    vec16 = vec16 && ((uintptr_t)req_out[r]) % 16 == 0;
+    if (req[r].n_samples < 1 || req[r].max_len < 1) return fail(c, JN_ESHAPE, "request %d shape", r);
+    rt[r] = ReqEntry{req[r].embeds, req_out[r], req[r].max_len, req[r].n_samples, (int32_t)n, 0};
+    n += req[r].n_samples;
+    mreq = std::max(mreq, req[r].max_len);
+  }
+  if (n != p->N) return fail(c, JN_ESHAPE, "requests hold %lld samples, packed batch %d", (long long)n, p->N);
+  jn_status st = stage_copy(c, p->req_table, rt.data(), sizeof(ReqEntry) * R);
+  if (st != JN_OK) return st;
+  JN_HIP(c, launch_unpack(c->stream, (const ReqEntry*)p->req_table, p->sample_request, p->sample_local,
+                          p->seqlens, p->cu_seqlens, p->N, mreq, rows, (int64_t)row_bytes, vec16),
+         "unpack kernel");
+  return JN_OK;
+}
+
+}  // extern "C"

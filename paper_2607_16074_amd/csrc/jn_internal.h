@@ -1,0 +1,118 @@
+// Internal declarations shared by the host library and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "joynexus.h"
+
+namespace jnx {
+
+// Device request table entry (one per request), written by jn_pack_group and
+// patched by jn_unpack with the output pointer.
+struct ReqEntry {
+  const void* in;      // bf16 [n][max_len][d]
+  void* out;           // unpack destination [n][max_len][row_bytes]
+  int32_t max_len;
+  int32_t n;
+  int32_t first;       // packed index of the request's first sample
+  int32_t reserved;
+};
+static_assert(sizeof(ReqEntry) == 32, "ReqEntry layout");
+
+// ------------------------------------------------------------ launchers ---
+// All launchers enqueue on `s`; shapes were validated by the caller.
+
+hipError_t launch_pack(hipStream_t s, const ReqEntry* req_table, const int32_t* sample_request,
+                       const int32_t* sample_local, const int32_t* seqlens, const int32_t* cu_seqlens,
+                       int32_t N, int32_t d, int32_t align, int32_t max_rows, void* tokens,
+                       int32_t* token_sample, int32_t* token_pos);
+
+hipError_t launch_unpack(hipStream_t s, const ReqEntry* req_table, const int32_t* sample_request,
+                         const int32_t* sample_local, const int32_t* seqlens, const int32_t* cu_seqlens,
+                         int32_t N, int32_t max_req_len, const void* rows, int64_t row_bytes, bool vec16);
+
+// x_out (fp32, optional) = widened x_bf16; h = RMS(x) * g  (bf16)
+hipError_t launch_rmsnorm_bf16in(hipStream_t s, const void* x_bf16, float* x_out, const void* g,
+                                 void* h, int32_t rows, int32_t d, float eps);
+// h = RMS(x) * g (bf16) from the fp32 residual stream
+hipError_t launch_rmsnorm_f32in(hipStream_t s, const float* x, const void* g, void* h, int32_t rows,
+                                int32_t d, float eps);
+
+enum GemmEpi : int32_t {
+  EPI_BF16 = 0,       // C bf16 = acc
+  EPI_GELU_BF16 = 1,  // C bf16 = gelu(acc)
+  EPI_RESID_F32 = 2,  // C fp32 += acc
+  EPI_GEGLU_BF16 = 3  // weights gate|up interleaved at load; C bf16 = gelu(gate) * up
+};
+
+// C[M][N] (+)= epi(A[M][K] * B[N][K]^T); A, B bf16 row-major with leading
+// dims lda, ldb (elements); for EPI_GEGLU_BF16, B is w_gate and B2 is w_up,
+// each [N][K], and C has N columns.
+hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B,
+                       const void* B2, int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N,
+                       int32_t K, int tile_hint);
+
+// Varlen attention over the packed batch (bidirectional inside each sample).
+// qkv: bf16 [T][3d]; out: bf16 [T][d].  Alignment rows of `out` are zeroed.
+hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int32_t* seqlens,
+                            const int32_t* cu_seqlens, int32_t N, int32_t d, int32_t n_heads,
+                            int32_t max_seqlen, int32_t align);
+
+// ---- heads ----
+// pooled[sample_tenant_rank[i]][:] = mean over valid rows of hidden for sample i
+hipError_t launch_pool(hipStream_t s, const void* hidden, const int32_t* seqlens,
+                       const int32_t* cu_seqlens, const int32_t* rank, int32_t N, int32_t d,
+                       float* pooled);
+
+// Grouped fp32 GEMM descriptor for the tenant heads:
+//   C(m,n) = sum_k A(m,k) B(k,n),  A(m,k) = A[m*sam + k*sak],  B(k,n) = B[k*sbk + n*sbn].
+// Tenant-ordered operands are addressed from the tenant's first row: the
+// kernel adds off_g * bump{A,B,C} to the base pointers, with
+// off_g = tenant_sample_off[tenant] read on the device.  The one dimension
+// equal to the tenant's row count n_g (M for forward / data-gradient, K for
+// weight-gradient) is given as -1 and read on the device as well.
+struct HeadGemm {
+  const float* A;
+  const float* B;
+  float* C;
+  const float* bias;  // forward: C(m,n) += bias[n]          (may be null)
+  float* Cact;        // forward: also store gelu(C) (same ldc / bump as C)
+  const float* Zg;    // data-gradient: C *= gelu'(Zg)  (same ldc / bump as C)
+  float* db;          // weight-gradient: db[m] = sum_k A(m,k), by tn == 0 tiles
+  int64_t sam, sak, sbk, sbn, ldc;
+  int64_t bumpA, bumpB, bumpC;
+  int32_t M, N, K;
+  int32_t tenant;
+  int32_t tiles_n;
+  int32_t reserved;
+};
+struct HeadTile {
+  int32_t desc;
+  int32_t tm;
+  int32_t tn;
+  int32_t reserved;
+};
+hipError_t launch_head_gemm(hipStream_t s, const HeadGemm* descs, const HeadTile* tiles, int32_t n_tiles,
+                            const int32_t* tenant_sample_off);
+
+// Per-tenant mean squared error over n_g * out elements:
+//   loss = mean((y - t)^2), dy = 2 (y - t) / (n_g * out), actions = y.
+// y and dy are tenant-ordered ([N][ld], rows from off_g); target and actions
+// are the tenant's own [n_g][out] buffers.
+struct LossDesc {
+  const float* y;
+  const float* target;
+  float* dy;
+  float* loss;
+  float* actions;
+  int32_t out;
+  int64_t ld;
+  int32_t tenant;
+  int32_t reserved;
+};
+hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tenant_sample_off);
+
+}  // namespace jnx

@@ -1,0 +1,148 @@
+"""The group-batched step as four library calls, with caller-owned buffers.
+
+``GroupStep`` holds the device copies of the frozen backbone and of every
+tenant's head, allocates the buffers a given group of requests needs once
+(``prepare``), and then runs
+
+    jn_pack_group -> jn_backbone_forward -> jn_tenant_heads_fwd_bwd -> jn_unpack
+
+on one stream (``run``) with no allocation and no host synchronisation.
+``isolated_runs`` builds one such step per tenant over the same device
+weights: the serial-execution comparator of grouped execution, using the
+same kernels and the same tile rule.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import (Backbone, Context, Head, HeadIO, Request, Tenant, jn_backbone_forward, jn_backbone_workspace_size,
+               jn_heads_workspace_size, jn_pack_group, jn_pack_plan, jn_tenant_heads_fwd_bwd, jn_unpack)
+
+
+def _dev_bf16(bits: np.ndarray, device):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to(device, non_blocking=False).view(torch.bfloat16)
+
+
+def _dev_f32(a: np.ndarray, device):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+
+class Model:
+    """Device weights: frozen backbone + per-tenant heads."""
+
+    def __init__(self, backbone: Backbone, heads: List[Head], tenant_meta: List[dict], prefix_sig: int):
+        self.backbone = backbone
+        self.heads = heads
+        self.tenant_meta = tenant_meta  # action_dim, chunk per tenant
+        self.prefix_sig = prefix_sig
+
+    @classmethod
+    def from_arrays(cls, layers: List[dict], gf: np.ndarray, n_heads: int, eps: float,
+                    heads: List[list], tenant_meta: List[dict], prefix_sig: int, device="cuda"):
+        """``layers``: per layer dict of bf16 bit arrays; ``heads``: per tenant
+        list of (W fp32 [out,in], b fp32 [out])."""
+        dl = [{k: _dev_bf16(v, device) for k, v in L.items()} for L in layers]
+        bb = Backbone(dl, _dev_bf16(gf, device), n_heads, eps)
+        hs = []
+        for g, layers_g in enumerate(heads):
+            W = [_dev_f32(w, device) for w, _ in layers_g]
+            b = [_dev_f32(x, device) for _, x in layers_g]
+            hs.append(Head(W, b, tenant_meta[g]["action_dim"], tenant_meta[g]["chunk"]))
+        return cls(bb, hs, tenant_meta, prefix_sig)
+
+
+class GroupStep:
+    """One group of requests over a subset of tenants, buffers allocated once."""
+
+    def __init__(self, model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
+                 tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda"):
+        import torch
+        self.model = model
+        self.ctx = ctx or Context()
+        self.tenants = list(tenants)              # global tenant ids, table order
+        slot = {g: k for k, g in enumerate(self.tenants)}
+        # requests re-labelled to table slots
+        self.requests = [Request(slot[r.tenant], r.embeds, r.lengths, r.max_len) for r in requests]
+        self.align = align
+        d = model.backbone.d
+        self.table = [Tenant(model.prefix_sig, d) for _ in self.tenants]
+        sz = jn_pack_plan(self.requests, self.table, d, align)
+        self.N, self.T = sz.N, sz.T
+        self.maps = torch.empty(int(sz.map_bytes), dtype=torch.uint8, device=device)
+        self.tokens = torch.empty((self.T, d), dtype=torch.bfloat16, device=device)
+        self.hidden = torch.empty((self.T, d), dtype=torch.bfloat16, device=device)
+        self.bb_ws = torch.empty(jn_backbone_workspace_size(model.backbone, self.T), dtype=torch.uint8, device=device)
+        self.heads = [model.heads[g] for g in self.tenants]
+        self.pooled = torch.empty((self.N, d), dtype=torch.float32, device=device)
+        self.ios = []
+        for k, g in enumerate(self.tenants):
+            h = model.heads[g]
+            n_g = int(sum(r.n for r in self.requests if r.tenant == k))
+            tgt = _dev_f32(targets[g], device)
+            acts = torch.empty((n_g, int(h.dims[-1])), dtype=torch.float32, device=device)
+            loss = torch.empty(1, dtype=torch.float32, device=device)
+            dW = [torch.empty_like(w) for w in h.W]
+            db = [torch.empty_like(x) for x in h.b]
+            self.ios.append(HeadIO(tgt, acts, loss, dW, db))
+        self.out_hidden = [torch.empty((r.n, r.max_len, d), dtype=torch.bfloat16, device=device) for r in self.requests]
+        # pack once to size the head workspace from a real packed batch
+        self.packed = jn_pack_group(self.ctx, self.requests, self.table, d, align, self.maps, self.tokens)
+        self.hd_ws = torch.empty(jn_heads_workspace_size(self.packed, self.heads), dtype=torch.uint8, device=device)
+        self.valid_tokens = int(sum(int(r.lengths.sum()) for r in self.requests))
+
+    # the four calls -------------------------------------------------------
+    def pack(self):
+        d = self.model.backbone.d
+        self.packed = jn_pack_group(self.ctx, self.requests, self.table, d, self.align, self.maps, self.tokens)
+
+    def backbone(self):
+        jn_backbone_forward(self.ctx, self.model.backbone, self.packed, self.hidden, self.bb_ws)
+
+    def heads_fwd_bwd(self):
+        jn_tenant_heads_fwd_bwd(self.ctx, self.packed, self.hidden, self.heads, self.ios, self.hd_ws, self.pooled)
+
+    def unpack(self):
+        d = self.model.backbone.d
+        jn_unpack(self.ctx, self.packed, self.requests, self.hidden, d * 2, self.out_hidden)
+
+    def run(self):
+        self.pack()
+        self.backbone()
+        self.heads_fwd_bwd()
+        self.unpack()
+
+
+def isolated_runs(model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
+                  tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda"):
+    """One ``GroupStep`` per tenant (its own requests only), sharing the weights."""
+    ctx = ctx or Context()
+    out = []
+    for g in tenants:
+        reqs = [r for r in requests if r.tenant == g]
+        out.append(GroupStep(model, reqs, targets, [g], align, ctx, device))
+    return out
+
+
+def from_workload(wl, device="cuda"):
+    """Device model, requests and targets from a workload description.
+
+    ``wl`` needs: ``spec`` (backbone: layers/d/heads/eps; tenants: action_dim,
+    chunk, schema_sig), ``layers``, ``gf``, ``heads``, ``targets`` and
+    ``requests`` (tenant, lengths, embeds bf16 bits, first).
+    """
+    spec = wl.spec
+    meta = [{"action_dim": t.action_dim, "chunk": t.chunk} for t in spec.tenants]
+    model = Model.from_arrays(wl.layers, wl.gf, spec.backbone.heads, spec.backbone.eps, wl.heads, meta,
+                              spec.tenants[0].schema_sig, device)
+    reqs = [Request(r.tenant, _dev_bf16(r.embeds, device), r.lengths) for r in wl.requests]
+    targets = {}
+    for g in range(spec.G):
+        idx = [k for r in wl.requests if r.tenant == g for k in range(r.first, r.first + r.n)]
+        t = np.asarray(wl.targets[g], np.float32)[np.array(idx, dtype=np.int64)]
+        targets[g] = t.reshape(len(idx), -1)
+    return model, reqs, targets
