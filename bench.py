@@ -1,0 +1,201 @@
+"""Benchmark of the group-batched step on one MI355X.
+
+A step = jn_pack_group -> jn_backbone_forward -> jn_tenant_heads_fwd_bwd ->
+jn_unpack over one group of requests with inputs resident in HBM.  Default
+workload: 8 tenants x 32 samples on an 18-layer d2048 GeGLU (2B-shaped)
+backbone with per-tenant 3-layer MLP heads (seeded synthetic inputs).
+
+Reported in one JSON line: grouped samples/s (value), backbone tokens/s,
+isolated per-tenant execution (the same calls once per tenant, same kernels
+and tile rule) and the speedup over it, the GEMM roofline of the dominant
+kernel measured with HIP events on the library stream, and the fp64 CPU
+oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "grouped samples/s + backbone tokens/s at 1 GPU; speedup vs isolated; % MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def gemm_flops_per_token(bb) -> dict:
+    d, f = bb.d, bb.ffn
+    up = 2 * (2 * f if bb.glu else f) * d
+    return {"gemm_qkv": 2 * 3 * d * d, "gemm_o": 2 * d * d, "gemm_up": up, "gemm_down": 2 * f * d}
+
+
+def time_steps(steps, fn, ctx, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ctx.set_trace(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    trace = ctx.trace_read()
+    ctx.set_trace(False)
+    return (t1 - t0) / steps, trace
+
+
+def cpu_oracle_baseline(wl, budget_s=25.0):
+    """The fp64 oracle on a bounded sample: one sample's full backbone plus
+    its tenant's head step; reported as oracle samples/s."""
+    import oracle
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    req = wl.requests[0]
+    key = (0, 0)
+    t0 = time.perf_counter()
+    res = oracle.step.isolated(wl, samples=[key], heads=False)
+    n0 = wl.spec.tenants[req.tenant].n_samples
+    P = np.repeat(res["pooled"][key][None, :], n0, axis=0)
+    oracle.step.tenant_from_pooled(wl, req.tenant, P)
+    dt = time.perf_counter() - t0
+    L = int(req.lengths[0])
+    return {"value": 1.0 / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 of {sum(q.n for q in wl.requests)} samples ({L} tokens): full backbone forward in fp64 "
+                      f"+ its tenant's head fwd/loss/grad over {n0} rows; {dt:.1f} s on the host",
+            "seconds": dt, "host_cpus": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--align", type=int, default=1)
+    ap.add_argument("--no-isolated", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="print per-kernel time shares to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the step is sharded by "
+              f"whole tenants across GPUs with no collective on the forward; run one process per GPU).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from paper_2607_16074_amd import step as jstep
+
+    t0 = time.perf_counter()
+    wl = W.make_workload(args.config)
+    spec = wl.spec
+    log(f"workload cfg{args.config} drawn in {time.perf_counter() - t0:.1f}s: {spec.name}")
+    model, reqs, targets = jstep.from_workload(wl, "cuda")
+    G = spec.G
+    grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align)
+    torch.cuda.synchronize()
+    N, valid = grouped.N, grouped.valid_tokens
+    log(f"N={N} samples, {valid} valid tokens, T={grouped.T} packed rows")
+
+    t_step, trace = time_steps(args.steps, grouped.run, grouped.ctx, args.warmup)
+    log(f"grouped: {t_step * 1e3:.2f} ms/step")
+
+    # per-kernel-class time from the trace
+    by_op = {}
+    for op, M, Nn, K, ms in trace:
+        e = by_op.setdefault(op, {"ms": 0.0, "launches": 0})
+        e["ms"] += ms
+        e["launches"] += 1
+    bb_ms = sum(v["ms"] for k, v in by_op.items() if k in ("rmsnorm", "gemm_qkv", "attention", "gemm_o",
+                                                          "gemm_up", "gemm_down")) / args.steps
+    fpt = gemm_flops_per_token(spec.backbone)
+    gemm_stats = {}
+    for op, per_tok in fpt.items():
+        if op in by_op:
+            avg = by_op[op]["ms"] / by_op[op]["launches"]
+            flops = per_tok * valid
+            gemm_stats[op] = {"avg_ms": avg, "tflops": flops / (avg * 1e-3) / 1e12,
+                              "launches_per_step": by_op[op]["launches"] // args.steps}
+    dom = max(gemm_stats, key=lambda k: gemm_stats[k]["avg_ms"] * gemm_stats[k]["launches_per_step"])
+    gemm_total_ms = sum(by_op[k]["ms"] for k in fpt if k in by_op) / args.steps
+    gemm_total_flops = sum(fpt[k] * valid * gemm_stats[k]["launches_per_step"] for k in gemm_stats)
+    gemm_tflops = gemm_total_flops / (gemm_total_ms * 1e-3) / 1e12
+    if args.breakdown:
+        tot = sum(v["ms"] for v in by_op.values())
+        for k, v in sorted(by_op.items(), key=lambda kv: -kv[1]["ms"]):
+            log(f"  {k:10s} {v['ms'] / args.steps:9.3f} ms/step  {100 * v['ms'] / tot:5.1f}%  "
+                f"launches/step {v['launches'] // args.steps}")
+        for k, v in gemm_stats.items():
+            log(f"  {k:10s} {v['avg_ms']:.3f} ms/launch  {v['tflops']:.0f} TFLOP/s")
+
+    iso_ms = None
+    if not args.no_isolated:
+        iso = jstep.isolated_runs(model, reqs, targets, list(range(G)), args.align, ctx=grouped.ctx)
+        torch.cuda.synchronize()
+
+        def run_iso():
+            for s in iso:
+                s.run()
+        t_iso, _ = time_steps(args.steps, run_iso, grouped.ctx, args.warmup)
+        iso_ms = t_iso * 1e3
+        log(f"isolated: {iso_ms:.2f} ms/step")
+        del iso
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_oracle_baseline(wl)
+        log(f"cpu oracle: {cpu['value']:.4f} samples/s on {cpu['cores']} threads")
+
+    gs = gemm_stats[dom]
+    result = {
+        "metric": METRIC,
+        "value": N / t_step,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"config {args.config}: {spec.name}; per-tenant MLP heads, seed {spec.seed}",
+                   "tenants": G, "samples": N, "valid_tokens": valid, "packed_rows": grouped.T,
+                   "align": args.align},
+        "backbone_tokens_per_s": valid / (bb_ms * 1e-3),
+        "backbone_ms": bb_ms,
+        "isolated_samples_per_s": (N / (iso_ms * 1e-3)) if iso_ms else None,
+        "isolated_ms_per_step": iso_ms,
+        "speedup_vs_isolated": (iso_ms / (t_step * 1e3)) if iso_ms else None,
+        "backbone_gemm_tflops": gemm_tflops,
+        "backbone_gemm_frac_of_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": f"gemm_kernel ({dom}, {spec.backbone.d}-wide)",
+                     "achieved": gs["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},
+        "gemm_by_op": gemm_stats,
+        "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample")},
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -64,6 +64,33 @@ jn_status jn_ctx_set_stream(jn_ctx* ctx, void* hip_stream);
 /* Message for the last non-OK status returned on this context ("" if none). */
 const char* jn_last_error(const jn_ctx* ctx);
 
+/* ------------------------------------------------------- measurement --- */
+
+/* Kernel classes reported by the launch trace. */
+typedef enum jn_op {
+  JN_OP_PACK = 1, JN_OP_RMSNORM = 2, JN_OP_GEMM_QKV = 3, JN_OP_ATTENTION = 4, JN_OP_GEMM_O = 5,
+  JN_OP_GEMM_UP = 6, JN_OP_GEMM_DOWN = 7, JN_OP_POOL = 8, JN_OP_HEAD_FWD = 9, JN_OP_LOSS = 10,
+  JN_OP_HEAD_BWD = 11, JN_OP_UNPACK = 12
+} jn_op;
+
+/* One traced kernel launch.  For GEMMs (M, N, K) is the launch shape
+ * (N counts gate and up rows for GeGLU); for the other kernels M is the
+ * number of rows touched and N the row width. */
+typedef struct jn_trace_entry {
+  int32_t op, M, N, K;
+  float ms;               /* device time between the bracketing events */
+  int32_t reserved;
+} jn_trace_entry;
+
+/* Enable (1) or disable (0) the launch trace: while enabled, every kernel the
+ * context enqueues is bracketed by a pair of HIP timing events on its stream.
+ * Enabling clears previously collected entries. */
+jn_status jn_ctx_set_trace(jn_ctx* ctx, int32_t enable);
+/* Wait for the traced launches to finish and copy up to `cap` entries (in
+ * launch order) to `out`; `*n` receives the number collected.  Clears the
+ * trace.  Synchronizes with the context stream. */
+jn_status jn_ctx_trace_read(jn_ctx* ctx, jn_trace_entry* out, int32_t cap, int32_t* n);
+
 /* ---------------------------------------------------------------- pack --- */
 
 /* One inference / training request of one tenant (App. A.3: a request carries

@@ -62,6 +62,17 @@ class Context:
         _check(_lib.jn_ctx_create(C.byref(h), C.c_void_p(stream.cuda_stream)), what="jn_ctx_create")
         self.handle = h
 
+    def set_trace(self, enable: bool):
+        """Bracket every kernel this context launches with timing events."""
+        _check(_lib.jn_ctx_set_trace(self.handle, 1 if enable else 0), self)
+
+    def trace_read(self, cap: int = 1 << 16) -> list:
+        """[(op name, M, N, K, ms)] of the traced launches, in launch order."""
+        buf = (_abi.jn_trace_entry * cap)()
+        n = C.c_int32()
+        _check(_lib.jn_ctx_trace_read(self.handle, buf, cap, C.byref(n)), self)
+        return [(_abi.OPS.get(e.op, str(e.op)), e.M, e.N, e.K, e.ms) for e in buf[: n.value]]
+
     def close(self):
         if self.handle:
             _lib.jn_ctx_destroy(self.handle)

@@ -17,11 +17,21 @@ STATUS_NAMES = {0: "JN_OK", 1: "JN_EINVAL", 2: "JN_EINCOMPAT", 3: "JN_ESHAPE", 4
                 5: "JN_EHIP", 6: "JN_EUNSUPPORTED"}
 
 EXPORTS = (
-    "jn_ctx_create", "jn_ctx_destroy", "jn_ctx_set_stream", "jn_last_error",
+    "jn_ctx_create", "jn_ctx_destroy", "jn_ctx_set_stream", "jn_last_error", "jn_ctx_set_trace",
+    "jn_ctx_trace_read",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group",
     "jn_backbone_workspace_size", "jn_backbone_forward",
     "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
 )
+
+
+OPS = {1: "pack", 2: "rmsnorm", 3: "gemm_qkv", 4: "attention", 5: "gemm_o", 6: "gemm_up", 7: "gemm_down",
+       8: "pool", 9: "head_fwd", 10: "loss", 11: "head_bwd", 12: "unpack"}
+
+
+class jn_trace_entry(C.Structure):
+    _fields_ = [("op", C.c_int32), ("M", C.c_int32), ("N", C.c_int32), ("K", C.c_int32), ("ms", C.c_float),
+                ("reserved", C.c_int32)]
 
 
 class jn_request(C.Structure):
@@ -99,6 +109,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "jn_ctx_destroy": (None, [V]),
         "jn_ctx_set_stream": (C.c_int, [V, V]),
         "jn_last_error": (C.c_char_p, [V]),
+        "jn_ctx_set_trace": (C.c_int, [V, C.c_int32]),
+        "jn_ctx_trace_read": (C.c_int, [V, P(jn_trace_entry), C.c_int32, P(C.c_int32)]),
         "jn_pack_plan": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
                                    P(jn_pack_sizes)]),
         "jn_pack_maps_host": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),

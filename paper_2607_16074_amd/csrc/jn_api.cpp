@@ -26,12 +26,25 @@ struct StageSlot {
 };
 }  // namespace
 
+namespace {
+struct TraceRec {
+  int32_t op, M, N, K;
+  hipEvent_t start, stop;
+};
+}  // namespace
+
 struct jn_ctx {
   hipStream_t stream = nullptr;
   int device = 0;
   std::string err;
   StageSlot slots[kSlots];
   int next = 0;
+  // launch trace (measurement only): a pair of timing events around every
+  // kernel launch while enabled
+  bool trace = false;
+  std::vector<TraceRec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t pool_used = 0;
 };
 
 namespace {
@@ -57,6 +70,34 @@ jn_status hip_fail(jn_ctx* c, hipError_t e, const char* what) {
   } while (0)
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+hipEvent_t trace_event(jn_ctx* c) {
+  if (c->pool_used == c->pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->pool.push_back(e);
+  }
+  return c->pool[c->pool_used++];
+}
+
+// Enqueue one kernel launch; with tracing on, bracket it with timing events.
+template <typename F>
+hipError_t traced(jn_ctx* c, int32_t op, int64_t M, int64_t N, int64_t K, F&& launch) {
+  if (!c->trace) return launch();
+  hipEvent_t a = trace_event(c), b = trace_event(c);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, c->stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, c->stream);
+  if (e != hipSuccess) return e;
+  c->recs.push_back(TraceRec{op, (int32_t)M, (int32_t)N, (int32_t)K, a, b});
+  return hipSuccess;
+}
+
+#define JN_TRACED(ctx, op, M, N, K, call, what) \
+  JN_HIP(ctx, traced(ctx, op, M, N, K, [&]() { return (call); }), what)
 
 // Stage `bytes` of host data in pinned memory and copy it to `dst` on the
 // context stream.  Slots are reused round-robin; a slot is rewritten only
@@ -274,6 +315,8 @@ void jn_ctx_destroy(jn_ctx* c) {
     if (s.host) hipHostFree(s.host);
     if (s.ev) hipEventDestroy(s.ev);
   }
+  if (!c->recs.empty()) hipEventSynchronize(c->recs.back().stop);
+  for (hipEvent_t e : c->pool) hipEventDestroy(e);
   delete c;
 }
 
@@ -284,6 +327,32 @@ jn_status jn_ctx_set_stream(jn_ctx* c, void* hip_stream) {
 }
 
 const char* jn_last_error(const jn_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+jn_status jn_ctx_set_trace(jn_ctx* c, int32_t enable) {
+  if (!c) return JN_EINVAL;
+  c->trace = enable != 0;
+  c->recs.clear();
+  c->pool_used = 0;
+  return JN_OK;
+}
+
+jn_status jn_ctx_trace_read(jn_ctx* c, jn_trace_entry* out, int32_t cap, int32_t* n) {
+  if (!c || !n || (cap > 0 && !out)) return JN_EINVAL;
+  *n = 0;
+  if (!c->recs.empty()) JN_HIP(c, hipEventSynchronize(c->recs.back().stop), "hipEventSynchronize(trace)");
+  int32_t k = 0;
+  for (const TraceRec& r : c->recs) {
+    if (k >= cap) break;
+    float ms = 0.f;
+    JN_HIP(c, hipEventElapsedTime(&ms, r.start, r.stop), "hipEventElapsedTime");
+    out[k] = jn_trace_entry{r.op, r.M, r.N, r.K, ms, 0};
+    ++k;
+  }
+  *n = k;
+  c->recs.clear();
+  c->pool_used = 0;
+  return JN_OK;
+}
 
 jn_status jn_pack_plan(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
                        const jn_pack_opts* o, jn_pack_sizes* out) {
@@ -356,10 +425,11 @@ jn_status jn_pack_group(jn_ctx* c, const jn_request* req, int32_t R, const jn_te
   jn_packed tmp;
   fill_packed(&tmp, base, m, p, R, G, o);
   tmp.tokens = tokens;
-  JN_HIP(c, launch_pack(c->stream, (const ReqEntry*)tmp.req_table, tmp.sample_request, tmp.sample_local,
+  JN_TRACED(c, JN_OP_PACK, p.T, o->d_model, 0,
+            launch_pack(c->stream, (const ReqEntry*)tmp.req_table, tmp.sample_request, tmp.sample_local,
                         tmp.seqlens, tmp.cu_seqlens, p.N, o->d_model, o->align, p.max_rows, tokens,
                         tmp.token_sample, tmp.token_pos),
-         "pack kernel");
+            "pack kernel");
   *out = tmp;
   return JN_OK;
 }
@@ -447,22 +517,28 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
   for (int l = 0; l < bb->n_layers; ++l) {
     const jn_layer& Ly = bb->layers[l];
     if (l == 0)
-      JN_HIP(c, launch_rmsnorm_bf16in(s, p->tokens, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
+      JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_bf16in(s, p->tokens, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
     else
-      JN_HIP(c, launch_rmsnorm_f32in(s, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
-    JN_HIP(c, launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0), "gemm qkv");
-    JN_HIP(c, launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, p->max_seqlen,
+      JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
+    JN_TRACED(c, JN_OP_GEMM_QKV, T, 3 * d, d,
+              launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0), "gemm qkv");
+    JN_TRACED(c, JN_OP_ATTENTION, T, d, bb->n_heads,
+              launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, p->max_seqlen,
                                p->align),
-           "attention");
-    JN_HIP(c, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0), "gemm o");
-    JN_HIP(c, launch_rmsnorm_f32in(s, x, Ly.g2, h, T, d, bb->eps), "rmsnorm");
+              "attention");
+    JN_TRACED(c, JN_OP_GEMM_O, T, d, d, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0),
+              "gemm o");
+    JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, Ly.g2, h, T, d, bb->eps), "rmsnorm");
     if (glu)
-      JN_HIP(c, launch_gemm(s, EPI_GEGLU_BF16, h, d, Ly.w_gate, Ly.w_up, d, mid, f, T, f, d, 0), "gemm geglu");
+      JN_TRACED(c, JN_OP_GEMM_UP, T, 2 * f, d,
+                launch_gemm(s, EPI_GEGLU_BF16, h, d, Ly.w_gate, Ly.w_up, d, mid, f, T, f, d, 0), "gemm geglu");
     else
-      JN_HIP(c, launch_gemm(s, EPI_GELU_BF16, h, d, Ly.w_up, nullptr, d, mid, f, T, f, d, 0), "gemm up");
-    JN_HIP(c, launch_gemm(s, EPI_RESID_F32, mid, f, Ly.w_down, nullptr, f, x, d, T, d, f, 0), "gemm down");
+      JN_TRACED(c, JN_OP_GEMM_UP, T, f, d, launch_gemm(s, EPI_GELU_BF16, h, d, Ly.w_up, nullptr, d, mid, f, T, f, d, 0),
+                "gemm up");
+    JN_TRACED(c, JN_OP_GEMM_DOWN, T, d, f,
+              launch_gemm(s, EPI_RESID_F32, mid, f, Ly.w_down, nullptr, f, x, d, T, d, f, 0), "gemm down");
   }
-  JN_HIP(c, launch_rmsnorm_f32in(s, x, bb->gf, hidden, T, d, bb->eps), "final rmsnorm");
+  JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, bb->gf, hidden, T, d, bb->eps), "final rmsnorm");
   return JN_OK;
 }
 
@@ -712,12 +788,17 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hid
   const HeadTile* dt = (const HeadTile*)(w + hp.tiles);
   hipStream_t s = c->stream;
 
-  JN_HIP(c, launch_pool(s, hidden, p->seqlens, p->cu_seqlens, p->sample_tenant_rank, p->N, p->d, P), "pool");
+  JN_TRACED(c, JN_OP_POOL, p->T, p->d, p->N,
+            launch_pool(s, hidden, p->seqlens, p->cu_seqlens, p->sample_tenant_rank, p->N, p->d, P), "pool");
   for (auto& r : fwd_rng)
-    if (r.second) JN_HIP(c, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off), "head fwd");
-  JN_HIP(c, launch_mse(s, dl, G, p->tenant_sample_off), "loss");
+    if (r.second)
+      JN_TRACED(c, JN_OP_HEAD_FWD, r.second, 0, 0, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off),
+                "head fwd");
+  JN_TRACED(c, JN_OP_LOSS, G, 0, 0, launch_mse(s, dl, G, p->tenant_sample_off), "loss");
   for (auto& r : bwd_rng)
-    if (r.second) JN_HIP(c, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off), "head bwd");
+    if (r.second)
+      JN_TRACED(c, JN_OP_HEAD_BWD, r.second, 0, 0, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off),
+                "head bwd");
   return JN_OK;
 }
 
@@ -747,7 +828,7 @@ jn_status jn_unpack(jn_ctx* c, const jn_packed* p, const jn_request* req, int32_
   if (n != p->N) return fail(c, JN_ESHAPE, "requests hold %lld samples, packed batch %d", (long long)n, p->N);
   jn_status st = stage_copy(c, p->req_table, rt.data(), sizeof(ReqEntry) * R);
   if (st != JN_OK) return st;
-  JN_HIP(c, launch_unpack(c->stream, (const ReqEntry*)p->req_table, p->sample_request, p->sample_local,
+  JN_TRACED(c, JN_OP_UNPACK, p->T, (int64_t)row_bytes, 0, launch_unpack(c->stream, (const ReqEntry*)p->req_table, p->sample_request, p->sample_local,
                           p->seqlens, p->cu_seqlens, p->N, mreq, rows, (int64_t)row_bytes, vec16),
          "unpack kernel");
   return JN_OK;

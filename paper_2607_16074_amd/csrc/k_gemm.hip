@@ -6,11 +6,20 @@
 // x tokens); each wavefront accumulates (BN/2) x (BM/2) with
 // v_mfma_f32_32x32x16_bf16.  The weight tile is the MFMA "A" operand, the
 // token tile the "B" operand, so each lane ends with 4 consecutive output
-// columns of one token row -- the epilogue writes 8-byte (bf16) / 16-byte
-// (fp32) vectors along the row-major output.  K advances 64 at a time through
-// double-buffered LDS (rows padded to 144 B: conflict-free 16-byte reads);
-// the next K slab is fetched from global memory into registers while the
-// current one feeds the MFMAs.  One barrier per K slab.
+// columns of one token row and the epilogue writes 8-byte (bf16) / 16-byte
+// (fp32) vectors along the row-major output.
+//
+// Operand staging: global_load_lds_dwordx4 moves 16-byte chunks straight from
+// global memory into LDS (no register staging).  K advances 32 per stage
+// through a 4-stage ring, so a slab is requested three stages before the
+// matrix cores read it.  An LDS row holds 32 bf16 (64 B, four 16-byte
+// chunks); chunk c of row r sits at position c ^ swz(r),
+// swz(r) = ((r >> 1) ^ (r >> 3)) & 3, which keeps every 8- and 16-lane
+// phase of the 16-byte fragment reads on distinct banks.  Each DMA
+// instruction fills 1 KB = 16 rows; the lane -> source-chunk assignment
+// applies the swizzle.  Fragments of the next stage are read from LDS while
+// the second half of the current stage runs on the matrix cores.  One
+// barrier per stage.
 //
 // Launch order: workgroups are dealt round-robin to the 8 XCDs; the tile id
 // is remapped so that each XCD owns one contiguous range of tiles, walked in
@@ -18,9 +27,9 @@
 // activation panels in that XCD's L2.
 //
 // Epilogues: bf16 store, GELU -> bf16, fp32 residual add (in place), and
-// GeGLU, whose gate and up weights are interleaved in 32-row blocks while the
-// weight tile is loaded, so the gate and up accumulators of an output column
-// land in the same lane.
+// GeGLU, whose gate and up weight rows are interleaved in 32-row blocks as
+// they are loaded, so the gate and up accumulators of an output column land
+// in the same lane.
 #include "jn_device.h"
 #include "jn_internal.h"
 
@@ -29,29 +38,61 @@ namespace jnx {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kBK = 64;         // K slab
-constexpr int kLDK = kBK + 8;   // LDS row pitch (elements): 144 B
-constexpr int kGroupM = 8;      // token tiles per L2 group
+#define JN_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
+#define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-template <int BN, int BM, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_kernel(const uint16_t* __restrict__ X, int64_t ldx,
-                                                      const uint16_t* __restrict__ W,
-                                                      const uint16_t* __restrict__ W2, int64_t ldw,
-                                                      void* __restrict__ C, int64_t ldc, int32_t M, int32_t N,
-                                                      int32_t K, int32_t tiles_m, int32_t tiles_n) {
+constexpr int kBK = 32;       // K per stage
+constexpr int kStages = 4;    // ring depth
+constexpr int kGroupM = 8;    // token tiles per L2 group
+
+__device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int T>
+__device__ __forceinline__ void gemm_frags(bf16x8 (&f)[T], const uint16_t* stage, int row0, int pos) {
+#pragma unroll
+  for (int i = 0; i < T; ++i) f[i] = *reinterpret_cast<const bf16x8*>(stage + (row0 + i * 32) * kBK + pos * 8);
+}
+
+template <int TN, int TM>
+__device__ __forceinline__ void gemm_mfma(f32x16 (&acc)[TN][TM], const bf16x8 (&fw)[TN], const bf16x8 (&fx)[TM]) {
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+}
+
+template <int BN, int BM, int WGN, int WGM, int EPI>
+__global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(const uint16_t* __restrict__ X, int64_t ldx,
+                                                                 const uint16_t* __restrict__ W,
+                                                                 const uint16_t* __restrict__ W2, int64_t ldw,
+                                                                 void* __restrict__ C, int64_t ldc, int32_t M,
+                                                                 int32_t N, int32_t K, int32_t tiles_m,
+                                                                 int32_t tiles_n) {
   constexpr bool GLU = EPI == EPI_GEGLU_BF16;
-  constexpr int WN = BN / 2, WM = BM / 2;  // per-wave tile
+  constexpr int NW = WGN * WGM;              // wavefronts
+  constexpr int WN = BN / WGN, WM = BM / WGM;  // per-wave tile
   constexpr int TN = WN / 32, TM = WM / 32;
-  constexpr int RW = BN / 32, RX = BM / 32;  // 16-byte chunks per thread per slab
-  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN][kLDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Xs[2][BM][kLDK];
+  constexpr int ROWS = BN + BM;              // weight rows then token rows in a stage
+  constexpr int NI = ROWS / (16 * NW);       // 1 KB DMA instructions per wave per stage
+  constexpr int STAGE = ROWS * kBK;          // elements per stage
+  static_assert(ROWS % (16 * NW) == 0 && TN >= 1 && TM >= 1, "tile shape");
+  static_assert(!GLU || TN % 2 == 0, "GeGLU pairs gate/up tiles inside a wave");
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * STAGE];
 
   // ---- XCD-aware tile order
   const int32_t ntiles = tiles_m * tiles_n;
   const int32_t b = blockIdx.x;
   const int32_t xcd = b & 7, local = b >> 3;
-  const int32_t q = ntiles >> 3, r = ntiles & 7;
-  const int32_t pid = xcd * q + min(xcd, r) + local;
+  const int32_t q8 = ntiles >> 3, r8 = ntiles & 7;
+  const int32_t pid = xcd * q8 + min(xcd, r8) + local;
   const int32_t per_group = kGroupM * tiles_n;
   const int32_t group = pid / per_group;
   const int32_t first_m = group * kGroupM;
@@ -59,44 +100,30 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const uint16_t* __restrict
   const int32_t tm = first_m + (pid % per_group) % gsize;
   const int32_t tn = (pid % per_group) / gsize;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wn = wave >> 1, wm = wave & 1;
-  const int lrow = tid >> 3;        // 0..31: row within a 32-row band for loads
-  const int lchunk = (tid & 7) * 8; // element offset of this thread's 16-byte chunk
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wn = wave / WGM, wm = wave % WGM;
 
-  // ---- global row sources (clamped into range: ragged tiles load valid rows)
-  const int32_t NL = GLU ? 2 * N : N;  // rows of the (interleaved) weight operand
-  const uint16_t* wsrc[RW];
+  // ---- DMA sources: this wave's instruction i fills stage rows 16*(wave*NI+i) ..
+  // +15; lane -> (row, chunk) with the swizzle applied to the source chunk.
+  const int32_t NL = GLU ? 2 * N : N;
+  const uint16_t* src[NI];
 #pragma unroll
-  for (int i = 0; i < RW; ++i) {
-    if constexpr (GLU) {
-      int32_t col = tn * (BN / 2) + (i >> 1) * 32 + lrow;
-      col = min(col, N - 1);
-      wsrc[i] = ((i & 1) ? W2 : W) + (int64_t)col * ldw + lchunk;
+  for (int i = 0; i < NI; ++i) {
+    const int row = 16 * (wave * NI + i) + (lane >> 2);
+    const int chunk = (lane & 3) ^ lds_swz(row);
+    if (row < BN) {
+      if constexpr (GLU) {
+        const int32_t col = min(tn * (BN / 2) + (row >> 6) * 32 + (row & 31), N - 1);
+        src[i] = (((row >> 5) & 1) ? W2 : W) + (int64_t)col * ldw + chunk * 8;
+      } else {
+        src[i] = W + (int64_t)min(tn * BN + row, NL - 1) * ldw + chunk * 8;
+      }
     } else {
-      int32_t row = min(tn * BN + i * 32 + lrow, NL - 1);
-      wsrc[i] = W + (int64_t)row * ldw + lchunk;
+      src[i] = X + (int64_t)min(tm * BM + row - BN, M - 1) * ldx + chunk * 8;
     }
   }
-  const int32_t xrow0 = tm * BM + lrow;
-
-  uint4 rw[RW], rx[RX];
-  auto load_slab = [&](int32_t k0) {
-#pragma unroll
-    for (int i = 0; i < RW; ++i) rw[i] = *reinterpret_cast<const uint4*>(wsrc[i] + k0);
-#pragma unroll
-    for (int i = 0; i < RX; ++i) {
-      const int32_t row = min(xrow0 + i * 32, M - 1);
-      rx[i] = *reinterpret_cast<const uint4*>(X + (int64_t)row * ldx + k0 + lchunk);
-    }
-  };
-  auto store_slab = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < RW; ++i) *reinterpret_cast<uint4*>(&Ws[buf][i * 32 + lrow][lchunk]) = rw[i];
-#pragma unroll
-    for (int i = 0; i < RX; ++i) *reinterpret_cast<uint4*>(&Xs[buf][i * 32 + lrow][lchunk]) = rx[i];
-  };
+  uint16_t* const dst0 = lds + wave * NI * 512;  // 512 elements = 1 KB per instruction
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -107,32 +134,55 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const uint16_t* __restrict
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int KT = K / kBK;
-  load_slab(0);
-  store_slab(0);
-  __syncthreads();
-  const int frow = lane & 31;
-  const int fk = (lane >> 5) * 8;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) load_slab((kt + 1) * kBK);
+  // fragment read positions: logical chunk 2*kk + (lane >> 5), swizzled by row
+  const int sw = lds_swz(lane & 31);
+  const int pos0 = (lane >> 5) ^ sw, pos1 = pos0 ^ 2;
+  const int wrow = wn * WN + (lane & 31), xrow = BN + wm * WM + (lane & 31);
+
+  // prologue: slabs 0 .. kStages-2 in flight
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      bf16x8 fw[TN], fx[TM];
+  for (int st = 0; st < kStages - 1; ++st) {
+    if (st < KT) {
 #pragma unroll
-      for (int i = 0; i < TN; ++i)
-        fw[i] = *reinterpret_cast<const bf16x8*>(&Ws[cur][wn * WN + i * 32 + frow][kk * 16 + fk]);
-#pragma unroll
-      for (int j = 0; j < TM; ++j)
-        fx[j] = *reinterpret_cast<const bf16x8*>(&Xs[cur][wm * WM + j * 32 + frow][kk * 16 + fk]);
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + st * kBK), JN_LPTR(dst0 + st * STAGE + i * 512), 16, 0, 0);
     }
-    if (kt + 1 < KT) store_slab(cur ^ 1);
-    __syncthreads();
   }
+  bf16x8 fw0[TN], fx0[TM], fw1[TN], fx1[TM];
+  if (KT > kStages - 2) wait_vmcnt<(kStages - 2) * NI>(); else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  gemm_frags<TN>(fw0, lds, wrow, pos0);
+  gemm_frags<TM>(fx0, lds, xrow, pos0);
+  gemm_frags<TN>(fw1, lds, wrow, pos1);
+  gemm_frags<TM>(fx1, lds, xrow, pos1);
+
+  for (int kt = 0; kt < KT - 1; ++kt) {
+    gemm_mfma<TN, TM>(acc, fw0, fx0);
+    __builtin_amdgcn_sched_barrier(0);
+    // slab kt+1 has landed for every wave; every wave is past its reads of
+    // the buffer that slab kt+kStages-1 refills
+    const bool refill = kt + kStages - 1 < KT;
+    if (refill) wait_vmcnt<(kStages - 3) * NI>(); else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (refill) {
+      const int st = (kt + kStages - 1) % kStages;
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + kStages - 1) * kBK),
+                                         JN_LPTR(dst0 + st * STAGE + i * 512), 16, 0, 0);
+    }
+    const uint16_t* nxt = lds + ((kt + 1) % kStages) * STAGE;
+    gemm_frags<TN>(fw0, nxt, wrow, pos0);
+    gemm_frags<TM>(fx0, nxt, xrow, pos0);
+    __builtin_amdgcn_sched_barrier(0);
+    gemm_mfma<TN, TM>(acc, fw1, fx1);
+    __builtin_amdgcn_sched_barrier(0);
+    gemm_frags<TN>(fw1, nxt, wrow, pos1);
+    gemm_frags<TM>(fx1, nxt, xrow, pos1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  gemm_mfma<TN, TM>(acc, fw0, fx0);
+  gemm_mfma<TN, TM>(acc, fw1, fx1);
 
   // ---- epilogue: lane owns output columns n..n+3 of token row m
   const int hi4 = (lane >> 5) * 4;
@@ -186,31 +236,29 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const uint16_t* __restrict
   }
 }
 
-template <int BN, int BM>
+template <int BN, int BM, int WGN, int WGM>
 static hipError_t launch_tile(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2,
                               int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K) {
   const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * N : N;
   const int32_t tiles_m = (M + BM - 1) / BM, tiles_n = (NL + BN - 1) / BN;
-  dim3 grid(tiles_m * tiles_n);
+  dim3 grid(tiles_m * tiles_n), block(64 * WGN * WGM);
   auto X = reinterpret_cast<const uint16_t*>(A);
   auto Wp = reinterpret_cast<const uint16_t*>(B);
   auto W2 = reinterpret_cast<const uint16_t*>(B2);
+#define JN_GEMM_CASE(E)                                                                                  \
+  case E:                                                                                                \
+    gemm_kernel<BN, BM, WGN, WGM, E><<<grid, block, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, \
+                                                            tiles_n);                                    \
+    break;
   switch (epi) {
-    case EPI_BF16:
-      gemm_kernel<BN, BM, EPI_BF16><<<grid, 256, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, tiles_n);
-      break;
-    case EPI_GELU_BF16:
-      gemm_kernel<BN, BM, EPI_GELU_BF16><<<grid, 256, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, tiles_n);
-      break;
-    case EPI_RESID_F32:
-      gemm_kernel<BN, BM, EPI_RESID_F32><<<grid, 256, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, tiles_n);
-      break;
-    case EPI_GEGLU_BF16:
-      gemm_kernel<BN, BM, EPI_GEGLU_BF16><<<grid, 256, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, tiles_n);
-      break;
+    JN_GEMM_CASE(EPI_BF16)
+    JN_GEMM_CASE(EPI_GELU_BF16)
+    JN_GEMM_CASE(EPI_RESID_F32)
+    JN_GEMM_CASE(EPI_GEGLU_BF16)
     default:
       return hipErrorInvalidValue;
   }
+#undef JN_GEMM_CASE
   return hipGetLastError();
 }
 
@@ -239,9 +287,9 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
   if (M <= 0 || N <= 0 || K <= 0 || K % kBK != 0 || N % 32 != 0) return hipErrorInvalidValue;
   const int t = tile_hint > 0 ? tile_hint - 1 : gemm_pick_tile(epi, M, N);
   switch (t) {
-    case 0: return launch_tile<256, 256>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
-    case 1: return launch_tile<256, 128>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
-    default: return launch_tile<128, 128>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
+    case 0: return launch_tile<256, 256, 2, 4>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
+    case 1: return launch_tile<256, 128, 4, 2>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
+    default: return launch_tile<128, 128, 2, 2>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
   }
 }
 
