@@ -10,7 +10,8 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libjoynexus.so")
+# the in-tree build; JN_LIB_PATH selects another build of the same sources
+LIB_PATH = os.environ.get("JN_LIB_PATH") or os.path.join(_HERE, "libjoynexus.so")
 
 JN_OK, JN_EINVAL, JN_EINCOMPAT, JN_ESHAPE, JN_ENOSPACE, JN_EHIP, JN_EUNSUPPORTED = range(7)
 STATUS_NAMES = {0: "JN_OK", 1: "JN_EINVAL", 2: "JN_EINCOMPAT", 3: "JN_ESHAPE", 4: "JN_ENOSPACE",

@@ -36,6 +36,14 @@ __device__ __forceinline__ float gelu_f(float u) {
   return 0.5f * u * (1.0f + tanhf(c * (u + 0.044715f * u * u * u)));
 }
 
+// The same tanh-form GELU written as u * sigmoid(2 sqrt(2/pi) (u + 0.044715 u^3))
+// with the hardware exp2 / reciprocal (relative error ~1e-6, far below the
+// bf16 rounding of the values it produces).  Used in GEMM epilogues.
+__device__ __forceinline__ float gelu_fast_f(float u) {
+  const float z = u * (1.5957691216057308f + 0.07135481627260025f * u * u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
+
 __device__ __forceinline__ float gelu_grad_f(float u) {
   const float c = 0.7978845608028654f;
   float t = tanhf(c * (u + 0.044715f * u * u * u));
