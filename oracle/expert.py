@@ -1,0 +1,162 @@
+"""Tenant-private action expert (config 4): forward, loss and weight
+gradients in fp64 -- oracle (test infrastructure only).
+
+Sec. 5.2 treats the action head as the tenant-private action module next to
+the resident base model (for GR00T- / pi0.5-style models a transformer
+"action expert" reading the VLM's features); App. A.3 feeds each tenant's
+decode with the shared features of its own requests.  Reading used here (the
+paper gives no layer definition): per sample, the expert embeds its
+``chunk`` noisy action tokens (``W_in``), runs ``L`` blocks of
+[RMSNorm -> self-attention over the sample's action tokens -> RMSNorm ->
+cross-attention whose keys / values are projected from *that sample's*
+valid backbone rows -> RMSNorm -> GELU MLP], each with a residual, then a
+final RMSNorm and ``W_out``; no biases.  Loss: the tenant's mean squared
+error against its targets; gradients for every expert weight and norm gain.
+The backbone is frozen: nothing flows back into the shared features.
+
+``rnd=True`` rounds to bf16 exactly where the GPU stores a GEMM
+operand in bf16 (forward: every GEMM input activation; backward: every
+incoming gradient before it meets a GEMM), computing everything else in
+fp64.  That is the GPU's precision contract, so parity of gradients can be
+checked at 1e-3 relative L2; with ``rnd=False`` the whole expert is
+plain fp64 (pinned against finite differences).
+
+Implemented with torch float64 CPU tensors and autograd for the chain rule
+(a library primitive; the custom ``Linear`` only decides rounding points).
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Sequence
+
+import numpy as np
+import torch
+
+from .backbone import bf16_to_f64
+
+
+def _round_bf16(t: torch.Tensor) -> torch.Tensor:
+    """Round fp64 values to the nearest bf16 (ties to even), returned in fp64."""
+    f = t.to(torch.float32)
+    u = f.view(torch.int32).to(torch.int64) & 0xFFFFFFFF
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16) << 16
+    r = torch.where(r >= 2 ** 31, r - 2 ** 32, r).to(torch.int32)
+    return r.view(torch.float32).to(torch.float64)
+
+
+class _Linear(torch.autograd.Function):
+    """y = x W^T with the GPU's rounding points: x is already bf16-valued; the
+    incoming gradient is rounded to bf16 before both backward products."""
+
+    @staticmethod
+    def forward(ctx, x, W, rnd):
+        ctx.save_for_backward(x, W)
+        ctx.rnd = rnd
+        return x @ W.T
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, W = ctx.saved_tensors
+        if ctx.rnd:
+            dy = _round_bf16(dy)
+        return dy @ W, dy.T @ x, None
+
+
+def linear(x, W, rnd: bool):
+    return _Linear.apply(x, W, rnd)
+
+
+class _RoundST(torch.autograd.Function):
+    """Forward: round to bf16 (a stored GEMM operand); backward: identity."""
+
+    @staticmethod
+    def forward(ctx, t):
+        return _round_bf16(t)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g
+
+
+def _q(t, rnd):
+    return _RoundST.apply(t) if rnd else t
+
+
+def _rms(x, g, eps):
+    return x / torch.sqrt(torch.mean(x * x, dim=-1, keepdim=True) + eps) * g
+
+
+def _gelu(u):
+    c = np.sqrt(2.0 / np.pi)
+    return 0.5 * u * (1.0 + torch.tanh(c * (u + 0.044715 * u ** 3)))
+
+
+def _attn(q, k, v, heads):
+    """Bidirectional multi-head attention: q [Lq, d], k/v [Lk, d]."""
+    Lq, d = q.shape
+    hd = d // heads
+    out = []
+    for h in range(heads):
+        sl = slice(h * hd, (h + 1) * hd)
+        s = (q[:, sl] @ k[:, sl].T) / np.sqrt(hd)
+        out.append(torch.softmax(s, dim=-1) @ v[:, sl])
+    return torch.cat(out, dim=1)
+
+
+def expert_params(w: dict) -> Dict[str, torch.Tensor]:
+    """fp64 leaf tensors (requires_grad) from an expert weight dict of bf16
+    bit arrays: w_in [d][a], w_out [a][d], gf [d], and per layer
+    wqkv_s [3d][d], wo_s [d][d], wq_c [d][d], wkv_c [2d][dp], wo_c [d][d],
+    w_up [f][d], w_down [d][f], g1, g2, g3 [d]."""
+    P = {}
+    for k in ("w_in", "w_out", "gf"):
+        P[k] = torch.tensor(bf16_to_f64(w[k]), requires_grad=True)
+    for l, lw in enumerate(w["layers"]):
+        for k, v in lw.items():
+            P[f"{l}.{k}"] = torch.tensor(bf16_to_f64(v), requires_grad=True)
+    return P
+
+
+def expert_forward(P, n_layers: int, heads: int, eps: float, u: Sequence[np.ndarray],
+                   z: Sequence[np.ndarray], rnd: bool) -> List[torch.Tensor]:
+    """Predictions [chunk, a] of every sample.  ``u[i]``: its noisy action
+    tokens [chunk, a] (fp32); ``z[i]``: its valid backbone rows [len_i, dp]
+    (bf16 bits or floats)."""
+    preds = []
+    for ui, zi in zip(u, z):
+        zt = torch.tensor(bf16_to_f64(zi) if zi.dtype == np.uint16 else np.asarray(zi, np.float64))
+        x = linear(_q(torch.tensor(np.asarray(ui, np.float64)), rnd), P["w_in"], rnd)
+        for l in range(n_layers):
+            g = lambda k: P[f"{l}.{k}"]  # noqa: E731
+            d = x.shape[1]
+            h = _q(_rms(x, g("g1"), eps), rnd)
+            qkv = linear(h, g("wqkv_s"), rnd)
+            a = _attn(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], heads)
+            x = x + linear(_q(a, rnd), g("wo_s"), rnd)
+            h = _q(_rms(x, g("g2"), eps), rnd)
+            q = linear(h, g("wq_c"), rnd)
+            kv = linear(zt, g("wkv_c"), rnd)
+            a = _attn(q, kv[:, :d], kv[:, d:], heads)
+            x = x + linear(_q(a, rnd), g("wo_c"), rnd)
+            h = _q(_rms(x, g("g3"), eps), rnd)
+            m = _q(_gelu(linear(h, g("w_up"), rnd)), rnd)
+            x = x + linear(m, g("w_down"), rnd)
+        y = _q(_rms(x, P["gf"], eps), rnd)
+        preds.append(linear(y, P["w_out"], rnd))
+    return preds
+
+
+def expert_step(w: dict, n_layers: int, heads: int, eps: float, u, z, targets, rnd: bool = False) -> Dict:
+    """Forward, the tenant's MSE loss and the gradient of every parameter.
+
+    ``targets``: [n, chunk, a].  Returns {"pred": [n, chunk, a] fp64,
+    "loss": float, "grads": {name: fp64 array}} with names as in
+    ``expert_params``."""
+    P = expert_params(w)
+    preds = expert_forward(P, n_layers, heads, eps, u, z, rnd)
+    Y = torch.stack(preds)
+    T = torch.tensor(np.asarray(targets, np.float64)).reshape(Y.shape)
+    loss = torch.mean((Y - T) ** 2)
+    loss.backward()
+    return {"pred": Y.detach().numpy(), "loss": float(loss.detach()),
+            "grads": {k: v.grad.numpy().copy() for k, v in P.items()}}

@@ -1,0 +1,94 @@
+"""Pins of the action-expert oracle (config 4) on tiny shapes."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import expert as ex
+
+
+def tiny_expert(rng, d=16, dp=8, f=32, a=3, L=2, scale=0.3):
+    def w(*s):
+        return W.f32_to_bf16_bits((rng.standard_normal(s) * scale).astype(np.float32))
+    g = lambda: W.f32_to_bf16_bits(rng.uniform(0.5, 1.5, d).astype(np.float32))  # noqa: E731
+    return {"w_in": w(d, a), "w_out": w(a, d), "gf": g(),
+            "layers": [{"wqkv_s": w(3 * d, d), "wo_s": w(d, d), "wq_c": w(d, d), "wkv_c": w(2 * d, dp),
+                        "wo_c": w(d, d), "w_up": w(f, d), "w_down": w(d, f), "g1": g(), "g2": g(), "g3": g()}
+                       for _ in range(L)]}
+
+
+def inputs(rng, n=2, chunk=4, a=3, dp=8, lens=(5, 7)):
+    u = [rng.standard_normal((chunk, a)).astype(np.float32) for _ in range(n)]
+    z = [rng.standard_normal((lens[i % len(lens)], dp)) for i in range(n)]
+    t = rng.standard_normal((n, chunk, a))
+    return u, z, t
+
+
+def test_round_bf16_matches_torch_conversion():
+    x = torch.tensor(np.random.default_rng(0).standard_normal(10000) * 10.0 ** np.random.default_rng(1).integers(-6, 6, 10000))
+    ref = x.to(torch.bfloat16).to(torch.float64)
+    assert torch.equal(ex._round_bf16(x), ref)
+
+
+def test_expert_grads_central_differences():
+    rng = np.random.default_rng(3)
+    w = tiny_expert(rng)
+    u, z, t = inputs(rng)
+    res = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=False)
+    P = ex.expert_params(w)
+    names = ["w_in", "w_out", "gf", "0.wqkv_s", "0.wo_s", "0.wq_c", "0.wkv_c", "0.wo_c", "1.w_up", "1.w_down",
+             "1.g1", "1.g2", "1.g3"]
+    h = 1e-6
+    for name in names:
+        base = P[name].detach().numpy()
+        idxs = [tuple(rng.integers(0, s) for s in base.shape) for _ in range(3)]
+        for idx in idxs:
+            def loss_at(delta):
+                Q = {k: v.detach().clone() for k, v in P.items()}
+                Q[name][idx] += delta
+                with torch.no_grad():
+                    preds = ex.expert_forward(Q, 2, 2, 1e-6, u, z, False)
+                    Y = torch.stack(preds)
+                    return float(torch.mean((Y - torch.tensor(t)) ** 2))
+            fd = (loss_at(h) - loss_at(-h)) / (2 * h)
+            g = res["grads"][name][idx]
+            assert abs(fd - g) <= 1e-6 * max(1.0, abs(g)) + 1e-9, (name, idx, fd, g)
+
+
+def test_expert_closed_forms_and_invariances():
+    rng = np.random.default_rng(4)
+    w = tiny_expert(rng)
+    u, z, t = inputs(rng)
+    # zero output projection: predictions are zero, loss = mean(t^2)
+    w0 = dict(w, w_out=np.zeros_like(w["w_out"]))
+    r0 = ex.expert_step(w0, 2, 2, 1e-6, u, z, t)
+    assert np.all(r0["pred"] == 0) and abs(r0["loss"] - float(np.mean(t ** 2))) < 1e-15
+    # zero key/value projection: cross-attention output is zero, so W_o_c gets no gradient
+    wz = {**w, "layers": [dict(l, wkv_c=np.zeros_like(l["wkv_c"])) for l in w["layers"]]}
+    rz = ex.expert_step(wz, 2, 2, 1e-6, u, z, t)
+    assert np.all(rz["grads"]["0.wo_c"] == 0) and np.all(rz["grads"]["1.wo_c"] == 0)
+    # cross-attention is invariant to the order of a sample's prefix rows
+    P = ex.expert_params(w)
+    with torch.no_grad():
+        a = ex.expert_forward(P, 2, 2, 1e-6, u, z, False)
+        zp = [zi[rng.permutation(zi.shape[0])] for zi in z]
+        b = ex.expert_forward(P, 2, 2, 1e-6, u, zp, False)
+        for x, y in zip(a, b):
+            assert torch.allclose(x, y, rtol=1e-12, atol=1e-14)
+        # no positions: permuting a sample's action tokens permutes its predictions
+        perm = rng.permutation(4)
+        c = ex.expert_forward(P, 2, 2, 1e-6, [ui[perm] for ui in u], z, False)
+        for x, y in zip(a, c):
+            assert torch.allclose(x[perm], y, rtol=1e-12, atol=1e-14)
+
+
+def test_expert_rounding_mode_is_close_to_fp64():
+    rng = np.random.default_rng(5)
+    w = tiny_expert(rng, scale=0.2)
+    u, z, t = inputs(rng)
+    a = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=False)
+    b = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=True)
+    for k in a["grads"]:
+        rel = np.linalg.norm(a["grads"][k] - b["grads"][k]) / max(np.linalg.norm(a["grads"][k]), 1e-30)
+        assert rel < 5e-2, (k, rel)
+    assert abs(a["loss"] - b["loss"]) < 1e-2 * a["loss"]

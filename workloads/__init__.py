@@ -80,6 +80,8 @@ class TenantSpec:
     action_dim: int
     chunk: int
     schema_sig: int = 0x4A4E5056_4C414631  # shared-prefix interface signature
+    # action expert instead of an MLP head: (layers, d, heads, ffn); None = MLP head
+    expert: Optional[Tuple[int, int, int, int]] = None
 
 
 @dataclasses.dataclass(frozen=True)
@@ -124,8 +126,11 @@ class Workload:
     gf: np.ndarray
     # per tenant: list of (W fp32 [out, in], b fp32 [out]); GELU between layers
     heads: List[List[Tuple[np.ndarray, np.ndarray]]]
-    # per tenant: fp32 [n_g, chunk, action_dim], rows in that tenant's arrival order
+    # per tenant: fp32 [n_g, chunk, action_dim], rows in that tenant's submission order
     targets: List[np.ndarray]
+    # per tenant (action-expert tenants only, else None): expert weights, noisy actions
+    experts: List[Optional[dict]] = dataclasses.field(default_factory=list)
+    noisy: List[Optional[np.ndarray]] = dataclasses.field(default_factory=list)
 
 
 # --------------------------------------------------------------------------
@@ -139,6 +144,8 @@ _BB_2B = BackboneSpec(layers=18, d=2048, heads=8, ffn=16384, glu=True)
 # Config 3's eight tenants cover every action_dim in {7,14,32} and chunk in {1,10,50}.
 _CFG3_SCHEMAS = ((7, 1), (7, 10), (7, 50), (14, 1), (14, 10), (14, 50), (32, 10), (32, 50))
 _CFG25_SCHEMAS = ((7, 1), (7, 8), (14, 4), (32, 10))
+# config 4's per-tenant action expert: 6 blocks, width 1024, 8 heads, MLP 4096
+_EXPERT_300M = (6, 1024, 8, 4096)
 
 
 def _rng(seed: int, cfg: int, stream: int) -> np.random.Generator:
@@ -152,6 +159,8 @@ _S_EMB = 20_000          # + request index
 _S_LAYER = 100_000       # + 16*layer + tensor index
 _S_HEAD = 500_000        # + 16*tenant + layer
 _S_TGT = 600_000         # + tenant
+_S_EXP = 700_000         # + 64*tenant + tensor index
+_S_NOISE = 900_000       # + tenant
 
 
 def zipf_counts(total: int, n_ranks: int, s: float) -> List[int]:
@@ -201,7 +210,8 @@ def config_spec(cfg: int, seed: int = 0) -> WorkloadSpec:
             cams = int(rng.integers(1, 4))
             n = int(rng.integers(4, 33))
             a = int(rng.choice([7, 14, 32]))
-            t.append(TenantSpec(n, 256 * cams, 16, 96, 256 * cams + 96, (768, 1024, a * 50), a, 50))
+            t.append(TenantSpec(n, 256 * cams, 16, 96, 256 * cams + 96, (768, 1024, a * 50), a, 50,
+                                expert=_EXPERT_300M))
         return WorkloadSpec(4, _BB_BASE, tuple(t), seed, "16 heterogeneous tenants, camera counts 1-3")
     if cfg == 5:
         rng = _rng(seed, 5, _S_META)
@@ -280,6 +290,37 @@ def head_weights(spec: WorkloadSpec, tenant: int) -> List[Tuple[np.ndarray, np.n
     return out
 
 
+def expert_weights(spec: WorkloadSpec, tenant: int) -> dict:
+    """bf16 action-expert weights ~N(0, 0.02), norm gains 1, [out][in] layout:
+    w_in [d][a], w_out [a][d], gf [d]; per layer wqkv_s [3d][d], wo_s [d][d],
+    wq_c [d][d], wkv_c [2d][dp] (keys then values, projected from the
+    backbone's width dp), wo_c [d][d], w_up [f][d], w_down [d][f], g1..g3 [d]."""
+    t = spec.tenants[tenant]
+    L, d, _, f = t.expert
+    dp, a = spec.backbone.d, t.action_dim
+    k = [0]
+
+    def w(shape):
+        k[0] += 1
+        rng = _rng(spec.seed, spec.config_id, _S_EXP + 64 * tenant + k[0])
+        return _normal_bf16(rng, shape, 0.02)
+
+    ones = f32_to_bf16_bits(np.ones(d, np.float32))
+    out = {"w_in": w((d, a)), "w_out": w((a, d)), "gf": ones.copy(), "layers": []}
+    for _ in range(L):
+        out["layers"].append({"wqkv_s": w((3 * d, d)), "wo_s": w((d, d)), "wq_c": w((d, d)),
+                              "wkv_c": w((2 * d, dp)), "wo_c": w((d, d)), "w_up": w((f, d)),
+                              "w_down": w((d, f)), "g1": ones.copy(), "g2": ones.copy(), "g3": ones.copy()})
+    return out
+
+
+def draw_noisy_actions(spec: WorkloadSpec, tenant: int) -> np.ndarray:
+    """fp32 [n, chunk, action_dim] ~N(0,1): the expert's input action tokens."""
+    t = spec.tenants[tenant]
+    rng = _rng(spec.seed, spec.config_id, _S_NOISE + tenant)
+    return rng.standard_normal((t.n_samples, t.chunk, t.action_dim), dtype=np.float32)
+
+
 def draw_targets(spec: WorkloadSpec, tenant: int) -> np.ndarray:
     t = spec.tenants[tenant]
     rng = _rng(spec.seed, spec.config_id, _S_TGT + tenant)
@@ -318,9 +359,11 @@ def make_workload(spec_or_cfg, seed: int = 0, with_weights: bool = True,
     if request_order is not None:
         requests = [requests[i] for i in request_order]
     gf = f32_to_bf16_bits(np.ones(spec.backbone.d, np.float32))
-    heads = [head_weights(spec, g) for g in range(G)]
+    heads = [head_weights(spec, g) if spec.tenants[g].expert is None else None for g in range(G)]
     targets = [draw_targets(spec, g) for g in range(G)]
-    return Workload(spec, requests, layers, gf, heads, targets)
+    experts = [expert_weights(spec, g) if spec.tenants[g].expert is not None else None for g in range(G)]
+    noisy = [draw_noisy_actions(spec, g) if spec.tenants[g].expert is not None else None for g in range(G)]
+    return Workload(spec, requests, layers, gf, heads, targets, experts, noisy)
 
 
 def tenant_rows(wl: Workload, tenant: int) -> List[Tuple[int, int]]:
@@ -330,6 +373,15 @@ def tenant_rows(wl: Workload, tenant: int) -> List[Tuple[int, int]]:
         if req.tenant == tenant:
             out.extend((r, s) for s in range(req.n))
     return out
+
+
+def tenant_rows_of(wl: Workload, tenant: int, arr: np.ndarray) -> np.ndarray:
+    """Rows of a per-tenant array (submission order) in arrival order."""
+    idx = []
+    for req in wl.requests:
+        if req.tenant == tenant:
+            idx.extend(range(req.first, req.first + req.n))
+    return arr[np.array(idx, dtype=np.int64)]
 
 
 def tenant_targets(wl: Workload, tenant: int) -> np.ndarray:
