@@ -70,7 +70,8 @@ const char* jn_last_error(const jn_ctx* ctx);
 typedef enum jn_op {
   JN_OP_PACK = 1, JN_OP_RMSNORM = 2, JN_OP_GEMM_QKV = 3, JN_OP_ATTENTION = 4, JN_OP_GEMM_O = 5,
   JN_OP_GEMM_UP = 6, JN_OP_GEMM_DOWN = 7, JN_OP_POOL = 8, JN_OP_HEAD_FWD = 9, JN_OP_LOSS = 10,
-  JN_OP_HEAD_BWD = 11, JN_OP_UNPACK = 12
+  JN_OP_HEAD_BWD = 11, JN_OP_UNPACK = 12, JN_OP_EXPERT_GEMM = 13, JN_OP_EXPERT_ATTENTION = 14,
+  JN_OP_EXPERT_OTHER = 15
 } jn_op;
 
 /* One traced kernel launch.  For GEMMs (M, N, K) is the launch shape
@@ -248,6 +249,79 @@ jn_status jn_heads_workspace_size(const jn_packed* p, const jn_head* heads, int3
 jn_status jn_tenant_heads_fwd_bwd(jn_ctx* ctx, const jn_packed* p, const void* hidden,
                                   const jn_head* heads, const jn_head_io* io, int32_t G,
                                   void* ws, size_t ws_bytes, float* pooled);
+
+/* ------------------------------------------------------- action expert --- */
+
+/* Per-tenant sample counts and valid prefix rows of a group (host only): the
+ * sizes jn_tenant_experts_fwd_bwd needs, from the same tables jn_pack_group
+ * takes.  samples[G], rows[G]. */
+jn_status jn_pack_tenant_sizes(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                               const jn_pack_opts* opts, int32_t* samples, int64_t* rows);
+
+/* A tenant-private action expert (the GR00T / pi0.5-style action module of a
+ * tenant, Sec. 5.2): per sample, `chunk` noisy action tokens embedded by W_in,
+ * n_layers blocks of [RMSNorm -> self-attention over the sample's action
+ * tokens -> RMSNorm -> cross-attention whose keys / values are projected
+ * (W_kv_c) from that sample's own valid backbone rows -> RMSNorm -> GELU MLP],
+ * residual each, final RMSNorm and W_out.  No biases.  Weights bf16 [out][in]. */
+typedef struct jn_expert_layer {
+  const void* wqkv_s;   /* [3d][d]  self-attention q | k | v            */
+  const void* wo_s;     /* [d][d]                                        */
+  const void* wq_c;     /* [d][d]   cross-attention queries             */
+  const void* wkv_c;    /* [2d][d_prefix] cross-attention keys | values */
+  const void* wo_c;     /* [d][d]                                        */
+  const void* w_up;     /* [ffn][d]                                      */
+  const void* w_down;   /* [d][ffn]                                      */
+  const void* g1;       /* [d] gains of the three pre-norms              */
+  const void* g2;
+  const void* g3;
+} jn_expert_layer;
+
+typedef struct jn_expert {
+  int32_t n_layers, d, n_heads, ffn;
+  int32_t action_dim;   /* <= 32 */
+  int32_t chunk;        /* action tokens per sample, <= 64 */
+  int32_t d_prefix;     /* backbone width */
+  float eps;
+  const void* w_in;     /* [d][action_dim] */
+  const void* w_out;    /* [action_dim][d] */
+  const void* gf;       /* [d]             */
+  const jn_expert_layer* layers;  /* host [n_layers] */
+} jn_expert;
+
+/* fp32 gradient outputs, same shapes as the weights they belong to. */
+typedef struct jn_expert_layer_grads {
+  float *wqkv_s, *wo_s, *wq_c, *wkv_c, *wo_c, *w_up, *w_down, *g1, *g2, *g3;
+} jn_expert_layer_grads;
+
+typedef struct jn_expert_io {
+  int32_t n_samples;      /* the tenant's samples in the packed batch      */
+  int32_t reserved;
+  int64_t prefix_rows;    /* sum of their valid lengths (jn_pack_tenant_sizes) */
+  const float* noisy;     /* device fp32 [n][chunk][action_dim], tenant arrival order */
+  const float* targets;   /* device fp32 [n][chunk][action_dim]            */
+  float* pred;            /* out: device fp32 [n][chunk][action_dim]       */
+  float* loss;            /* out: device fp32 [1], mean squared error      */
+  float* dw_in;           /* out: fp32 [d][action_dim]                     */
+  float* dw_out;          /* out: fp32 [action_dim][d]                     */
+  float* dgf;             /* out: fp32 [d]                                 */
+  const jn_expert_layer_grads* layers;  /* host [n_layers] of device outputs */
+} jn_expert_io;
+
+jn_status jn_experts_workspace_size(const jn_packed* p, const jn_expert* ex, const jn_expert_io* io, int32_t G,
+                                    size_t* bytes);
+
+/* The tenant stage for action-expert tenants: for every tenant g of the packed
+ * batch (ex[g], io[g]; all experts share n_layers, d, n_heads, ffn, chunk and
+ * d_prefix) the expert forward over its samples, its loss
+ * L_g = mean((pred - target)^2) and dL_g / d(every expert weight and gain).
+ * `hidden` is jn_backbone_forward's output; no gradient flows into it.
+ * Precision: GEMM operands bf16 (activations rounded where they are stored for
+ * a GEMM, incoming gradients rounded before a GEMM), fp32 accumulation, fp32
+ * residual, norms, attention, GELU derivative and loss.  Gradient outputs must
+ * be 16-byte aligned. */
+jn_status jn_tenant_experts_fwd_bwd(jn_ctx* ctx, const jn_packed* p, const void* hidden, const jn_expert* ex,
+                                    const jn_expert_io* io, int32_t G, void* ws, size_t ws_bytes);
 
 /* -------------------------------------------------------------- unpack --- */
 

@@ -14,7 +14,8 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 from . import _abi
-from ._abi import (JN_OK, STATUS_NAMES, jn_backbone, jn_head, jn_head_io, jn_layer, jn_pack_opts,
+from ._abi import (EXPERT_LAYER_FIELDS, JN_OK, STATUS_NAMES, jn_backbone, jn_expert, jn_expert_io,
+                   jn_expert_layer, jn_expert_layer_grads, jn_head, jn_head_io, jn_layer, jn_pack_opts,
                    jn_pack_sizes, jn_packed, jn_request, jn_tenant)
 
 _lib = _abi.load()
@@ -23,6 +24,7 @@ __all__ = [
     "JNError", "Context", "Request", "Tenant", "Backbone", "Head", "HeadIO",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group", "jn_backbone_workspace_size",
     "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
+    "Expert", "ExpertIO", "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
     "lib_path",
 ]
 
@@ -292,6 +294,84 @@ def jn_tenant_heads_fwd_bwd(ctx: Context, packed: Packed, hidden, heads: Sequenc
     ha, ia = _head_arrays(heads, ios)
     _check(_lib.jn_tenant_heads_fwd_bwd(ctx.handle, C.byref(packed.struct), _ptr(hidden), ha, ia, len(heads),
                                         _ptr(ws), ws.numel() * ws.element_size(), _ptr(pooled)), ctx)
+
+
+# ------------------------------------------------------- action expert ------
+
+def jn_pack_tenant_sizes(reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int = 1):
+    """(samples [G] int32, prefix rows [G] int64) of every tenant in the group."""
+    ra, keep = _requests(reqs)
+    ta = _tenants(tenants)
+    G = len(tenants)
+    n = np.zeros(G, np.int32)
+    r = np.zeros(G, np.int64)
+    _check(_lib.jn_pack_tenant_sizes(ra, len(reqs), ta, G, C.byref(_opts(d, align)),
+                                     n.ctypes.data_as(C.POINTER(C.c_int32)),
+                                     r.ctypes.data_as(C.POINTER(C.c_int64))), what="jn_pack_tenant_sizes")
+    return n, r
+
+
+class Expert:
+    """A tenant's action expert: device bf16 tensors w_in [d, a], w_out [a, d],
+    gf [d] and per layer a dict with the keys of ``EXPERT_LAYER_FIELDS``."""
+
+    def __init__(self, w_in, w_out, gf, layers: List[dict], n_heads: int, chunk: int, d_prefix: int, eps: float):
+        self.w_in, self.w_out, self.gf, self.layers = w_in, w_out, gf, layers
+        s = jn_expert()
+        s.n_layers = len(layers)
+        s.d = int(w_in.shape[0])
+        s.n_heads = int(n_heads)
+        s.ffn = int(layers[0]["w_up"].shape[0])
+        s.action_dim = int(w_in.shape[1])
+        s.chunk = int(chunk)
+        s.d_prefix = int(d_prefix)
+        s.eps = float(eps)
+        s.w_in, s.w_out, s.gf = _ptr(w_in), _ptr(w_out), _ptr(gf)
+        self._layers = (jn_expert_layer * len(layers))(
+            *[jn_expert_layer(*[_ptr(lw[k]) for k in EXPERT_LAYER_FIELDS]) for lw in layers])
+        s.layers = C.cast(self._layers, C.POINTER(jn_expert_layer))
+        self.struct = s
+
+
+class ExpertIO:
+    """A tenant's expert inputs and outputs (device fp32 tensors): noisy /
+    targets / pred [n, chunk, a], loss [1], dw_in, dw_out, dgf and per layer
+    a dict of gradients keyed as ``EXPERT_LAYER_FIELDS``."""
+
+    def __init__(self, n_samples: int, prefix_rows: int, noisy, targets, pred, loss, dw_in, dw_out, dgf,
+                 layers: List[dict]):
+        self.noisy, self.targets, self.pred, self.loss = noisy, targets, pred, loss
+        self.dw_in, self.dw_out, self.dgf, self.layers = dw_in, dw_out, dgf, layers
+        s = jn_expert_io()
+        s.n_samples = int(n_samples)
+        s.prefix_rows = int(prefix_rows)
+        s.noisy, s.targets, s.pred, s.loss = _ptr(noisy), _ptr(targets), _ptr(pred), _ptr(loss)
+        s.dw_in, s.dw_out, s.dgf = _ptr(dw_in), _ptr(dw_out), _ptr(dgf)
+        self._layers = (jn_expert_layer_grads * len(layers))(
+            *[jn_expert_layer_grads(*[_ptr(lg[k]) for k in EXPERT_LAYER_FIELDS]) for lg in layers])
+        s.layers = C.cast(self._layers, C.POINTER(jn_expert_layer_grads))
+        self.struct = s
+
+
+def _expert_arrays(ex: Sequence[Expert], ios: Sequence[ExpertIO]):
+    ea = (jn_expert * len(ex))(*[e.struct for e in ex])
+    ia = (jn_expert_io * len(ios))(*[x.struct for x in ios])
+    return ea, ia
+
+
+def jn_experts_workspace_size(packed: Packed, ex: Sequence[Expert], ios: Sequence[ExpertIO]) -> int:
+    ea, ia = _expert_arrays(ex, ios)
+    n = C.c_size_t()
+    _check(_lib.jn_experts_workspace_size(C.byref(packed.struct), ea, ia, len(ex), C.byref(n)),
+           what="jn_experts_workspace_size")
+    return int(n.value)
+
+
+def jn_tenant_experts_fwd_bwd(ctx: Context, packed: Packed, hidden, ex: Sequence[Expert], ios: Sequence[ExpertIO],
+                              ws):
+    ea, ia = _expert_arrays(ex, ios)
+    _check(_lib.jn_tenant_experts_fwd_bwd(ctx.handle, C.byref(packed.struct), _ptr(hidden), ea, ia, len(ex),
+                                          _ptr(ws), ws.numel() * ws.element_size()), ctx)
 
 
 # -------------------------------------------------------------- unpack ------

@@ -22,12 +22,15 @@ EXPORTS = (
     "jn_ctx_trace_read",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group",
     "jn_backbone_workspace_size", "jn_backbone_forward",
-    "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
+    "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd",
+    "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
+    "jn_unpack",
 )
 
 
 OPS = {1: "pack", 2: "rmsnorm", 3: "gemm_qkv", 4: "attention", 5: "gemm_o", 6: "gemm_up", 7: "gemm_down",
-       8: "pool", 9: "head_fwd", 10: "loss", 11: "head_bwd", 12: "unpack"}
+       8: "pool", 9: "head_fwd", 10: "loss", 11: "head_bwd", 12: "unpack", 13: "expert_gemm",
+       14: "expert_attention", 15: "expert_other"}
 
 
 class jn_trace_entry(C.Structure):
@@ -93,6 +96,31 @@ class jn_head_io(C.Structure):
                 ("dW", C.POINTER(C.c_void_p)), ("db", C.POINTER(C.c_void_p))]
 
 
+EXPERT_LAYER_FIELDS = ("wqkv_s", "wo_s", "wq_c", "wkv_c", "wo_c", "w_up", "w_down", "g1", "g2", "g3")
+
+
+class jn_expert_layer(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in EXPERT_LAYER_FIELDS]
+
+
+class jn_expert(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d", C.c_int32), ("n_heads", C.c_int32), ("ffn", C.c_int32),
+                ("action_dim", C.c_int32), ("chunk", C.c_int32), ("d_prefix", C.c_int32), ("eps", C.c_float),
+                ("w_in", C.c_void_p), ("w_out", C.c_void_p), ("gf", C.c_void_p),
+                ("layers", C.POINTER(jn_expert_layer))]
+
+
+class jn_expert_layer_grads(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in EXPERT_LAYER_FIELDS]
+
+
+class jn_expert_io(C.Structure):
+    _fields_ = [("n_samples", C.c_int32), ("reserved", C.c_int32), ("prefix_rows", C.c_int64),
+                ("noisy", C.c_void_p), ("targets", C.c_void_p), ("pred", C.c_void_p), ("loss", C.c_void_p),
+                ("dw_in", C.c_void_p), ("dw_out", C.c_void_p), ("dgf", C.c_void_p),
+                ("layers", C.POINTER(jn_expert_layer_grads))]
+
+
 _lib = None
 
 
@@ -123,6 +151,12 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "jn_heads_workspace_size": (C.c_int, [P(jn_packed), P(jn_head), C.c_int32, P(C.c_size_t)]),
         "jn_tenant_heads_fwd_bwd": (C.c_int, [V, P(jn_packed), V, P(jn_head), P(jn_head_io), C.c_int32, V,
                                               C.c_size_t, V]),
+        "jn_pack_tenant_sizes": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                           P(C.c_int32), P(C.c_int64)]),
+        "jn_experts_workspace_size": (C.c_int, [P(jn_packed), P(jn_expert), P(jn_expert_io), C.c_int32,
+                                                P(C.c_size_t)]),
+        "jn_tenant_experts_fwd_bwd": (C.c_int, [V, P(jn_packed), V, P(jn_expert), P(jn_expert_io), C.c_int32, V,
+                                                C.c_size_t]),
         "jn_unpack": (C.c_int, [V, P(jn_packed), P(jn_request), C.c_int32, V, C.c_size_t, P(V)]),
     }
     for name, (res, args) in sig.items():

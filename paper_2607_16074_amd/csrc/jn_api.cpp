@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <new>
 #include <string>
 #include <vector>
@@ -831,6 +832,649 @@ jn_status jn_unpack(jn_ctx* c, const jn_packed* p, const jn_request* req, int32_
   JN_TRACED(c, JN_OP_UNPACK, p->T, (int64_t)row_bytes, 0, launch_unpack(c->stream, (const ReqEntry*)p->req_table, p->sample_request, p->sample_local,
                           p->seqlens, p->cu_seqlens, p->N, mreq, rows, (int64_t)row_bytes, vec16),
          "unpack kernel");
+  return JN_OK;
+}
+
+}  // extern "C"
+
+// --------------------------------------------------------- action expert ---
+
+namespace {
+
+struct ExpShape {
+  int32_t L, d, H, f, chunk, dp;
+  float eps;
+};
+
+// Host view of one expert call: per-tenant rows and padded contraction sizes.
+struct ExpPlan {
+  ExpShape sh{};
+  int32_t G = 0, N = 0;
+  std::vector<int32_t> rows, roff, Ka, kaoff, Kz, kzoff;
+  std::vector<int64_t> Pz, zoff;
+  int64_t Na = 0, Pzt = 0, KaT = 0, KzT = 0;
+};
+
+// Workspace regions (byte offsets); per-layer saves are arrays of offsets.
+struct ExpLayout {
+  size_t arena = 0, arena_bytes = 0;
+  size_t x, xf, yb, ub, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, TA, TB,
+      WT, dwinp, dwoutp;
+  std::vector<size_t> x1, x2, x3, h1, h2, h3, qkv, os, osb, lses, qc, kv, oc, ocb, lsec, pre, mb;
+  size_t total = 0;
+};
+
+jn_status exp_plan(jn_ctx* c, const jn_packed* p, const jn_expert* ex, const jn_expert_io* io, int32_t G,
+                   ExpPlan* P) {
+  if (!ex || !io) return fail(c, JN_EINVAL, "null experts or io");
+  if (G != p->G) return fail(c, JN_EINVAL, "G=%d but the packed batch has %d tenants", G, p->G);
+  const jn_expert& e0 = ex[0];
+  ExpShape sh{e0.n_layers, e0.d, e0.n_heads, e0.ffn, e0.chunk, e0.d_prefix, e0.eps};
+  if (sh.L < 1 || sh.d < 1 || sh.H < 1 || sh.f < 1 || sh.chunk < 1) return fail(c, JN_EINVAL, "expert sizes must be positive");
+  if (sh.chunk > 64) return fail(c, JN_EUNSUPPORTED, "chunk %d > 64", sh.chunk);
+  if (sh.d % sh.H != 0 || (sh.d / sh.H != 64 && sh.d / sh.H != 128))
+    return fail(c, JN_EUNSUPPORTED, "expert head dim must be 64 or 128");
+  if (sh.d != 256 && sh.d != 512 && sh.d != 1024 && sh.d != 2048) return fail(c, JN_EUNSUPPORTED, "expert width %d", sh.d);
+  if (sh.f % 32 != 0 || sh.dp % 32 != 0) return fail(c, JN_EUNSUPPORTED, "ffn and d_prefix must be multiples of 32");
+  if (sh.dp != p->d) return fail(c, JN_EINCOMPAT, "expert reads width %d, backbone has %d", sh.dp, p->d);
+  if (!(sh.eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
+  P->sh = sh;
+  P->G = G;
+  P->N = p->N;
+  int64_t n = 0;
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_expert& e = ex[g];
+    if (e.n_layers != sh.L || e.d != sh.d || e.n_heads != sh.H || e.ffn != sh.f || e.chunk != sh.chunk ||
+        e.d_prefix != sh.dp || e.eps != sh.eps)
+      return fail(c, JN_EUNSUPPORTED, "expert %d differs in shape from expert 0", g);
+    if (e.action_dim < 1 || e.action_dim > 32) return fail(c, JN_EUNSUPPORTED, "expert %d action_dim %d", g, e.action_dim);
+    if (!e.w_in || !e.w_out || !e.gf || !e.layers) return fail(c, JN_EINVAL, "expert %d incomplete", g);
+    for (int l = 0; l < sh.L; ++l) {
+      const jn_expert_layer& L = e.layers[l];
+      const void* ps[] = {L.wqkv_s, L.wo_s, L.wq_c, L.wkv_c, L.wo_c, L.w_up, L.w_down, L.g1, L.g2, L.g3};
+      for (const void* q : ps)
+        if (!q) return fail(c, JN_EINVAL, "expert %d layer %d has a null weight", g, l);
+    }
+    const jn_expert_io& I = io[g];
+    if (I.n_samples < 1 || I.prefix_rows < I.n_samples) return fail(c, JN_ESHAPE, "io %d sizes", g);
+    if (!I.noisy || !I.targets || !I.pred || !I.loss || !I.dw_in || !I.dw_out || !I.dgf || !I.layers)
+      return fail(c, JN_EINVAL, "io %d incomplete", g);
+    for (int l = 0; l < sh.L; ++l) {
+      const jn_expert_layer_grads& Gr = I.layers[l];
+      float* ps[] = {Gr.wqkv_s, Gr.wo_s, Gr.wq_c, Gr.wkv_c, Gr.wo_c, Gr.w_up, Gr.w_down, Gr.g1, Gr.g2, Gr.g3};
+      for (float* q : ps)
+        if (!q || ((uintptr_t)q) % 16 != 0) return fail(c, JN_EINVAL, "io %d layer %d gradient null or unaligned", g, l);
+    }
+    n += I.n_samples;
+  }
+  if (n != p->N) return fail(c, JN_ESHAPE, "io holds %lld samples, packed batch %d", (long long)n, p->N);
+  P->rows.resize(G);
+  P->roff.assign(G + 1, 0);
+  P->Ka.resize(G);
+  P->kaoff.assign(G + 1, 0);
+  P->Kz.resize(G);
+  P->kzoff.assign(G + 1, 0);
+  P->Pz.resize(G);
+  P->zoff.assign(G + 1, 0);
+  for (int32_t g = 0; g < G; ++g) {
+    P->rows[g] = io[g].n_samples * sh.chunk;
+    P->roff[g + 1] = P->roff[g] + P->rows[g];
+    P->Ka[g] = (P->rows[g] + 31) / 32 * 32;
+    P->kaoff[g + 1] = P->kaoff[g] + P->Ka[g];
+    P->Pz[g] = io[g].prefix_rows;
+    P->zoff[g + 1] = P->zoff[g] + P->Pz[g];
+    P->Kz[g] = (int32_t)((P->Pz[g] + 31) / 32 * 32);
+    P->kzoff[g + 1] = P->kzoff[g] + P->Kz[g];
+  }
+  P->Na = P->roff[G];
+  P->Pzt = P->zoff[G];
+  P->KaT = P->kaoff[G];
+  P->KzT = P->kzoff[G];
+  if (P->Pzt > p->T) return fail(c, JN_ESHAPE, "io prefix rows exceed the packed batch");
+  if (P->Na >= (1ll << 31) || P->Pzt * 2 * sh.d >= (1ll << 40)) return fail(c, JN_ESHAPE, "expert batch too large");
+  return JN_OK;
+}
+
+ExpLayout exp_layout(const ExpPlan& P) {
+  ExpLayout Ly;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  const ExpShape& s = P.sh;
+  const int64_t Na = P.Na, Pz = P.Pzt, d = s.d, f = s.f, H = s.H, G = P.G;
+  const int64_t wmax = std::max<int64_t>(3 * d, f);
+  Ly.arena_bytes = (size_t)(64 * s.L + 64) * G * 224 + (1 << 16);
+  Ly.arena = take(Ly.arena_bytes);
+  Ly.x = take(4 * Na * d);
+  Ly.xf = take(4 * Na * d);
+  Ly.yb = take(2 * Na * d);
+  Ly.ub = take(2 * Na * 32);
+  Ly.predp = take(4 * Na * 32);
+  Ly.dpred = take(4 * Na * 32);
+  Ly.dpredb = take(2 * Na * 32);
+  Ly.z = take(2 * Pz * s.dp);
+  Ly.zoff = take(4 * (P.N + 1));
+  Ly.winp = take(2 * G * d * 32);
+  Ly.woutp = take(2 * G * 32 * d);
+  Ly.woutpT = take(2 * G * d * 32);
+  Ly.dx = take(4 * Na * d);
+  Ly.dxb = take(2 * Na * d);
+  Ly.tf = take(4 * Na * d);
+  Ly.tq = take(4 * Na * 3 * d);
+  Ly.tb = take(2 * Na * wmax);
+  Ly.dkv = take(4 * Pz * 2 * d);
+  Ly.dkvb = take(2 * Pz * 2 * d);
+  Ly.gx = take(4 * Na * d);
+  Ly.TA = take(2 * std::max<int64_t>(wmax * P.KaT, 2 * d * P.KzT));
+  Ly.TB = take(2 * std::max<int64_t>(wmax * P.KaT, (int64_t)s.dp * P.KzT));
+  Ly.WT = take(2 * G * std::max<int64_t>(f * d, 3 * d * d) + 2 * G * 2 * d * s.dp);
+  Ly.dwinp = take(4 * G * d * 32);
+  Ly.dwoutp = take(4 * G * 32 * d);
+  for (int l = 0; l < s.L; ++l) {
+    Ly.x1.push_back(take(4 * Na * d));
+    Ly.x2.push_back(take(4 * Na * d));
+    Ly.x3.push_back(take(4 * Na * d));
+    Ly.h1.push_back(take(2 * Na * d));
+    Ly.h2.push_back(take(2 * Na * d));
+    Ly.h3.push_back(take(2 * Na * d));
+    Ly.qkv.push_back(take(4 * Na * 3 * d));
+    Ly.os.push_back(take(4 * Na * d));
+    Ly.osb.push_back(take(2 * Na * d));
+    Ly.lses.push_back(take(4 * Na * H));
+    Ly.qc.push_back(take(4 * Na * d));
+    Ly.kv.push_back(take(4 * Pz * 2 * d));
+    Ly.oc.push_back(take(4 * Na * d));
+    Ly.ocb.push_back(take(2 * Na * d));
+    Ly.lsec.push_back(take(4 * Na * H));
+    Ly.pre.push_back(take(4 * Na * f));
+    Ly.mb.push_back(take(2 * Na * f));
+  }
+  Ly.total = o;
+  return Ly;
+}
+
+// Records grouped launches: descriptor tables go to a host image of the arena,
+// the launches run after one upload of that image.
+struct Recorder {
+  std::vector<char> img;
+  size_t cap = 0;
+  bool overflow = false;
+  std::vector<std::function<hipError_t(char*)>> ops;
+  std::vector<int32_t> opcode;
+  size_t add(const void* src, size_t bytes) {
+    size_t at = align_up(img.size(), 256);
+    if (at + bytes > cap) {
+      overflow = true;
+      return 0;
+    }
+    img.resize(at + bytes);
+    std::memcpy(img.data() + at, src, bytes);
+    return at;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+jn_status jn_pack_tenant_sizes(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                               const jn_pack_opts* o, int32_t* samples, int64_t* rows) {
+  if (!samples || !rows) return JN_EINVAL;
+  Plan p;
+  jn_status st = make_plan(nullptr, req, R, ten, G, o, &p);
+  if (st != JN_OK) return st;
+  for (int32_t g = 0; g < G; ++g) {
+    samples[g] = 0;
+    rows[g] = 0;
+  }
+  for (int32_t i = 0; i < p.N; ++i) {
+    samples[p.sten[i]] += 1;
+    rows[p.sten[i]] += p.seqlens[i];
+  }
+  return JN_OK;
+}
+
+jn_status jn_experts_workspace_size(const jn_packed* p, const jn_expert* ex, const jn_expert_io* io, int32_t G,
+                                    size_t* bytes) {
+  if (!bytes || !valid_packed(p)) return JN_EINVAL;
+  ExpPlan P;
+  jn_status st = exp_plan(nullptr, p, ex, io, G, &P);
+  if (st != JN_OK) return st;
+  *bytes = exp_layout(P).total;
+  return JN_OK;
+}
+
+jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_expert* ex,
+                                    const jn_expert_io* io, int32_t G, void* ws, size_t ws_bytes) {
+  if (!c) return JN_EINVAL;
+  if (!valid_packed(p) || !p->tenant_perm) return fail(c, JN_EINVAL, "invalid packed batch");
+  if (!hidden || !ws) return fail(c, JN_EINVAL, "null hidden or workspace");
+  ExpPlan P;
+  jn_status st = exp_plan(c, p, ex, io, G, &P);
+  if (st != JN_OK) return st;
+  const ExpLayout Ly = exp_layout(P);
+  if (ws_bytes < Ly.total) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, Ly.total);
+  if (((uintptr_t)ws) % 256 != 0) return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte aligned");
+
+  char* w = (char*)ws;
+  char* const darena = w + Ly.arena;
+  const ExpShape& S = P.sh;
+  const int64_t d = S.d, f = S.f, dp = S.dp, H = S.H;
+  auto F = [&](size_t off) { return (float*)(w + off); };
+  auto B = [&](size_t off) { return (uint16_t*)(w + off); };
+  Recorder rec;
+  rec.cap = Ly.arena_bytes;
+  const size_t roff_at = rec.add(P.roff.data(), 4 * P.roff.size());
+  hipStream_t s = c->stream;
+
+  // ---- recording helpers
+  auto gemm = [&](int epi, std::vector<GemmArgs> probs) {
+    int32_t maxm = 0;
+    for (auto& g : probs) maxm = std::max(maxm, g.M);
+    const int shape = gemm_grouped_tile_shape(maxm);
+    const int32_t tiles = gemm_grouped_prepare(probs.data(), (int32_t)probs.size(), shape);
+    const size_t at = rec.add(probs.data(), sizeof(GemmArgs) * probs.size());
+    const int32_t n = (int32_t)probs.size();
+    rec.ops.push_back([=](char* a) { return launch_gemm_grouped(s, epi, (const GemmArgs*)(a + at), n, tiles, shape); });
+    rec.opcode.push_back(JN_OP_EXPERT_GEMM);
+  };
+  auto per_tenant_gemm = [&](int epi, std::function<GemmArgs(int32_t)> fn) {
+    std::vector<GemmArgs> v;
+    for (int32_t g = 0; g < G; ++g) v.push_back(fn(g));
+    gemm(epi, v);
+  };
+  auto copy = [&](std::vector<CopyDesc> dv) {
+    const int32_t blocks = copy2d_prepare(dv.data(), (int32_t)dv.size());
+    const size_t at = rec.add(dv.data(), sizeof(CopyDesc) * dv.size());
+    const int32_t n = (int32_t)dv.size();
+    rec.ops.push_back([=](char* a) { return launch_copy2d(s, (const CopyDesc*)(a + at), n, blocks); });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+  };
+  auto trans = [&](std::vector<TransDesc> dv) {
+    const int32_t blocks = transpose_prepare(dv.data(), (int32_t)dv.size());
+    const size_t at = rec.add(dv.data(), sizeof(TransDesc) * dv.size());
+    const int32_t n = (int32_t)dv.size();
+    rec.ops.push_back([=](char* a) { return launch_transpose(s, (const TransDesc*)(a + at), n, blocks); });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+  };
+  auto ptr_table = [&](std::function<const void*(int32_t)> fn) {
+    std::vector<const void*> v(G);
+    for (int32_t g = 0; g < G; ++g) v[g] = fn(g);
+    return rec.add(v.data(), sizeof(void*) * G);
+  };
+  auto rms_fwd = [&](size_t x_at, size_t gains_at, size_t h_at) {
+    const int64_t rows = P.Na;
+    rec.ops.push_back([=](char* a) {
+      return launch_xrms_fwd(s, F(x_at), (const void* const*)(a + gains_at), (const int32_t*)(a + roff_at), G,
+                             (int32_t)rows, (int32_t)d, S.eps, w + h_at);
+    });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+  };
+  auto rms_bwd = [&](size_t x_at, size_t gains_at, size_t dg_at) {
+    const int64_t rows = P.Na;
+    rec.ops.push_back([=](char* a) {
+      return launch_xrms_bwd(s, F(x_at), (const void* const*)(a + gains_at), (const int32_t*)(a + roff_at), G,
+                             (int32_t)rows, (int32_t)d, S.eps, F(Ly.tf), F(Ly.dx), F(Ly.gx), (float* const*)(a + dg_at));
+    });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+  };
+  auto attn = [&](AttnArgs A, bool bwd) {
+    const int32_t n = P.N;
+    rec.ops.push_back([=](char*) { return launch_xattn(s, A, n, bwd); });
+    rec.opcode.push_back(JN_OP_EXPERT_ATTENTION);
+  };
+  // whole-buffer copy / conversion of Na rows
+  auto rows_copy = [&](const void* src, bool sb, void* dst, bool db, int64_t rows, int64_t cols) {
+    CopyDesc cd{};
+    cd.src = src;
+    cd.dst = dst;
+    cd.src_ld = cols;
+    cd.dst_ld = cols;
+    cd.rows = (int32_t)rows;
+    cd.cols = (int32_t)cols;
+    cd.src_rows = src ? (int32_t)rows : 0;
+    cd.src_cols = (int32_t)cols;
+    cd.src_bf16 = sb;
+    cd.dst_bf16 = db;
+    copy({cd});
+  };
+  // transpose a [rows_g][width] per-tenant block of a row buffer (ld = width)
+  // into `dst_at` as [width][K_g] blocks (K padded with zeros)
+  auto trans_rows = [&](const uint16_t* src, int64_t width, uint16_t* dst, bool prefix) {
+    std::vector<TransDesc> v;
+    for (int32_t g = 0; g < G; ++g) {
+      TransDesc t{};
+      const int64_t r0 = prefix ? P.zoff[g] : P.roff[g];
+      const int64_t k0 = prefix ? P.kzoff[g] : P.kaoff[g];
+      t.src = src + r0 * width;
+      t.src_ld = width;
+      t.rows = prefix ? (int32_t)P.Pz[g] : P.rows[g];
+      t.cols = (int32_t)width;
+      t.rows_pad = prefix ? P.Kz[g] : P.Ka[g];
+      t.dst = dst + width * k0;
+      t.dst_ld = t.rows_pad;
+      v.push_back(t);
+    }
+    trans(v);
+  };
+  // transposed copy of each tenant's weight [rows][cols] -> WT block [cols][rows]
+  auto trans_w = [&](std::function<const void*(int32_t)> wsel, int64_t rows, int64_t cols) {
+    std::vector<TransDesc> v;
+    for (int32_t g = 0; g < G; ++g) {
+      TransDesc t{};
+      t.src = (const uint16_t*)wsel(g);
+      t.src_ld = cols;
+      t.rows = (int32_t)rows;
+      t.cols = (int32_t)cols;
+      t.rows_pad = (int32_t)rows;
+      t.dst = B(Ly.WT) + (int64_t)g * rows * cols;
+      t.dst_ld = rows;
+      v.push_back(t);
+    }
+    trans(v);
+  };
+  auto WTg = [&](int32_t g, int64_t rows, int64_t cols) { return B(Ly.WT) + (int64_t)g * rows * cols; };
+  // data GEMM over each tenant's rows: C[rows][N] = X[rows][K] W[N][K]^T
+  auto rows_gemm = [&](int epi, const uint16_t* X, int64_t K, std::function<const uint16_t*(int32_t)> Wsel, int64_t N,
+                       void* C, int64_t ldc, bool cfp32, float* aux = nullptr) {
+    per_tenant_gemm(epi, [&](int32_t g) {
+      GemmArgs a{};
+      a.X = X + (int64_t)P.roff[g] * K;
+      a.ldx = K;
+      a.W = Wsel(g);
+      a.ldw = K;
+      a.C = cfp32 ? (void*)((float*)C + (int64_t)P.roff[g] * ldc) : (void*)((uint16_t*)C + (int64_t)P.roff[g] * ldc);
+      a.ldc = ldc;
+      if (aux) {
+        a.aux = aux + (int64_t)P.roff[g] * N;
+        a.ldaux = N;
+      }
+      a.M = P.rows[g];
+      a.N = (int32_t)N;
+      a.K = (int32_t)K;
+      return a;
+    });
+  };
+  // weight-gradient GEMM: C[out][in] = TA_g [out][K_g] . TB_g [in][K_g]^T
+  auto wgrad = [&](int64_t out, int64_t in, std::function<float*(int32_t)> Csel, bool prefix) {
+    per_tenant_gemm(EPI_F32, [&](int32_t g) {
+      GemmArgs a{};
+      const int64_t k0 = prefix ? P.kzoff[g] : P.kaoff[g];
+      const int32_t K = prefix ? P.Kz[g] : P.Ka[g];
+      a.X = B(Ly.TA) + out * k0;
+      a.ldx = K;
+      a.W = B(Ly.TB) + in * k0;
+      a.ldw = K;
+      a.C = Csel(g);
+      a.ldc = in;
+      a.M = (int32_t)out;
+      a.N = (int32_t)in;
+      a.K = K;
+      return a;
+    });
+  };
+  auto Wl = [&](int l, const void* jn_expert_layer::*m) {
+    return [=](int32_t g) { return (const uint16_t*)(ex[g].layers[l].*m); };
+  };
+  auto Gl = [&](int l, float* jn_expert_layer_grads::*m) { return [=](int32_t g) { return io[g].layers[l].*m; }; };
+
+  // ---------------------------------------------------------------- forward
+  {
+    std::vector<CopyDesc> v;
+    for (int32_t g = 0; g < G; ++g) {
+      const int32_t a = ex[g].action_dim;
+      CopyDesc u{io[g].noisy, B(Ly.ub) + (int64_t)P.roff[g] * 32, a, 32, P.rows[g], 32, P.rows[g], a, 0, 1, 0, 0};
+      CopyDesc wi{ex[g].w_in, B(Ly.winp) + (int64_t)g * d * 32, a, 32, (int32_t)d, 32, (int32_t)d, a, 1, 1, 0, 0};
+      CopyDesc wo{ex[g].w_out, B(Ly.woutp) + (int64_t)g * 32 * d, d, d, 32, (int32_t)d, a, (int32_t)d, 1, 1, 0, 0};
+      v.push_back(u);
+      v.push_back(wi);
+      v.push_back(wo);
+    }
+    copy(v);
+    std::vector<TransDesc> t;
+    for (int32_t g = 0; g < G; ++g)
+      t.push_back(TransDesc{B(Ly.woutp) + (int64_t)g * 32 * d, B(Ly.woutpT) + (int64_t)g * d * 32, d, 32, 32,
+                            (int32_t)d, 32, 0});
+    trans(t);
+    const int64_t cap = P.Pzt;
+    rec.ops.push_back([=](char*) {
+      return launch_prefix(s, hidden, p->tenant_perm, p->seqlens, p->cu_seqlens, p->N, p->max_seqlen, (int32_t)dp, cap,
+                           (int32_t*)(w + Ly.zoff), w + Ly.z);
+    });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+    rows_gemm(EPI_F32, B(Ly.ub), 32, [&](int32_t g) { return B(Ly.winp) + (int64_t)g * d * 32; }, d, F(Ly.x), d, true);
+  }
+  const float scale = 1.0f / sqrtf((float)(d / H));
+  for (int l = 0; l < S.L; ++l) {
+    const size_t g1 = ptr_table([&](int32_t g) { return ex[g].layers[l].g1; });
+    const size_t g2 = ptr_table([&](int32_t g) { return ex[g].layers[l].g2; });
+    const size_t g3 = ptr_table([&](int32_t g) { return ex[g].layers[l].g3; });
+    // self-attention block
+    rows_copy(F(Ly.x), false, F(Ly.x1[l]), false, P.Na, d);
+    rms_fwd(Ly.x1[l], g1, Ly.h1[l]);
+    rows_gemm(EPI_F32, B(Ly.h1[l]), d, Wl(l, &jn_expert_layer::wqkv_s), 3 * d, F(Ly.qkv[l]), 3 * d, true);
+    {
+      AttnArgs A{};
+      A.Q = F(Ly.qkv[l]);
+      A.K = F(Ly.qkv[l]);
+      A.V = F(Ly.qkv[l]);
+      A.O = F(Ly.os[l]);
+      A.lse = F(Ly.lses[l]);
+      A.ldq = 3 * d;
+      A.ldkv = 3 * d;
+      A.ldo = d;
+      A.kcol = (int32_t)d;
+      A.vcol = (int32_t)(2 * d);
+      A.Lq = S.chunk;
+      A.hd = (int32_t)(d / H);
+      A.nheads = (int32_t)H;
+      A.scale = scale;
+      attn(A, false);
+    }
+    rows_copy(F(Ly.os[l]), false, B(Ly.osb[l]), true, P.Na, d);
+    rows_gemm(EPI_RESID_F32, B(Ly.osb[l]), d, Wl(l, &jn_expert_layer::wo_s), d, F(Ly.x), d, true);
+    // cross-attention block
+    rows_copy(F(Ly.x), false, F(Ly.x2[l]), false, P.Na, d);
+    rms_fwd(Ly.x2[l], g2, Ly.h2[l]);
+    rows_gemm(EPI_F32, B(Ly.h2[l]), d, Wl(l, &jn_expert_layer::wq_c), d, F(Ly.qc[l]), d, true);
+    per_tenant_gemm(EPI_F32, [&](int32_t g) {
+      GemmArgs a{};
+      a.X = B(Ly.z) + P.zoff[g] * dp;
+      a.ldx = dp;
+      a.W = (const uint16_t*)ex[g].layers[l].wkv_c;
+      a.ldw = dp;
+      a.C = F(Ly.kv[l]) + P.zoff[g] * 2 * d;
+      a.ldc = 2 * d;
+      a.M = (int32_t)P.Pz[g];
+      a.N = (int32_t)(2 * d);
+      a.K = (int32_t)dp;
+      return a;
+    });
+    {
+      AttnArgs A{};
+      A.Q = F(Ly.qc[l]);
+      A.K = F(Ly.kv[l]);
+      A.V = F(Ly.kv[l]);
+      A.O = F(Ly.oc[l]);
+      A.lse = F(Ly.lsec[l]);
+      A.zoff = (const int32_t*)(w + Ly.zoff);
+      A.kv_cap = P.Pzt;
+      A.ldq = d;
+      A.ldkv = 2 * d;
+      A.ldo = d;
+      A.kcol = 0;
+      A.vcol = (int32_t)d;
+      A.Lq = S.chunk;
+      A.hd = (int32_t)(d / H);
+      A.nheads = (int32_t)H;
+      A.scale = scale;
+      attn(A, false);
+    }
+    rows_copy(F(Ly.oc[l]), false, B(Ly.ocb[l]), true, P.Na, d);
+    rows_gemm(EPI_RESID_F32, B(Ly.ocb[l]), d, Wl(l, &jn_expert_layer::wo_c), d, F(Ly.x), d, true);
+    // MLP block
+    rows_copy(F(Ly.x), false, F(Ly.x3[l]), false, P.Na, d);
+    rms_fwd(Ly.x3[l], g3, Ly.h3[l]);
+    rows_gemm(EPI_GELU_SAVE, B(Ly.h3[l]), d, Wl(l, &jn_expert_layer::w_up), f, B(Ly.mb[l]), f, false, F(Ly.pre[l]));
+    rows_gemm(EPI_RESID_F32, B(Ly.mb[l]), f, Wl(l, &jn_expert_layer::w_down), d, F(Ly.x), d, true);
+  }
+  const size_t gfa = ptr_table([&](int32_t g) { return ex[g].gf; });
+  rows_copy(F(Ly.x), false, F(Ly.xf), false, P.Na, d);
+  rms_fwd(Ly.xf, gfa, Ly.yb);
+  rows_gemm(EPI_F32, B(Ly.yb), d, [&](int32_t g) { return B(Ly.woutp) + (int64_t)g * 32 * d; }, 32, F(Ly.predp), 32,
+            true);
+  {
+    std::vector<XLossDesc> v(G);
+    for (int32_t g = 0; g < G; ++g) v[g] = XLossDesc{io[g].targets, io[g].pred, io[g].loss, ex[g].action_dim, 0};
+    const size_t at = rec.add(v.data(), sizeof(XLossDesc) * G);
+    rec.ops.push_back([=](char* a) {
+      return launch_xloss(s, (const XLossDesc*)(a + at), (const int32_t*)(a + roff_at), G, F(Ly.predp), 32,
+                          F(Ly.dpred));
+    });
+    rec.opcode.push_back(JN_OP_LOSS);
+  }
+
+  // --------------------------------------------------------------- backward
+  rows_copy(F(Ly.dpred), false, B(Ly.dpredb), true, P.Na, 32);
+  trans_rows(B(Ly.dpredb), 32, B(Ly.TA), false);
+  trans_rows(B(Ly.yb), d, B(Ly.TB), false);
+  wgrad(32, d, [&](int32_t g) { return F(Ly.dwoutp) + (int64_t)g * 32 * d; }, false);
+  rows_gemm(EPI_F32, B(Ly.dpredb), 32, [&](int32_t g) { return B(Ly.woutpT) + (int64_t)g * d * 32; }, d, F(Ly.tf), d,
+            true);
+  rows_copy(nullptr, false, F(Ly.dx), false, P.Na, d);  // dx = 0
+  rms_bwd(Ly.xf, gfa, ptr_table([&](int32_t g) { return (const void*)io[g].dgf; }));
+  for (int l = S.L - 1; l >= 0; --l) {
+    const size_t g1 = ptr_table([&](int32_t g) { return ex[g].layers[l].g1; });
+    const size_t g2 = ptr_table([&](int32_t g) { return ex[g].layers[l].g2; });
+    const size_t g3 = ptr_table([&](int32_t g) { return ex[g].layers[l].g3; });
+    // MLP block: x += m W_down^T, m = gelu(h3 W_up^T)
+    rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
+    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
+    trans_rows(B(Ly.mb[l]), f, B(Ly.TB), false);
+    wgrad(d, f, Gl(l, &jn_expert_layer_grads::w_down), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].w_down; }, d, f);
+    rows_gemm(EPI_GELUGRAD_BF16, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, f); }, f, B(Ly.tb), f,
+              false, F(Ly.pre[l]));
+    trans_rows(B(Ly.tb), f, B(Ly.TA), false);
+    trans_rows(B(Ly.h3[l]), d, B(Ly.TB), false);
+    wgrad(f, d, Gl(l, &jn_expert_layer_grads::w_up), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].w_up; }, f, d);
+    rows_gemm(EPI_F32, B(Ly.tb), f, [&](int32_t g) { return (const uint16_t*)WTg(g, f, d); }, d, F(Ly.tf), d, true);
+    rms_bwd(Ly.x3[l], g3, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g3; }));
+    // cross-attention block
+    rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
+    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
+    trans_rows(B(Ly.ocb[l]), d, B(Ly.TB), false);
+    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wo_c), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].wo_c; }, d, d);
+    rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
+    {
+      AttnArgs A{};
+      A.Q = F(Ly.qc[l]);
+      A.K = F(Ly.kv[l]);
+      A.V = F(Ly.kv[l]);
+      A.O = F(Ly.oc[l]);
+      A.lse = F(Ly.lsec[l]);
+      A.dO = F(Ly.tf);
+      A.dQ = F(Ly.tq);
+      A.dK = F(Ly.dkv);
+      A.dV = F(Ly.dkv);
+      A.zoff = (const int32_t*)(w + Ly.zoff);
+      A.kv_cap = P.Pzt;
+      A.ldq = d;
+      A.ldkv = 2 * d;
+      A.ldo = d;
+      A.lddq = d;
+      A.lddkv = 2 * d;
+      A.kcol = 0;
+      A.vcol = (int32_t)d;
+      A.dkcol = 0;
+      A.dvcol = (int32_t)d;
+      A.Lq = S.chunk;
+      A.hd = (int32_t)(d / H);
+      A.nheads = (int32_t)H;
+      A.scale = scale;
+      attn(A, true);
+    }
+    rows_copy(F(Ly.tq), false, B(Ly.tb), true, P.Na, d);
+    rows_copy(F(Ly.dkv), false, B(Ly.dkvb), true, P.Pzt, 2 * d);
+    trans_rows(B(Ly.tb), d, B(Ly.TA), false);
+    trans_rows(B(Ly.h2[l]), d, B(Ly.TB), false);
+    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wq_c), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].wq_c; }, d, d);
+    rows_gemm(EPI_F32, B(Ly.tb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
+    trans_rows(B(Ly.dkvb), 2 * d, B(Ly.TA), true);
+    trans_rows(B(Ly.z), dp, B(Ly.TB), true);
+    wgrad(2 * d, dp, Gl(l, &jn_expert_layer_grads::wkv_c), true);
+    rms_bwd(Ly.x2[l], g2, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g2; }));
+    // self-attention block
+    rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
+    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
+    trans_rows(B(Ly.osb[l]), d, B(Ly.TB), false);
+    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wo_s), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].wo_s; }, d, d);
+    rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
+    {
+      AttnArgs A{};
+      A.Q = F(Ly.qkv[l]);
+      A.K = F(Ly.qkv[l]);
+      A.V = F(Ly.qkv[l]);
+      A.O = F(Ly.os[l]);
+      A.lse = F(Ly.lses[l]);
+      A.dO = F(Ly.tf);
+      A.dQ = F(Ly.tq);
+      A.dK = F(Ly.tq);
+      A.dV = F(Ly.tq);
+      A.ldq = 3 * d;
+      A.ldkv = 3 * d;
+      A.ldo = d;
+      A.lddq = 3 * d;
+      A.lddkv = 3 * d;
+      A.kcol = (int32_t)d;
+      A.vcol = (int32_t)(2 * d);
+      A.dkcol = (int32_t)d;
+      A.dvcol = (int32_t)(2 * d);
+      A.Lq = S.chunk;
+      A.hd = (int32_t)(d / H);
+      A.nheads = (int32_t)H;
+      A.scale = scale;
+      attn(A, true);
+    }
+    rows_copy(F(Ly.tq), false, B(Ly.tb), true, P.Na, 3 * d);
+    trans_rows(B(Ly.tb), 3 * d, B(Ly.TA), false);
+    trans_rows(B(Ly.h1[l]), d, B(Ly.TB), false);
+    wgrad(3 * d, d, Gl(l, &jn_expert_layer_grads::wqkv_s), false);
+    trans_w([&](int32_t g) { return ex[g].layers[l].wqkv_s; }, 3 * d, d);
+    rows_gemm(EPI_F32, B(Ly.tb), 3 * d, [&](int32_t g) { return (const uint16_t*)WTg(g, 3 * d, d); }, d, F(Ly.tf), d,
+              true);
+    rms_bwd(Ly.x1[l], g1, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g1; }));
+  }
+  // input projection and the padded output-projection gradient
+  rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
+  trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
+  trans_rows(B(Ly.ub), 32, B(Ly.TB), false);
+  wgrad(d, 32, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * 32; }, false);
+  {
+    std::vector<CopyDesc> v;
+    for (int32_t g = 0; g < G; ++g) {
+      const int32_t a = ex[g].action_dim;
+      v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * 32, io[g].dw_in, 32, a, (int32_t)d, a, (int32_t)d, a, 0, 0, 0, 0});
+      v.push_back(CopyDesc{F(Ly.dwoutp) + (int64_t)g * 32 * d, io[g].dw_out, d, d, a, (int32_t)d, a, (int32_t)d, 0, 0, 0, 0});
+    }
+    copy(v);
+  }
+  if (rec.overflow) return fail(c, JN_ENOSPACE, "internal: expert descriptor arena too small");
+
+  // ---- one upload of every table, then the launches in order
+  st = stage_copy(c, darena, rec.img.data(), rec.img.size());
+  if (st != JN_OK) return st;
+  for (size_t i = 0; i < rec.ops.size(); ++i) {
+    auto& op = rec.ops[i];
+    JN_TRACED(c, rec.opcode[i], P.Na, d, 0, op(darena), "expert launch");
+  }
   return JN_OK;
 }
 

@@ -42,11 +42,34 @@ hipError_t launch_rmsnorm_f32in(hipStream_t s, const float* x, const void* g, vo
                                 int32_t d, float eps);
 
 enum GemmEpi : int32_t {
-  EPI_BF16 = 0,       // C bf16 = acc
-  EPI_GELU_BF16 = 1,  // C bf16 = gelu(acc)
-  EPI_RESID_F32 = 2,  // C fp32 += acc
-  EPI_GEGLU_BF16 = 3  // weights gate|up interleaved at load; C bf16 = gelu(gate) * up
+  EPI_BF16 = 0,          // C bf16 = acc
+  EPI_GELU_BF16 = 1,     // C bf16 = gelu(acc)
+  EPI_RESID_F32 = 2,     // C fp32 += acc
+  EPI_GEGLU_BF16 = 3,    // weights gate|up interleaved at load; C bf16 = gelu(gate) * up
+  EPI_F32 = 4,           // C fp32 = acc
+  EPI_GELU_SAVE = 5,     // aux fp32 = acc; C bf16 = gelu(acc)
+  EPI_GELUGRAD_BF16 = 6  // C bf16 = acc * gelu'(aux fp32)
 };
+
+// One GEMM problem: C[M][N] (+)= epi(X[M][K] W[N][K]^T); bf16 X, W row-major.
+struct GemmArgs {
+  const uint16_t* X;
+  const uint16_t* W;
+  const uint16_t* W2;   // GeGLU up weights
+  void* C;
+  float* aux;           // GELU pre-activation (saved or read)
+  int64_t ldx, ldw, ldc, ldaux;
+  int32_t M, N, K;
+  int32_t tiles_m, tiles_n, tile_start;  // filled by the launchers
+};
+
+// Grouped launch over nprob problems sharing one epilogue: the host fills
+// the problems, calls gemm_grouped_prepare (tile ranges, returns the tile
+// total), uploads them and launches.  shape from gemm_grouped_tile_shape.
+int gemm_grouped_tile_shape(int32_t max_m);
+int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape);
+hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
+                               int shape);
 
 // C[M][N] (+)= epi(A[M][K] * B[N][K]^T); A, B bf16 row-major with leading
 // dims lda, ldb (elements); for EPI_GEGLU_BF16, B is w_gate and B2 is w_up,
@@ -114,5 +137,73 @@ struct LossDesc {
   int32_t reserved;
 };
 hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tenant_sample_off);
+
+// ---- action expert (k_expert.hip) ----
+// dst[r][c] = cvt(src[r][c]) for r < src_rows, c < src_cols, else 0; r < rows, c < cols.
+struct CopyDesc {
+  const void* src;
+  void* dst;
+  int64_t src_ld, dst_ld;
+  int32_t rows, cols, src_rows, src_cols;
+  int32_t src_bf16, dst_bf16;
+  int32_t block_start, reserved;
+};
+int32_t copy2d_prepare(CopyDesc* d, int32_t n);
+hipError_t launch_copy2d(hipStream_t s, const CopyDesc* d, int32_t n, int32_t blocks);
+
+// bf16 dst[c][r] = src[r][c] (r < rows), 0 for rows <= r < rows_pad; c < cols.
+struct TransDesc {
+  const uint16_t* src;
+  uint16_t* dst;
+  int64_t src_ld, dst_ld;
+  int32_t rows, cols, rows_pad, block_start;
+};
+int32_t transpose_prepare(TransDesc* d, int32_t n);
+hipError_t launch_transpose(hipStream_t s, const TransDesc* d, int32_t n, int32_t blocks);
+
+// zoff[k] for tenant-order samples k (prefix sums of their valid lengths) and
+// the tenant-ordered copy z of their backbone rows (rows >= cap dropped).
+hipError_t launch_prefix(hipStream_t s, const void* hidden, const int32_t* tenant_perm, const int32_t* seqlens,
+                         const int32_t* cu_seqlens, int32_t N, int32_t max_seqlen, int32_t d, int64_t cap,
+                         int32_t* zoff, void* z);
+
+// RMSNorm with per-tenant gains (rows tenant-contiguous, roff [G+1] device).
+hipError_t launch_xrms_fwd(hipStream_t s, const float* x, const void* const* gains, const int32_t* roff, int32_t G,
+                           int32_t rows, int32_t d, float eps, void* h);
+// dx += dRMS(x, g) . dh ; dg[t] = column sums over tenant t's rows (gx scratch [rows][d]).
+hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gains, const int32_t* roff, int32_t G,
+                           int32_t rows, int32_t d, float eps, const float* dh, float* dx, float* gx,
+                           float* const* dg);
+
+// fp32 attention of each tenant-order sample k over its own keys: queries
+// rows [k*Lq, (k+1)*Lq) of Q; keys / values rows [kv0, kv0 + Lk) with
+// kv0 = zoff[k], Lk = zoff[k+1] - zoff[k] (cross, clamped to kv_cap) or the
+// sample's own query rows (self, zoff null).
+struct AttnArgs {
+  const float* Q;
+  const float* K;
+  const float* V;
+  float* O;        // forward output / backward input
+  float* lse;      // forward output / backward input, [rows][nheads]
+  const float* dO;
+  float* dQ;
+  float* dK;
+  float* dV;
+  const int32_t* zoff;
+  int64_t ldq, ldkv, ldo, lddq, lddkv, kv_cap;
+  int32_t kcol, vcol, dkcol, dvcol;
+  int32_t Lq, hd, nheads, reserved;
+  float scale;
+};
+hipError_t launch_xattn(hipStream_t s, const AttnArgs& A, int32_t nsamples, bool backward);
+
+struct XLossDesc {
+  const float* target;  // [rows_t][a]
+  float* pred;          // [rows_t][a]
+  float* loss;          // [1]
+  int32_t a, reserved;
+};
+hipError_t launch_xloss(hipStream_t s, const XLossDesc* d, const int32_t* roff, int32_t G, const float* pred_pad,
+                        int32_t ldp, float* dpred_pad);
 
 }  // namespace jnx

@@ -75,12 +75,13 @@ __device__ __forceinline__ void gemm_mfma(f32x16 (&acc)[TN][TM], const bf16x8 (&
 }
 
 template <int BN, int BM, int WGN, int WGM, int EPI>
-__global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(const uint16_t* __restrict__ X, int64_t ldx,
-                                                                 const uint16_t* __restrict__ W,
-                                                                 const uint16_t* __restrict__ W2, int64_t ldw,
-                                                                 void* __restrict__ C, int64_t ldc, int32_t M,
-                                                                 int32_t N, int32_t K, int32_t tiles_m,
-                                                                 int32_t tiles_n) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16_t* __restrict__ lds) {
+  const uint16_t* __restrict__ X = g.X;
+  const uint16_t* __restrict__ W = g.W;
+  const uint16_t* __restrict__ W2 = g.W2;
+  void* __restrict__ C = g.C;
+  const int64_t ldx = g.ldx, ldw = g.ldw, ldc = g.ldc;
+  const int32_t M = g.M, N = g.N, K = g.K, tiles_n = g.tiles_n, tiles_m = g.tiles_m;
   constexpr bool GLU = EPI == EPI_GEGLU_BF16;
   constexpr int NW = WGN * WGM;              // wavefronts
   constexpr int WN = BN / WGN, WM = BM / WGM;  // per-wave tile
@@ -90,10 +91,8 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(const uint16_t*
   constexpr int STAGE = ROWS * kBK;          // elements per stage
   static_assert(ROWS % (16 * NW) == 0 && TN >= 1 && TM >= 1, "tile shape");
   static_assert(!GLU || TN % 2 == 0, "GeGLU pairs gate/up tiles inside a wave");
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * STAGE];
 
   // ---- grouped tile order
-  const int32_t pid = blockIdx.x;
   const int32_t per_group = kGroupM * tiles_n;
   const int32_t group = pid / per_group;
   const int32_t first_m = group * kGroupM;
@@ -237,6 +236,23 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(const uint16_t*
             o.z += v[2];
             o.w += v[3];
             *p = o;
+          } else if constexpr (EPI == EPI_F32) {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n) =
+                make_float4(v[0], v[1], v[2], v[3]);
+          } else if constexpr (EPI == EPI_GELU_SAVE) {
+            *reinterpret_cast<float4*>(g.aux + (int64_t)m * g.ldaux + n) = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+                make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+          } else if constexpr (EPI == EPI_GELUGRAD_BF16) {
+            const float4 z = *reinterpret_cast<const float4*>(g.aux + (int64_t)m * g.ldaux + n);
+            v[0] *= gelu_grad_f(z.x);
+            v[1] *= gelu_grad_f(z.y);
+            v[2] *= gelu_grad_f(z.z);
+            v[3] *= gelu_grad_f(z.w);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+                make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
           } else {
             if constexpr (EPI == EPI_GELU_BF16) {
 #pragma unroll
@@ -251,25 +267,61 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(const uint16_t*
   }
 }
 
+template <int BN, int BM, int WGN, int WGM, int EPI>
+__global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * (BN + BM) * kBK];
+  gemm_tile<BN, BM, WGN, WGM, EPI>(g, blockIdx.x, lds);
+}
+
+// One launch over several independent problems (one per tenant): block b
+// runs tile b - tile_start[p] of the problem p whose tile range holds b.
+template <int BN, int BM, int WGN, int WGM, int EPI>
+__global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_grouped_kernel(const GemmArgs* __restrict__ probs,
+                                                                         int32_t nprob) {
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * (BN + BM) * kBK];
+  const int32_t b = blockIdx.x;
+  int32_t p = 0;
+  while (p + 1 < nprob && probs[p + 1].tile_start <= b) ++p;
+  const GemmArgs g = probs[p];
+  gemm_tile<BN, BM, WGN, WGM, EPI>(g, b - g.tile_start, lds);
+}
+
 template <int BN, int BM, int WGN, int WGM>
-static hipError_t launch_tile(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2,
-                              int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K) {
-  const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * N : N;
-  const int32_t tiles_m = (M + BM - 1) / BM, tiles_n = (NL + BN - 1) / BN;
-  dim3 grid(tiles_m * tiles_n), block(64 * WGN * WGM);
-  auto X = reinterpret_cast<const uint16_t*>(A);
-  auto Wp = reinterpret_cast<const uint16_t*>(B);
-  auto W2 = reinterpret_cast<const uint16_t*>(B2);
-#define JN_GEMM_CASE(E)                                                                                  \
-  case E:                                                                                                \
-    gemm_kernel<BN, BM, WGN, WGM, E><<<grid, block, 0, s>>>(X, lda, Wp, W2, ldb, C, ldc, M, N, K, tiles_m, \
-                                                            tiles_n);                                    \
-    break;
+static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g) {
+  const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
+  g.tiles_m = (g.M + BM - 1) / BM;
+  g.tiles_n = (NL + BN - 1) / BN;
+  g.tile_start = 0;
+  dim3 grid(g.tiles_m * g.tiles_n), block(64 * WGN * WGM);
+#define JN_GEMM_CASE(E) \
+  case E: gemm_kernel<BN, BM, WGN, WGM, E><<<grid, block, 0, s>>>(g); break;
   switch (epi) {
     JN_GEMM_CASE(EPI_BF16)
     JN_GEMM_CASE(EPI_GELU_BF16)
     JN_GEMM_CASE(EPI_RESID_F32)
     JN_GEMM_CASE(EPI_GEGLU_BF16)
+    JN_GEMM_CASE(EPI_F32)
+    JN_GEMM_CASE(EPI_GELU_SAVE)
+    JN_GEMM_CASE(EPI_GELUGRAD_BF16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef JN_GEMM_CASE
+  return hipGetLastError();
+}
+
+template <int BN, int BM, int WGN, int WGM>
+static hipError_t launch_grouped_tile(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob,
+                                      int32_t total_tiles) {
+  dim3 grid(total_tiles), block(64 * WGN * WGM);
+#define JN_GEMM_CASE(E) \
+  case E: gemm_grouped_kernel<BN, BM, WGN, WGM, E><<<grid, block, 0, s>>>(dprobs, nprob); break;
+  switch (epi) {
+    JN_GEMM_CASE(EPI_BF16)
+    JN_GEMM_CASE(EPI_RESID_F32)
+    JN_GEMM_CASE(EPI_F32)
+    JN_GEMM_CASE(EPI_GELU_SAVE)
+    JN_GEMM_CASE(EPI_GELUGRAD_BF16)
     default:
       return hipErrorInvalidValue;
   }
@@ -300,12 +352,44 @@ int gemm_pick_tile(int epi, int32_t M, int32_t N) {
 hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2, int64_t ldb,
                        void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int tile_hint) {
   if (M <= 0 || N <= 0 || K <= 0 || K % kBK != 0 || N % 32 != 0) return hipErrorInvalidValue;
+  GemmArgs g{};
+  g.X = reinterpret_cast<const uint16_t*>(A);
+  g.W = reinterpret_cast<const uint16_t*>(B);
+  g.W2 = reinterpret_cast<const uint16_t*>(B2);
+  g.C = C;
+  g.ldx = lda;
+  g.ldw = ldb;
+  g.ldc = ldc;
+  g.M = M;
+  g.N = N;
+  g.K = K;
   const int t = tile_hint > 0 ? tile_hint - 1 : gemm_pick_tile(epi, M, N);
   switch (t) {
-    case 0: return launch_tile<256, 256, 2, 4>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
-    case 1: return launch_tile<256, 128, 4, 2>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
-    default: return launch_tile<128, 128, 2, 2>(s, epi, A, lda, B, B2, ldb, C, ldc, M, N, K);
+    case 0: return launch_tile<256, 256, 2, 4>(s, epi, g);
+    case 1: return launch_tile<256, 128, 4, 2>(s, epi, g);
+    default: return launch_tile<128, 128, 2, 2>(s, epi, g);
   }
+}
+
+int gemm_grouped_tile_shape(int32_t max_m) { return max_m >= 1024 ? 1 : 2; }
+
+int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
+  const int BN = shape == 1 ? 256 : 128, BM = 128;
+  int32_t total = 0;
+  for (int32_t p = 0; p < nprob; ++p) {
+    probs[p].tiles_m = (probs[p].M + BM - 1) / BM;
+    probs[p].tiles_n = (probs[p].N + BN - 1) / BN;
+    probs[p].tile_start = total;
+    total += probs[p].tiles_m * probs[p].tiles_n;
+  }
+  return total;
+}
+
+hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
+                               int shape) {
+  if (nprob <= 0 || total_tiles <= 0) return hipErrorInvalidValue;
+  if (shape == 1) return launch_grouped_tile<256, 128, 4, 2>(s, epi, dprobs, nprob, total_tiles);
+  return launch_grouped_tile<128, 128, 2, 2>(s, epi, dprobs, nprob, total_tiles);
 }
 
 }  // namespace jnx

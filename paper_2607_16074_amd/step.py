@@ -6,6 +6,9 @@ tenant's head, allocates the buffers a given group of requests needs once
 
     jn_pack_group -> jn_backbone_forward -> jn_tenant_heads_fwd_bwd -> jn_unpack
 
+(``jn_tenant_experts_fwd_bwd`` in place of the heads call when the group's
+tenants carry action experts)
+
 on one stream (``run``) with no allocation and no host synchronisation.
 ``isolated_runs`` builds one such step per tenant over the same device
 weights: the serial-execution comparator of grouped execution, using the
@@ -17,8 +20,10 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from . import (Backbone, Context, Head, HeadIO, Request, Tenant, jn_backbone_forward, jn_backbone_workspace_size,
-               jn_heads_workspace_size, jn_pack_group, jn_pack_plan, jn_tenant_heads_fwd_bwd, jn_unpack)
+from . import (EXPERT_LAYER_FIELDS, Backbone, Context, Expert, ExpertIO, Head, HeadIO, Request, Tenant,
+               jn_backbone_forward, jn_backbone_workspace_size, jn_experts_workspace_size, jn_heads_workspace_size,
+               jn_pack_group, jn_pack_plan, jn_pack_tenant_sizes, jn_tenant_experts_fwd_bwd, jn_tenant_heads_fwd_bwd,
+               jn_unpack)
 
 
 def _dev_bf16(bits: np.ndarray, device):
@@ -33,34 +38,51 @@ def _dev_f32(a: np.ndarray, device):
 
 
 class Model:
-    """Device weights: frozen backbone + per-tenant heads."""
+    """Device weights: frozen backbone + per-tenant heads or action experts."""
 
-    def __init__(self, backbone: Backbone, heads: List[Head], tenant_meta: List[dict], prefix_sig: int):
+    def __init__(self, backbone: Backbone, heads: List[Optional[Head]], tenant_meta: List[dict], prefix_sig: int,
+                 experts: Optional[List[Optional[Expert]]] = None):
         self.backbone = backbone
         self.heads = heads
+        self.experts = experts or [None] * len(heads)
         self.tenant_meta = tenant_meta  # action_dim, chunk per tenant
         self.prefix_sig = prefix_sig
 
     @classmethod
     def from_arrays(cls, layers: List[dict], gf: np.ndarray, n_heads: int, eps: float,
-                    heads: List[list], tenant_meta: List[dict], prefix_sig: int, device="cuda"):
+                    heads: List[Optional[list]], tenant_meta: List[dict], prefix_sig: int, device="cuda",
+                    experts: Optional[List[Optional[dict]]] = None):
         """``layers``: per layer dict of bf16 bit arrays; ``heads``: per tenant
-        list of (W fp32 [out,in], b fp32 [out])."""
+        list of (W fp32 [out,in], b fp32 [out]) or None; ``experts``: per
+        tenant None or a dict of bf16 bit arrays (w_in, w_out, gf, layers)
+        with ``tenant_meta[g]["expert_heads"]`` attention heads."""
         dl = [{k: _dev_bf16(v, device) for k, v in L.items()} for L in layers]
         bb = Backbone(dl, _dev_bf16(gf, device), n_heads, eps)
-        hs = []
+        hs, xs = [], []
         for g, layers_g in enumerate(heads):
-            W = [_dev_f32(w, device) for w, _ in layers_g]
-            b = [_dev_f32(x, device) for _, x in layers_g]
-            hs.append(Head(W, b, tenant_meta[g]["action_dim"], tenant_meta[g]["chunk"]))
-        return cls(bb, hs, tenant_meta, prefix_sig)
+            if layers_g is None:
+                hs.append(None)
+            else:
+                W = [_dev_f32(w, device) for w, _ in layers_g]
+                b = [_dev_f32(x, device) for _, x in layers_g]
+                hs.append(Head(W, b, tenant_meta[g]["action_dim"], tenant_meta[g]["chunk"]))
+            e = experts[g] if experts is not None else None
+            if e is None:
+                xs.append(None)
+            else:
+                xl = [{k: _dev_bf16(v, device) for k, v in L.items()} for L in e["layers"]]
+                xs.append(Expert(_dev_bf16(e["w_in"], device), _dev_bf16(e["w_out"], device),
+                                 _dev_bf16(e["gf"], device), xl, tenant_meta[g]["expert_heads"],
+                                 tenant_meta[g]["chunk"], bb.d, eps))
+        return cls(bb, hs, tenant_meta, prefix_sig, xs)
 
 
 class GroupStep:
     """One group of requests over a subset of tenants, buffers allocated once."""
 
     def __init__(self, model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
-                 tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda"):
+                 tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda",
+                 noisy: Optional[Dict[int, np.ndarray]] = None):
         import torch
         self.model = model
         self.ctx = ctx or Context()
@@ -77,22 +99,43 @@ class GroupStep:
         self.tokens = torch.empty((self.T, d), dtype=torch.bfloat16, device=device)
         self.hidden = torch.empty((self.T, d), dtype=torch.bfloat16, device=device)
         self.bb_ws = torch.empty(jn_backbone_workspace_size(model.backbone, self.T), dtype=torch.uint8, device=device)
+        self.experts = [model.experts[g] for g in self.tenants]
+        self.use_experts = self.experts[0] is not None
+        if any((x is not None) != self.use_experts for x in self.experts):
+            raise ValueError("a group mixes expert tenants with MLP-head tenants")
         self.heads = [model.heads[g] for g in self.tenants]
         self.pooled = torch.empty((self.N, d), dtype=torch.float32, device=device)
-        self.ios = []
-        for k, g in enumerate(self.tenants):
-            h = model.heads[g]
-            n_g = int(sum(r.n for r in self.requests if r.tenant == k))
-            tgt = _dev_f32(targets[g], device)
-            acts = torch.empty((n_g, int(h.dims[-1])), dtype=torch.float32, device=device)
-            loss = torch.empty(1, dtype=torch.float32, device=device)
-            dW = [torch.empty_like(w) for w in h.W]
-            db = [torch.empty_like(x) for x in h.b]
-            self.ios.append(HeadIO(tgt, acts, loss, dW, db))
         self.out_hidden = [torch.empty((r.n, r.max_len, d), dtype=torch.bfloat16, device=device) for r in self.requests]
-        # pack once to size the head workspace from a real packed batch
+        # pack once to size the tenant-stage workspace from a real packed batch
         self.packed = jn_pack_group(self.ctx, self.requests, self.table, d, align, self.maps, self.tokens)
-        self.hd_ws = torch.empty(jn_heads_workspace_size(self.packed, self.heads), dtype=torch.uint8, device=device)
+        self.ios = []
+        if self.use_experts:
+            n_s, rows = jn_pack_tenant_sizes(self.requests, self.table, d, align)
+            for k, g in enumerate(self.tenants):
+                e = model.experts[g]
+                w_in, w_out, gf, xl = e.w_in, e.w_out, e.gf, e.layers
+                f32 = lambda t: torch.empty(t.shape, dtype=torch.float32, device=device)  # noqa: E731
+                shape = (int(n_s[k]), e.struct.chunk, e.struct.action_dim)
+                self.ios.append(ExpertIO(int(n_s[k]), int(rows[k]), _dev_f32(noisy[g], device).reshape(shape),
+                                         _dev_f32(targets[g], device).reshape(shape),
+                                         torch.empty(shape, dtype=torch.float32, device=device),
+                                         torch.empty(1, dtype=torch.float32, device=device),
+                                         f32(w_in), f32(w_out), f32(gf),
+                                         [{k2: f32(L[k2]) for k2 in EXPERT_LAYER_FIELDS} for L in xl]))
+            self.hd_ws = torch.empty(jn_experts_workspace_size(self.packed, self.experts, self.ios), dtype=torch.uint8,
+                                     device=device)
+        else:
+            for k, g in enumerate(self.tenants):
+                h = model.heads[g]
+                n_g = int(sum(r.n for r in self.requests if r.tenant == k))
+                tgt = _dev_f32(targets[g], device)
+                acts = torch.empty((n_g, int(h.dims[-1])), dtype=torch.float32, device=device)
+                loss = torch.empty(1, dtype=torch.float32, device=device)
+                dW = [torch.empty_like(w) for w in h.W]
+                db = [torch.empty_like(x) for x in h.b]
+                self.ios.append(HeadIO(tgt, acts, loss, dW, db))
+            self.hd_ws = torch.empty(jn_heads_workspace_size(self.packed, self.heads), dtype=torch.uint8,
+                                     device=device)
         self.valid_tokens = int(sum(int(r.lengths.sum()) for r in self.requests))
 
     # the four calls -------------------------------------------------------
@@ -104,7 +147,11 @@ class GroupStep:
         jn_backbone_forward(self.ctx, self.model.backbone, self.packed, self.hidden, self.bb_ws)
 
     def heads_fwd_bwd(self):
-        jn_tenant_heads_fwd_bwd(self.ctx, self.packed, self.hidden, self.heads, self.ios, self.hd_ws, self.pooled)
+        if self.use_experts:
+            jn_tenant_experts_fwd_bwd(self.ctx, self.packed, self.hidden, self.experts, self.ios, self.hd_ws)
+        else:
+            jn_tenant_heads_fwd_bwd(self.ctx, self.packed, self.hidden, self.heads, self.ios, self.hd_ws,
+                                    self.pooled)
 
     def unpack(self):
         d = self.model.backbone.d
@@ -118,31 +165,42 @@ class GroupStep:
 
 
 def isolated_runs(model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
-                  tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda"):
+                  tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda",
+                  noisy: Optional[Dict[int, np.ndarray]] = None):
     """One ``GroupStep`` per tenant (its own requests only), sharing the weights."""
     ctx = ctx or Context()
     out = []
     for g in tenants:
         reqs = [r for r in requests if r.tenant == g]
-        out.append(GroupStep(model, reqs, targets, [g], align, ctx, device))
+        out.append(GroupStep(model, reqs, targets, [g], align, ctx, device, noisy))
     return out
 
 
-def from_workload(wl, device="cuda"):
+def from_workload(wl, device="cuda", with_noisy: bool = False):
     """Device model, requests and targets from a workload description.
 
     ``wl`` needs: ``spec`` (backbone: layers/d/heads/eps; tenants: action_dim,
     chunk, schema_sig), ``layers``, ``gf``, ``heads``, ``targets`` and
-    ``requests`` (tenant, lengths, embeds bf16 bits, first).
+    ``requests`` (tenant, lengths, embeds bf16 bits, first); for action-expert
+    tenants also ``experts`` and ``noisy``.  ``with_noisy`` adds a fourth
+    result: every expert tenant's noisy action tokens in arrival order.
     """
     spec = wl.spec
-    meta = [{"action_dim": t.action_dim, "chunk": t.chunk} for t in spec.tenants]
+    meta = [{"action_dim": t.action_dim, "chunk": t.chunk,
+             "expert_heads": t.expert[2] if t.expert is not None else 0} for t in spec.tenants]
     model = Model.from_arrays(wl.layers, wl.gf, spec.backbone.heads, spec.backbone.eps, wl.heads, meta,
-                              spec.tenants[0].schema_sig, device)
+                              spec.tenants[0].schema_sig, device, getattr(wl, "experts", None))
     reqs = [Request(r.tenant, _dev_bf16(r.embeds, device), r.lengths) for r in wl.requests]
-    targets = {}
+    targets, noisy = {}, {}
     for g in range(spec.G):
-        idx = [k for r in wl.requests if r.tenant == g for k in range(r.first, r.first + r.n)]
-        t = np.asarray(wl.targets[g], np.float32)[np.array(idx, dtype=np.int64)]
-        targets[g] = t.reshape(len(idx), -1)
+        idx = np.array([k for r in wl.requests if r.tenant == g for k in range(r.first, r.first + r.n)],
+                       dtype=np.int64)
+        t = np.asarray(wl.targets[g], np.float32)[idx]
+        if spec.tenants[g].expert is None:
+            targets[g] = t.reshape(len(idx), -1)
+        else:
+            targets[g] = t
+            noisy[g] = np.asarray(wl.noisy[g], np.float32)[idx]
+    if with_noisy:
+        return model, reqs, targets, noisy
     return model, reqs, targets

@@ -36,7 +36,10 @@ def test_struct_layout_matches_c(tmp_path, lib):
     from paper_2607_16074_amd import _abi
     structs = {"jn_request": _abi.jn_request, "jn_tenant": _abi.jn_tenant, "jn_pack_opts": _abi.jn_pack_opts,
                "jn_pack_sizes": _abi.jn_pack_sizes, "jn_packed": _abi.jn_packed, "jn_layer": _abi.jn_layer,
-               "jn_backbone": _abi.jn_backbone, "jn_head": _abi.jn_head, "jn_head_io": _abi.jn_head_io}
+               "jn_backbone": _abi.jn_backbone, "jn_head": _abi.jn_head, "jn_head_io": _abi.jn_head_io,
+               "jn_expert_layer": _abi.jn_expert_layer, "jn_expert": _abi.jn_expert,
+               "jn_expert_layer_grads": _abi.jn_expert_layer_grads, "jn_expert_io": _abi.jn_expert_io,
+               "jn_trace_entry": _abi.jn_trace_entry}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "joynexus.h"', "int main(void){"]
     for name, cls in structs.items():
         lines.append(f'printf("{name} %zu\\n", sizeof({name}));')
@@ -119,3 +122,90 @@ def test_host_plan_errors(lib):
     with pytest.raises(lib.JNError) as e:
         lib.jn_pack_plan(_reqs(lib, [0], [[2]], [4]), T(), d, 0)
     assert e.value.status == lib._abi.JN_EINVAL
+
+
+# ------------------------------------------------------ expert validation ---
+
+def test_pack_tenant_sizes_match_plan(lib):
+    rng = np.random.default_rng(11)
+    for trial in range(10):
+        G = int(rng.integers(1, 5))
+        R = int(rng.integers(G, 2 * G + 2))
+        tn = list(rng.permutation(np.concatenate([np.arange(G), rng.integers(0, G, R - G)])))
+        mls = [int(rng.integers(1, 200)) for _ in range(R)]
+        lens = [list(rng.integers(1, m + 1, size=int(rng.integers(1, 6)))) for m in mls]
+        align = int(rng.choice([1, 16, 64]))
+        n, rows = lib.jn_pack_tenant_sizes(_reqs(lib, tn, lens, mls), [lib.Tenant(1, 128)] * G, 128, align)
+        for g in range(G):
+            mine = [l for t, ls in zip(tn, lens) if t == g for l in ls]
+            assert n[g] == len(mine) and rows[g] == sum(mine), (trial, g)
+
+
+def _host_packed(lib, tn, lens, mls, G, d):
+    """A jn_packed whose maps live in host memory (enough for size queries)."""
+    import ctypes as C
+    sz = lib.jn_pack_plan(_reqs(lib, tn, lens, mls), [lib.Tenant(1, d)] * G, d, 1)
+    buf = np.zeros(int(sz.map_bytes), dtype=np.uint8)
+    ra, keep = lib._requests(_reqs(lib, tn, lens, mls))
+    out = lib._abi.jn_packed()
+    st = lib._lib.jn_pack_maps_host(ra, len(tn), lib._tenants([lib.Tenant(1, d)] * G), G,
+                                    C.byref(lib._opts(d, 1)), buf.ctypes.data_as(C.c_void_p), buf.nbytes,
+                                    C.byref(out))
+    assert st == 0
+    return lib.Packed(out, buf, None), buf, keep
+
+
+def _fake_expert(lib, d=256, H=4, f=512, L=1, a=7, chunk=10, dp=128):
+    import torch
+    e = lambda *s: torch.zeros(s, dtype=torch.bfloat16)  # noqa: E731
+    layers = [{"wqkv_s": e(3 * d, d), "wo_s": e(d, d), "wq_c": e(d, d), "wkv_c": e(2 * d, dp), "wo_c": e(d, d),
+               "w_up": e(f, d), "w_down": e(d, f), "g1": e(d), "g2": e(d), "g3": e(d)} for _ in range(L)]
+    return lib.Expert(e(d, a), e(a, d), e(d), layers, H, chunk, dp, 1e-6)
+
+
+def _fake_io(lib, n, rows, d=256, f=512, L=1, a=7, chunk=10, dp=128):
+    import torch
+    z = lambda *s: torch.zeros(s, dtype=torch.float32)  # noqa: E731
+    layers = [{"wqkv_s": z(3 * d, d), "wo_s": z(d, d), "wq_c": z(d, d), "wkv_c": z(2 * d, dp), "wo_c": z(d, d),
+               "w_up": z(f, d), "w_down": z(d, f), "g1": z(d), "g2": z(d), "g3": z(d)} for _ in range(L)]
+    return lib.ExpertIO(n, rows, z(n, chunk, a), z(n, chunk, a), z(n, chunk, a), z(1), z(d, a), z(a, d), z(d),
+                        layers)
+
+
+def test_experts_workspace_validation(lib):
+    """Shape contract of jn_tenant_experts_fwd_bwd, checked on the host."""
+    E = lib._abi
+    tn, lens, mls = [0, 1], [[5, 9, 1], [12, 3]], [12, 12]
+    p, buf, keep = _host_packed(lib, tn, lens, mls, 2, 128)
+    ex = [_fake_expert(lib), _fake_expert(lib, a=32)]
+    ios = [_fake_io(lib, 3, 15), _fake_io(lib, 2, 15, a=32)]
+    n0 = lib.jn_experts_workspace_size(p, ex, ios)
+    assert n0 > 0
+    bad = [
+        (lambda: ([ex[0]], [ios[0]]), E.JN_EINVAL),                                   # G differs from the batch
+        (lambda: (ex, [_fake_io(lib, 2, 15), ios[1]]), E.JN_ESHAPE),                  # sample count
+        (lambda: (ex, [_fake_io(lib, 3, 2), ios[1]]), E.JN_ESHAPE),                   # prefix rows < samples
+        (lambda: ([_fake_expert(lib, chunk=65), _fake_expert(lib, a=32, chunk=65)],
+                  [_fake_io(lib, 3, 15, chunk=65), _fake_io(lib, 2, 15, a=32, chunk=65)]), E.JN_EUNSUPPORTED),
+        (lambda: ([_fake_expert(lib, H=8), _fake_expert(lib, H=8, a=32)], ios), E.JN_EUNSUPPORTED),  # hd 32
+        (lambda: ([_fake_expert(lib, a=33), ex[1]], [_fake_io(lib, 3, 15, a=33), ios[1]]), E.JN_EUNSUPPORTED),
+        (lambda: ([_fake_expert(lib, dp=256), _fake_expert(lib, a=32, dp=256)], ios), E.JN_EINCOMPAT),
+        (lambda: ([ex[0], _fake_expert(lib, f=1024, a=32)], ios), E.JN_EUNSUPPORTED),  # shapes differ
+        (lambda: (ex, [_fake_io(lib, 3, 1000), ios[1]]), E.JN_ESHAPE),                 # prefix beyond the batch
+    ]
+    for make, code in bad:
+        exs, iss = make()
+        with pytest.raises(lib.JNError) as e:
+            lib.jn_experts_workspace_size(p, exs, iss)
+        assert e.value.status == code, (code, e.value)
+    # null weight and unaligned gradient pointers
+    ex_null = _fake_expert(lib)
+    ex_null._layers[0].wo_c = None
+    with pytest.raises(lib.JNError) as e:
+        lib.jn_experts_workspace_size(p, [ex_null, ex[1]], ios)
+    assert e.value.status == E.JN_EINVAL
+    io_un = _fake_io(lib, 3, 15)
+    io_un._layers[0].w_up = io_un._layers[0].w_up + 4
+    with pytest.raises(lib.JNError) as e:
+        lib.jn_experts_workspace_size(p, ex, [io_un, ios[1]])
+    assert e.value.status == E.JN_EINVAL

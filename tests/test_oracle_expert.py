@@ -92,3 +92,33 @@ def test_expert_rounding_mode_is_close_to_fp64():
         rel = np.linalg.norm(a["grads"][k] - b["grads"][k]) / max(np.linalg.norm(a["grads"][k]), 1e-30)
         assert rel < 5e-2, (k, rel)
     assert abs(a["loss"] - b["loss"]) < 1e-2 * a["loss"]
+
+
+def test_bf16_rounding_noise_floor():
+    """The parity bar of the GPU expert rests on this: with bf16 rounding
+    points, fp32-sized perturbations (relative 2^-22) before each rounding
+    move predictions and gradients by ~1e-3 (not by ~1e-6): rounding flips
+    propagate.  Pinned so the floor, and the 1e-2 bar derived from it (about
+    twice the worst floor seen up to 6 layers), stay documented."""
+    rng = np.random.default_rng(5)
+    w = tiny_expert(rng, d=64, dp=32, f=128, a=7, L=2, scale=0.1)
+    u, z, t = inputs(rng, n=3, chunk=8, a=7, dp=32, lens=(20, 33))
+    z = [W.f32_to_bf16_bits(np.asarray(x, np.float32)) for x in z]
+    ref = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=True)
+    orig = ex._round_bf16
+    g = torch.Generator().manual_seed(0)
+
+    def jitter(x):
+        return orig(x * (1 + 2.0 ** -22 * torch.randn(x.shape, generator=g, dtype=torch.float64)))
+
+    try:
+        ex._round_bf16 = jitter
+        jit = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=True)
+    finally:
+        ex._round_bf16 = orig
+    rel = lambda a, b: float(np.linalg.norm(a - b) / np.linalg.norm(b))  # noqa: E731
+    floors = [rel(jit["pred"], ref["pred"])] + [rel(jit["grads"][k], ref["grads"][k]) for k in ref["grads"]]
+    assert 2e-4 < max(floors) < 5e-3, max(floors)
+    # the rounding points themselves move results by more than the floor
+    plain = ex.expert_step(w, 2, 2, 1e-6, u, z, t, rnd=False)
+    assert max(rel(plain["grads"][k], ref["grads"][k]) for k in ref["grads"]) > max(floors)
