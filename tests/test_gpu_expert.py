@@ -167,3 +167,28 @@ def test_expert_config4_shapes_sampled(jn):
     wl = W.make_workload(spec)
     st, targets, noisy = run_experts(wl)
     check_stagewise(wl, st, targets, noisy)
+
+
+def test_expert_config4_full_group(jn):
+    """All sixteen tenants of the heterogeneous configuration in one group:
+    oracle backbone on four samples, expert stage of the two tenants with the
+    fewest samples (every tenant's outputs are finite)."""
+    import oracle
+    wl = W.make_workload(4)
+    _say(f"config 4: N={sum(q.n for q in wl.requests)}")
+    st, targets, noisy = run_experts(wl)
+    keys = [(0, 0), (5, wl.requests[5].n - 1), (10, 1), (15, 0)]
+    iso = oracle.step.isolated(wl, samples=keys, heads=False)
+    hid = st.hidden.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    hid = W.bf16_bits_to_f32(hid)
+    cu = st.packed.map_tensor("cu_seqlens").cpu().numpy()
+    flat = [(r, s) for r, q in enumerate(wl.requests) for s in range(q.n)]
+    for i, key in enumerate(flat):
+        if key in iso["hidden"]:
+            z = iso["hidden"][key]
+            e = float(np.max(np.abs(hid[cu[i]: cu[i] + z.shape[0]] - z)) / np.max(np.abs(z)))
+            assert e < 2e-2, (key, e)
+    for io in st.ios:
+        assert torch.isfinite(io.pred).all() and torch.isfinite(io.loss).all()
+    few = sorted(range(wl.spec.G), key=lambda g: (wl.spec.tenants[g].n_samples, g))[:2]
+    check_stagewise(wl, st, targets, noisy, only=few)

@@ -247,6 +247,20 @@ def test_config_sampled_end_to_end(jn, cfg):
     _say(f"  hidden {worst:.3e} on {len(keys)} samples, head grads {gw:.3e}")
 
 
+def test_config3_sampled_end_to_end(jn):
+    """The 2B-shaped configuration (18-layer d2048 GeGLU, 8 tenants x 32) in
+    the launch configuration the benchmark times; oracle backbone on the
+    first sample of the first tenant and the last sample of the last tenant
+    (each ~6 s of fp64 work), head stage of all eight tenants."""
+    wl = W.make_workload(3)
+    _say(f"config 3: N={sum(q.n for q in wl.requests)}")
+    st = run_group(wl)
+    keys = [(0, 0), (len(wl.requests) - 1, wl.requests[-1].n - 1)]
+    worst = _check_backbone(wl, st, keys)
+    gw = check_heads_stagewise(wl, st)
+    _say(f"  hidden {worst:.3e} on {len(keys)} samples, head grads {gw:.3e}")
+
+
 def test_grouped_equals_isolated_bitwise(jn):
     """The defining invariant (Sec. 5.2): grouping changes no tenant's result."""
     from paper_2607_16074_amd import step as jstep
