@@ -80,6 +80,10 @@ def test_expert_closed_forms_and_invariances():
         c = ex.expert_forward(P, 2, 2, 1e-6, [ui[perm] for ui in u], z, False)
         for x, y in zip(a, c):
             assert torch.allclose(x[perm], y, rtol=1e-12, atol=1e-14)
+        # a sample's prediction never depends on another sample's prefix
+        z2 = [z[0], z[1] + 5.0]
+        d = ex.expert_forward(P, 2, 2, 1e-6, u, z2, False)
+        assert torch.equal(a[0], d[0]) and not torch.allclose(a[1], d[1])
 
 
 def test_expert_rounding_mode_is_close_to_fp64():
