@@ -841,6 +841,11 @@ jn_status jn_unpack(jn_ctx* c, const jn_packed* p, const jn_request* req, int32_
 
 namespace {
 
+// Action vectors are padded to kAP columns (zeros) and each tenant's rows to a
+// multiple of kKP for the weight-gradient contractions: the GEMM's K step.
+constexpr int kAP = 64;
+constexpr int kKP = 64;
+
 struct ExpShape {
   int32_t L, d, H, f, chunk, dp;
   float eps;
@@ -875,7 +880,7 @@ jn_status exp_plan(jn_ctx* c, const jn_packed* p, const jn_expert* ex, const jn_
   if (sh.d % sh.H != 0 || (sh.d / sh.H != 64 && sh.d / sh.H != 128))
     return fail(c, JN_EUNSUPPORTED, "expert head dim must be 64 or 128");
   if (sh.d != 256 && sh.d != 512 && sh.d != 1024 && sh.d != 2048) return fail(c, JN_EUNSUPPORTED, "expert width %d", sh.d);
-  if (sh.f % 32 != 0 || sh.dp % 32 != 0) return fail(c, JN_EUNSUPPORTED, "ffn and d_prefix must be multiples of 32");
+  if (sh.f % 64 != 0 || sh.dp % 64 != 0) return fail(c, JN_EUNSUPPORTED, "ffn and d_prefix must be multiples of 64");
   if (sh.dp != p->d) return fail(c, JN_EINCOMPAT, "expert reads width %d, backbone has %d", sh.dp, p->d);
   if (!(sh.eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
   P->sh = sh;
@@ -919,11 +924,11 @@ jn_status exp_plan(jn_ctx* c, const jn_packed* p, const jn_expert* ex, const jn_
   for (int32_t g = 0; g < G; ++g) {
     P->rows[g] = io[g].n_samples * sh.chunk;
     P->roff[g + 1] = P->roff[g] + P->rows[g];
-    P->Ka[g] = (P->rows[g] + 31) / 32 * 32;
+    P->Ka[g] = (P->rows[g] + kKP - 1) / kKP * kKP;
     P->kaoff[g + 1] = P->kaoff[g] + P->Ka[g];
     P->Pz[g] = io[g].prefix_rows;
     P->zoff[g + 1] = P->zoff[g] + P->Pz[g];
-    P->Kz[g] = (int32_t)((P->Pz[g] + 31) / 32 * 32);
+    P->Kz[g] = (int32_t)((P->Pz[g] + kKP - 1) / kKP * kKP);
     P->kzoff[g + 1] = P->kzoff[g] + P->Kz[g];
   }
   P->Na = P->roff[G];
@@ -951,15 +956,15 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.x = take(4 * Na * d);
   Ly.xf = take(4 * Na * d);
   Ly.yb = take(2 * Na * d);
-  Ly.ub = take(2 * Na * 32);
-  Ly.predp = take(4 * Na * 32);
-  Ly.dpred = take(4 * Na * 32);
-  Ly.dpredb = take(2 * Na * 32);
+  Ly.ub = take(2 * Na * kAP);
+  Ly.predp = take(4 * Na * kAP);
+  Ly.dpred = take(4 * Na * kAP);
+  Ly.dpredb = take(2 * Na * kAP);
   Ly.z = take(2 * Pz * s.dp);
   Ly.zoff = take(4 * (P.N + 1));
-  Ly.winp = take(2 * G * d * 32);
-  Ly.woutp = take(2 * G * 32 * d);
-  Ly.woutpT = take(2 * G * d * 32);
+  Ly.winp = take(2 * G * d * kAP);
+  Ly.woutp = take(2 * G * kAP * d);
+  Ly.woutpT = take(2 * G * d * kAP);
   Ly.dx = take(4 * Na * d);
   Ly.dxb = take(2 * Na * d);
   Ly.tf = take(4 * Na * d);
@@ -971,8 +976,8 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.TA = take(2 * std::max<int64_t>(wmax * P.KaT, 2 * d * P.KzT));
   Ly.TB = take(2 * std::max<int64_t>(wmax * P.KaT, (int64_t)s.dp * P.KzT));
   Ly.WT = take(2 * G * std::max<int64_t>(f * d, 3 * d * d) + 2 * G * 2 * d * s.dp);
-  Ly.dwinp = take(4 * G * d * 32);
-  Ly.dwoutp = take(4 * G * 32 * d);
+  Ly.dwinp = take(4 * G * d * kAP);
+  Ly.dwoutp = take(4 * G * kAP * d);
   for (int l = 0; l < s.L; ++l) {
     Ly.x1.push_back(take(4 * Na * d));
     Ly.x2.push_back(take(4 * Na * d));
@@ -1002,6 +1007,7 @@ struct Recorder {
   std::vector<char> img;
   size_t cap = 0;
   bool overflow = false;
+  bool bad_gemm = false;
   std::vector<std::function<hipError_t(char*)>> ops;
   std::vector<int32_t> opcode;
   size_t add(const void* src, size_t bytes) {
@@ -1076,6 +1082,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     for (auto& g : probs) maxm = std::max(maxm, g.M);
     const int shape = gemm_grouped_tile_shape(maxm);
     const int32_t tiles = gemm_grouped_prepare(probs.data(), (int32_t)probs.size(), shape);
+    if (tiles < 0) rec.bad_gemm = true;
     const size_t at = rec.add(probs.data(), sizeof(GemmArgs) * probs.size());
     const int32_t n = (int32_t)probs.size();
     rec.ops.push_back([=](char* a) { return launch_gemm_grouped(s, epi, (const GemmArgs*)(a + at), n, tiles, shape); });
@@ -1226,9 +1233,9 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     std::vector<CopyDesc> v;
     for (int32_t g = 0; g < G; ++g) {
       const int32_t a = ex[g].action_dim;
-      CopyDesc u{io[g].noisy, B(Ly.ub) + (int64_t)P.roff[g] * 32, a, 32, P.rows[g], 32, P.rows[g], a, 0, 1, 0, 0};
-      CopyDesc wi{ex[g].w_in, B(Ly.winp) + (int64_t)g * d * 32, a, 32, (int32_t)d, 32, (int32_t)d, a, 1, 1, 0, 0};
-      CopyDesc wo{ex[g].w_out, B(Ly.woutp) + (int64_t)g * 32 * d, d, d, 32, (int32_t)d, a, (int32_t)d, 1, 1, 0, 0};
+      CopyDesc u{io[g].noisy, B(Ly.ub) + (int64_t)P.roff[g] * kAP, a, kAP, P.rows[g], kAP, P.rows[g], a, 0, 1, 0, 0};
+      CopyDesc wi{ex[g].w_in, B(Ly.winp) + (int64_t)g * d * kAP, a, kAP, (int32_t)d, kAP, (int32_t)d, a, 1, 1, 0, 0};
+      CopyDesc wo{ex[g].w_out, B(Ly.woutp) + (int64_t)g * kAP * d, d, d, kAP, (int32_t)d, a, (int32_t)d, 1, 1, 0, 0};
       v.push_back(u);
       v.push_back(wi);
       v.push_back(wo);
@@ -1236,8 +1243,8 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     copy(v);
     std::vector<TransDesc> t;
     for (int32_t g = 0; g < G; ++g)
-      t.push_back(TransDesc{B(Ly.woutp) + (int64_t)g * 32 * d, B(Ly.woutpT) + (int64_t)g * d * 32, d, 32, 32,
-                            (int32_t)d, 32, 0});
+      t.push_back(TransDesc{B(Ly.woutp) + (int64_t)g * kAP * d, B(Ly.woutpT) + (int64_t)g * d * kAP, d, kAP, kAP,
+                            (int32_t)d, kAP, 0});
     trans(t);
     const int64_t cap = P.Pzt;
     rec.ops.push_back([=](char*) {
@@ -1245,7 +1252,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
                            (int32_t*)(w + Ly.zoff), w + Ly.z);
     });
     rec.opcode.push_back(JN_OP_EXPERT_OTHER);
-    rows_gemm(EPI_F32, B(Ly.ub), 32, [&](int32_t g) { return B(Ly.winp) + (int64_t)g * d * 32; }, d, F(Ly.x), d, true);
+    rows_gemm(EPI_F32, B(Ly.ub), kAP, [&](int32_t g) { return B(Ly.winp) + (int64_t)g * d * kAP; }, d, F(Ly.x), d, true);
   }
   const float scale = 1.0f / sqrtf((float)(d / H));
   for (int l = 0; l < S.L; ++l) {
@@ -1324,26 +1331,26 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
   const size_t gfa = ptr_table([&](int32_t g) { return ex[g].gf; });
   rows_copy(F(Ly.x), false, F(Ly.xf), false, P.Na, d);
   rms_fwd(Ly.xf, gfa, Ly.yb);
-  rows_gemm(EPI_F32, B(Ly.yb), d, [&](int32_t g) { return B(Ly.woutp) + (int64_t)g * 32 * d; }, 32, F(Ly.predp), 32,
-            true);
+  rows_gemm(EPI_F32, B(Ly.yb), d, [&](int32_t g) { return B(Ly.woutp) + (int64_t)g * kAP * d; }, kAP, F(Ly.predp),
+            kAP, true);
   {
     std::vector<XLossDesc> v(G);
     for (int32_t g = 0; g < G; ++g) v[g] = XLossDesc{io[g].targets, io[g].pred, io[g].loss, ex[g].action_dim, 0};
     const size_t at = rec.add(v.data(), sizeof(XLossDesc) * G);
     rec.ops.push_back([=](char* a) {
-      return launch_xloss(s, (const XLossDesc*)(a + at), (const int32_t*)(a + roff_at), G, F(Ly.predp), 32,
+      return launch_xloss(s, (const XLossDesc*)(a + at), (const int32_t*)(a + roff_at), G, F(Ly.predp), kAP,
                           F(Ly.dpred));
     });
     rec.opcode.push_back(JN_OP_LOSS);
   }
 
   // --------------------------------------------------------------- backward
-  rows_copy(F(Ly.dpred), false, B(Ly.dpredb), true, P.Na, 32);
-  trans_rows(B(Ly.dpredb), 32, B(Ly.TA), false);
+  rows_copy(F(Ly.dpred), false, B(Ly.dpredb), true, P.Na, kAP);
+  trans_rows(B(Ly.dpredb), kAP, B(Ly.TA), false);
   trans_rows(B(Ly.yb), d, B(Ly.TB), false);
-  wgrad(32, d, [&](int32_t g) { return F(Ly.dwoutp) + (int64_t)g * 32 * d; }, false);
-  rows_gemm(EPI_F32, B(Ly.dpredb), 32, [&](int32_t g) { return B(Ly.woutpT) + (int64_t)g * d * 32; }, d, F(Ly.tf), d,
-            true);
+  wgrad(kAP, d, [&](int32_t g) { return F(Ly.dwoutp) + (int64_t)g * kAP * d; }, false);
+  rows_gemm(EPI_F32, B(Ly.dpredb), kAP, [&](int32_t g) { return B(Ly.woutpT) + (int64_t)g * d * kAP; }, d, F(Ly.tf),
+            d, true);
   rows_copy(nullptr, false, F(Ly.dx), false, P.Na, d);  // dx = 0
   rms_bwd(Ly.xf, gfa, ptr_table([&](int32_t g) { return (const void*)io[g].dgf; }));
   for (int l = S.L - 1; l >= 0; --l) {
@@ -1455,18 +1462,21 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
   // input projection and the padded output-projection gradient
   rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
   trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-  trans_rows(B(Ly.ub), 32, B(Ly.TB), false);
-  wgrad(d, 32, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * 32; }, false);
+  trans_rows(B(Ly.ub), kAP, B(Ly.TB), false);
+  wgrad(d, kAP, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * kAP; }, false);
   {
     std::vector<CopyDesc> v;
     for (int32_t g = 0; g < G; ++g) {
       const int32_t a = ex[g].action_dim;
-      v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * 32, io[g].dw_in, 32, a, (int32_t)d, a, (int32_t)d, a, 0, 0, 0, 0});
-      v.push_back(CopyDesc{F(Ly.dwoutp) + (int64_t)g * 32 * d, io[g].dw_out, d, d, a, (int32_t)d, a, (int32_t)d, 0, 0, 0, 0});
+      v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * kAP, io[g].dw_in, kAP, a, (int32_t)d, a, (int32_t)d, a, 0, 0, 0,
+                           0});
+      v.push_back(CopyDesc{F(Ly.dwoutp) + (int64_t)g * kAP * d, io[g].dw_out, d, d, a, (int32_t)d, a, (int32_t)d, 0, 0, 0,
+                           0});
     }
     copy(v);
   }
   if (rec.overflow) return fail(c, JN_ENOSPACE, "internal: expert descriptor arena too small");
+  if (rec.bad_gemm) return fail(c, JN_EUNSUPPORTED, "internal: an expert GEMM has an unsupported shape");
 
   // ---- one upload of every table, then the launches in order
   st = stage_copy(c, darena, rec.img.data(), rec.img.size());

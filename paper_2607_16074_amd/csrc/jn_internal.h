@@ -65,7 +65,8 @@ struct GemmArgs {
 
 // Grouped launch over nprob problems sharing one epilogue: the host fills
 // the problems, calls gemm_grouped_prepare (tile ranges, returns the tile
-// total), uploads them and launches.  shape from gemm_grouped_tile_shape.
+// total, or -1 if a problem is not M, N, K > 0 with K % 64 == 0 and
+// N % 32 == 0), uploads them and launches.  shape from gemm_grouped_tile_shape.
 int gemm_grouped_tile_shape(int32_t max_m);
 int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape);
 hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,

@@ -2,34 +2,34 @@
 //
 //   C[M][N] (+)= epi( X[M][K] * W[N][K]^T )     X = activations, W = weights
 //
-// Tiling: a workgroup of 4 wavefronts (2 x 2) owns a BN x BM tile (weight rows
-// x tokens); each wavefront accumulates (BN/2) x (BM/2) with
-// v_mfma_f32_32x32x16_bf16.  The weight tile is the MFMA "A" operand, the
+// Tiling: a workgroup of WGN x WGM wavefronts owns a BN x BM tile (weight rows
+// x tokens; 256x256 with 8 wavefronts for large launches); each wavefront
+// accumulates (BN/WGN) x (BM/WGM) with v_mfma_f32_32x32x16_bf16.  The weight tile is the MFMA "A" operand, the
 // token tile the "B" operand, so each lane ends with 4 consecutive output
 // columns of one token row and the epilogue writes 8-byte (bf16) / 16-byte
 // (fp32) vectors along the row-major output.
 //
 // Operand staging: global_load_lds_dwordx4 moves 16-byte chunks straight from
-// global memory into LDS (no register staging).  K advances 32 per stage
-// through a 4-stage ring, so a slab is requested three stages before the
-// matrix cores read it.  An LDS row holds 32 bf16 (64 B, four 16-byte
-// chunks); chunk c of row r sits at position c ^ swz(r), swz(r) =
-// (r >> 2) & 3.  gfx950 serves a 16-byte-per-lane LDS read 256 B per clock in
-// four phases of 16 lanes that are not 16 consecutive lanes (lanes l and l+16
-// never share a phase; lanes 0-3 and 20-23 do); with this swizzle every phase
-// of the MFMA fragment reads (rows lane & 31, chunk half lane >> 5) covers all
-// 64 banks -- measured with the LDS bank-conflict counter.  Each DMA
-// instruction fills 1 KB = 16 rows; the lane -> source-chunk assignment
-// applies the swizzle.  Fragments of the next stage are read from LDS while
-// the second half of the current stage runs on the matrix cores.  One
-// barrier per stage.
+// global memory into LDS (no register staging).  K advances 64 per stage
+// (one 128-byte segment of every operand row) through two stages, so one slab
+// is in flight while the other is consumed.  Chunk c of LDS row r sits at
+// position c ^ swz(r), swz(r) = (r >> 1) & 7: two 128-byte rows share a 256-byte
+// bank row, and with this swizzle every 16-lane phase of a fragment read
+// (rows lane & 31, chunk 2*step + (lane >> 5)) covers all 64 banks (derived
+// from the bank-conflict counter's response to probe patterns; the GEMM runs
+// conflict-free).  Each DMA instruction fills 1 KB = 8 rows; the lane ->
+// source-chunk assignment applies the swizzle.  Per slab, four K=16 steps:
+// the fragments of step s+1 are read under the MFMAs of step s; the next
+// slab's DMA is interleaved with the first MFMAs; the one barrier per slab
+// sits before the last step's MFMAs, which then cover the read of the next
+// slab's first fragments.
 //
 // Launch order: tiles are walked in groups of 16 token-tiles (token tile
 // fastest).  Workgroups are dealt round-robin to the 8 XCDs, so each XCD's
 // resident tiles share a token tile and walk the weight tiles, and every
 // weight slab is requested by all XCDs at about the same time.  Measured on
-// the 2048-wide workloads this beats giving each XCD a contiguous 2-D block
-// of tiles (an explicit XCD remap) by ~7%.
+// the 2048-wide workloads, giving each XCD a contiguous block of tiles (an
+// explicit XCD remap) is no faster with 4x8 blocks and 13% slower with 16x2.
 //
 // Epilogues: bf16 store, GELU -> bf16, fp32 residual add (in place), and
 // GeGLU, whose gate and up weight rows are interleaved in 32-row blocks as
@@ -46,11 +46,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #define JN_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-constexpr int kBK = 32;       // K per stage
-constexpr int kStages = 4;    // ring depth
+constexpr int kBK = 64;       // K per stage (128-byte rows)
+constexpr int kStages = 2;    // double buffer
 constexpr int kGroupM = 16;   // token tiles per L2 group
 
-__device__ __forceinline__ int lds_swz(int r) { return (r >> 2) & 3; }
+__device__ __forceinline__ int lds_swz(int r) { return (r >> 1) & 7; }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
 // vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]).
@@ -58,6 +58,13 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// s_waitcnt with only the LDS / scalar-memory counter constrained.
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (N << 8));
 }
 
 template <int T>
@@ -87,9 +94,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   constexpr int WN = BN / WGN, WM = BM / WGM;  // per-wave tile
   constexpr int TN = WN / 32, TM = WM / 32;
   constexpr int ROWS = BN + BM;              // weight rows then token rows in a stage
-  constexpr int NI = ROWS / (16 * NW);       // 1 KB DMA instructions per wave per stage
+  constexpr int NI = ROWS / (8 * NW);        // 1 KB DMA instructions per wave per stage
   constexpr int STAGE = ROWS * kBK;          // elements per stage
-  static_assert(ROWS % (16 * NW) == 0 && TN >= 1 && TM >= 1, "tile shape");
+  static_assert(ROWS % (8 * NW) == 0 && TN >= 1 && TM >= 1, "tile shape");
   static_assert(!GLU || TN % 2 == 0, "GeGLU pairs gate/up tiles inside a wave");
 
   // ---- grouped tile order
@@ -104,14 +111,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave / WGM, wm = wave % WGM;
 
-  // ---- DMA sources: this wave's instruction i fills stage rows 16*(wave*NI+i) ..
-  // +15; lane -> (row, chunk) with the swizzle applied to the source chunk.
+  // ---- DMA sources: this wave's instruction i fills stage rows 8*(wave*NI+i) ..
+  // +7 (1 KB); lane -> (row lane>>3, position lane&7), and the position holds
+  // logical chunk position ^ swz(row) of that row's 128-byte K segment.
   const int32_t NL = GLU ? 2 * N : N;
   const uint16_t* src[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
-    const int row = 16 * (wave * NI + i) + (lane >> 2);
-    const int chunk = (lane & 3) ^ lds_swz(row);
+    const int row = 8 * (wave * NI + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ lds_swz(row);
     if (row < BN) {
       if constexpr (GLU) {
         const int32_t col = min(tn * (BN / 2) + (row >> 6) * 32 + (row & 31), N - 1);
@@ -134,68 +142,69 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int KT = K / kBK;
-  // fragment read positions: logical chunk 2*kk + (lane >> 5), swizzled by row
-  const int sw = lds_swz(lane & 31);
-  const int pos0 = (lane >> 5) ^ sw, pos1 = pos0 ^ 2;
+  // fragment rows and their swizzle (row0 of every fragment is a multiple of 32)
+  const int sw = lds_swz(lane & 31), half = lane >> 5;
   const int wrow = wn * WN + (lane & 31), xrow = BN + wm * WM + (lane & 31);
 
-  // prologue: slabs 0 .. kStages-2 in flight
+  // prologue: slabs 0 and 1 in flight
 #pragma unroll
-  for (int st = 0; st < kStages - 1; ++st) {
-    if (st < KT) {
+  for (int i = 0; i < NI; ++i)
+    __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(dst0 + i * 512), 16, 0, 0);
+  if (KT > 1) {
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + st * kBK), JN_LPTR(dst0 + st * STAGE + i * 512), 16, 0, 0);
-    }
+    for (int i = 0; i < NI; ++i)
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(dst0 + STAGE + i * 512), 16, 0, 0);
+    wait_vmcnt<NI>();
+  } else {
+    wait_vmcnt<0>();
   }
-  // Fragment order: kk0 of slab kt is in registers when its MFMAs start; kk1
-  // of slab kt is read right after them (before the stage barrier, so the
-  // barrier wait covers its latency); kk0 of slab kt+1 is read after the
-  // first MFMA of slab kt's kk1 group, under the remaining seven.  No wait
-  // ever covers reads issued just before it.
-  bf16x8 fw0[TN], fx0[TM], fw1[TN], fx1[TM];
-  if (KT > kStages - 2) wait_vmcnt<(kStages - 2) * NI>(); else wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  gemm_frags<TN>(fw0, lds, wrow, pos0);
-  gemm_frags<TM>(fx0, lds, xrow, pos0);
 
+  // Per slab: four K=16 steps; the fragments of step s+1 are read while the
+  // MFMAs of step s run.  The DMA of slab kt+1 (into the buffer slab kt-1
+  // used) is interleaved with the first MFMAs of slab kt.  The stage barrier
+  // sits before the last step's MFMAs: each wave has waited for its slab kt+1
+  // DMA and for its last reads of slab kt, meets the others, reads step 0 of
+  // slab kt+1 and only then issues the last eight MFMAs of slab kt, which
+  // cover that read.
+  bf16x8 fw[2][TN], fx[2][TM];
+  gemm_frags<TN>(fw[0], lds, wrow, half ^ sw);
+  gemm_frags<TM>(fx[0], lds, xrow, half ^ sw);
   for (int kt = 0; kt < KT; ++kt) {
-    const uint16_t* cur = lds + (kt % kStages) * STAGE;
-    gemm_mfma<TN, TM>(acc, fw0, fx0);
-    __builtin_amdgcn_sched_barrier(0);
-    gemm_frags<TN>(fw1, cur, wrow, pos1);
-    gemm_frags<TM>(fx1, cur, xrow, pos1);
-    __builtin_amdgcn_sched_barrier(0);
-    const bool more = kt + 1 < KT;
-    if (more) {
-      // slab kt+1 landed for every wave; every wave is past its reads of the
-      // buffer that slab kt+kStages-1 refills
-      const bool refill = kt + kStages - 1 < KT;
-      if (refill) wait_vmcnt<(kStages - 3) * NI>(); else wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-      if (refill) {
-        const int st = (kt + kStages - 1) % kStages;
+    const uint16_t* cur = lds + (kt & 1) * STAGE;
+    const bool fill = kt >= 1 && kt + 1 < KT;  // slab kt+1 goes into the buffer slab kt-1 used
+    uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
-          __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + kStages - 1) * kBK),
-                                           JN_LPTR(dst0 + st * STAGE + i * 512), 16, 0, 0);
+    for (int step = 0; step < 4; ++step) {
+      const int b = step & 1;
+      if (step < 3) {
+        const int pos = (2 * (step + 1) + half) ^ sw;
+        gemm_frags<TN>(fw[b ^ 1], cur, wrow, pos);
+        gemm_frags<TM>(fx[b ^ 1], cur, xrow, pos);
+      } else if (kt + 1 < KT) {
+        wait_vmcnt<0>();
+        wait_lgkmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        const uint16_t* nxt = lds + ((kt + 1) & 1) * STAGE;
+        gemm_frags<TN>(fw[0], nxt, wrow, half ^ sw);
+        gemm_frags<TM>(fx[0], nxt, xrow, half ^ sw);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < TN * TM; ++q) {
+        const int i = q / TM, j = q % TM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[b][i], fx[b][j], acc[i][j], 0, 0, 0);
+        // DMA d of slab kt+1 after MFMA d of the slab (as early as possible)
+        constexpr int PER = (NI + TN * TM - 1) / (TN * TM);  // DMAs per MFMA
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          const int d = (step * TN * TM + q) * PER + e;
+          if (d < NI && fill)
+            __builtin_amdgcn_global_load_lds(JN_GPTR(src[d] + (kt + 1) * kBK), JN_LPTR(fdst + d * 512), 16, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
-    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw1[0], fx1[0], acc[0][0], 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (more) {
-      const uint16_t* nxt = lds + ((kt + 1) % kStages) * STAGE;
-      gemm_frags<TN>(fw0, nxt, wrow, pos0);
-      gemm_frags<TM>(fx0, nxt, xrow, pos0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < TN; ++i)
-#pragma unroll
-      for (int j = 0; j < TM; ++j)
-        if (i + j > 0) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw1[i], fx1[j], acc[i][j], 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
   }
 
   // ---- epilogue: lane owns output columns n..n+3 of token row m
@@ -377,6 +386,8 @@ int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
   const int BN = shape == 1 ? 256 : 128, BM = 128;
   int32_t total = 0;
   for (int32_t p = 0; p < nprob; ++p) {
+    const GemmArgs& g = probs[p];
+    if (g.M <= 0 || g.N <= 0 || g.K <= 0 || g.K % kBK != 0 || g.N % 32 != 0) return -1;
     probs[p].tiles_m = (probs[p].M + BM - 1) / BM;
     probs[p].tiles_n = (probs[p].N + BN - 1) / BN;
     probs[p].tile_start = total;
