@@ -43,15 +43,16 @@ def source_hash(path: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(config: int):
     """HBM bytes per launch of the dominant GEMM from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary, or None once the kernel source changed."""
+    FETCH_SIZE / WRITE_SIZE summary (taken on the 8x32 2B-shaped workload), or
+    None for another workload or once the kernel source changed."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256_16") != source_hash(GEMM_SRC):
+    if config != t.get("config", 3) or t.get("kernel_source_sha256_16") != source_hash(GEMM_SRC):
         return None
     return t.get("bytes_per_launch")
 
@@ -105,14 +106,25 @@ def cpu_oracle_baseline(wl, budget_s=25.0):
     key = (0, 0)
     t0 = time.perf_counter()
     res = oracle.step.isolated(wl, samples=[key], heads=False)
-    n0 = wl.spec.tenants[req.tenant].n_samples
-    P = np.repeat(res["pooled"][key][None, :], n0, axis=0)
-    oracle.step.tenant_from_pooled(wl, req.tenant, P)
+    ten = wl.spec.tenants[req.tenant]
+    if ten.expert is None:
+        n0 = ten.n_samples
+        P = np.repeat(res["pooled"][key][None, :], n0, axis=0)
+        oracle.step.tenant_from_pooled(wl, req.tenant, P)
+        what = f"its tenant's head fwd/loss/grad over {n0} rows"
+    else:
+        # the sample's own expert forward, loss and gradients (one sample of its tenant)
+        from oracle import expert as oexpert
+        L_e, _, H_e, _ = ten.expert
+        z = res["hidden"][key]
+        oexpert.expert_step(wl.experts[req.tenant], L_e, H_e, wl.spec.backbone.eps, [wl.noisy[req.tenant][0]], [z],
+                            wl.targets[req.tenant][:1])
+        what = "its tenant's action-expert fwd/loss/grad for that sample"
     dt = time.perf_counter() - t0
     L = int(req.lengths[0])
     return {"value": 1.0 / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"1 of {sum(q.n for q in wl.requests)} samples ({L} tokens): full backbone forward in fp64 "
-                      f"+ its tenant's head fwd/loss/grad over {n0} rows; {dt:.1f} s on the host",
+                      f"+ {what}; {dt:.1f} s on the host",
             "seconds": dt, "host_cpus": os.cpu_count()}
 
 
@@ -145,9 +157,10 @@ def main():
     wl = W.make_workload(args.config)
     spec = wl.spec
     log(f"workload cfg{args.config} drawn in {time.perf_counter() - t0:.1f}s: {spec.name}")
-    model, reqs, targets = jstep.from_workload(wl, "cuda")
+    model, reqs, targets, noisy = jstep.from_workload(wl, "cuda", with_noisy=True)
     G = spec.G
-    grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align)
+    experts = spec.tenants[0].expert is not None
+    grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align, noisy=noisy)
     torch.cuda.synchronize()
     N, valid = grouped.N, grouped.valid_tokens
     log(f"N={N} samples, {valid} valid tokens, T={grouped.T} packed rows")
@@ -185,7 +198,7 @@ def main():
 
     iso_ms = None
     if not args.no_isolated:
-        iso = jstep.isolated_runs(model, reqs, targets, list(range(G)), args.align, ctx=grouped.ctx)
+        iso = jstep.isolated_runs(model, reqs, targets, list(range(G)), args.align, ctx=grouped.ctx, noisy=noisy)
         torch.cuda.synchronize()
 
         def run_iso():
@@ -216,11 +229,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"config {args.config}: {spec.name}; per-tenant MLP heads, seed {spec.seed}",
+        "config": {"workload": f"config {args.config}: {spec.name}; per-tenant "
+                               f"{'action experts' if experts else 'MLP heads'}, seed {spec.seed}",
                    "tenants": G, "samples": N, "valid_tokens": valid, "packed_rows": grouped.T,
                    "align": args.align},
         "backbone_tokens_per_s": valid / (bb_ms * 1e-3),
         "backbone_ms": bb_ms,
+        "tenant_stage_ms": sum(v["ms"] for k, v in by_op.items()
+                               if k in ("pool", "head_fwd", "loss", "head_bwd", "expert_gemm", "expert_attention",
+                                        "expert_other")) / args.steps,
         "isolated_samples_per_s": (N / (iso_ms * 1e-3)) if iso_ms else None,
         "isolated_ms_per_step": iso_ms,
         "speedup_vs_isolated": (iso_ms / (t_step * 1e3)) if iso_ms else None,
@@ -228,7 +245,7 @@ def main():
         "backbone_gemm_frac_of_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": f"gemm_kernel ({dom}, {spec.backbone.d}-wide)",
                      "achieved": gs["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
+                     "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(args.config),
                      "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},
         "gemm_by_op": gemm_stats,
         "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample")},
