@@ -1276,6 +1276,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.kcol = (int32_t)d;
       A.vcol = (int32_t)(2 * d);
       A.Lq = S.chunk;
+      A.max_lk = S.chunk;
       A.hd = (int32_t)(d / H);
       A.nheads = (int32_t)H;
       A.scale = scale;
@@ -1315,6 +1316,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.kcol = 0;
       A.vcol = (int32_t)d;
       A.Lq = S.chunk;
+      A.max_lk = p->max_seqlen;
       A.hd = (int32_t)(d / H);
       A.nheads = (int32_t)H;
       A.scale = scale;
@@ -1401,6 +1403,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.dkcol = 0;
       A.dvcol = (int32_t)d;
       A.Lq = S.chunk;
+      A.max_lk = p->max_seqlen;
       A.hd = (int32_t)(d / H);
       A.nheads = (int32_t)H;
       A.scale = scale;
@@ -1445,6 +1448,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.dkcol = (int32_t)d;
       A.dvcol = (int32_t)(2 * d);
       A.Lq = S.chunk;
+      A.max_lk = S.chunk;
       A.hd = (int32_t)(d / H);
       A.nheads = (int32_t)H;
       A.scale = scale;

@@ -193,7 +193,7 @@ struct AttnArgs {
   const int32_t* zoff;
   int64_t ldq, ldkv, ldo, lddq, lddkv, kv_cap;
   int32_t kcol, vcol, dkcol, dvcol;
-  int32_t Lq, hd, nheads, reserved;
+  int32_t Lq, hd, nheads, max_lk;    // max_lk: largest key count of any sample
   float scale;
 };
 hipError_t launch_xattn(hipStream_t s, const AttnArgs& A, int32_t nsamples, bool backward);

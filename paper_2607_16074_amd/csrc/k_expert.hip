@@ -8,9 +8,9 @@
 //   prefix       tenant-ordered copy of every sample's valid backbone rows
 //   rmsnorm      per-tenant-gain RMSNorm forward (fp32 -> bf16) and backward
 //                (fp32), gain gradients by fixed-order column sums
-//   attention    fp32 self- / cross-attention forward and backward, one
-//                workgroup per (sample, head); a sample's queries never see
-//                another sample's keys
+//   attention    fp32 self- / cross-attention forward and backward on the
+//                fp32 matrix cores, per (sample, head); a sample's queries
+//                never see another sample's keys
 //   loss         per-tenant mean squared error and its gradient
 #include "jn_device.h"
 #include "jn_internal.h"
@@ -295,24 +295,26 @@ hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gai
 }
 
 // -------------------------------------------------------------- attention ---
-// One workgroup per (sample k, head h); queries: rows q_row0 + 0..Lq-1 of Q
-// (Lq <= 64); keys / values: rows kv_row0 .. kv_row0 + Lk - 1 of K / V.  Self
-// attention: kv rows = the sample's own action rows; cross attention: the
-// sample's rows of the tenant-ordered prefix (zoff).  Thread t owns query row
-// t >> 2 and a quarter of the head dims; keys are processed 32 at a time.
+// fp32 attention on the fp32 matrix cores (v_mfma_f32_32x32x2_f32).  Queries:
+// rows q_row0 + 0..Lq-1 of Q (Lq <= 64, two groups of 32); keys / values: rows
+// kv_row0 .. + Lk - 1 of K / V.  Self attention: the sample's own action rows;
+// cross attention: the sample's rows of the tenant-ordered prefix (zoff), so a
+// query never sees another sample's keys.
+//
+// MFMA lane layout (32x32x2): lane l supplies A[l & 31][l >> 5] and
+// B[l >> 5][l & 31]; accumulator r of lane l is C[mrow(r, l)][l & 31].  Scores
+// are computed transposed, S^T = K Q^T, so each lane owns one query column and
+// softmax statistics need one exchange with lane l ^ 32.  In P V the k index of
+// step t pairs key kfor(t, half) with the half's lane, which is exactly the key
+// whose score that lane holds in register t: P never leaves registers.
 
-constexpr int kAQ = 64;   // max queries per sample
-constexpr int kAK = 32;   // keys per step
+typedef float f32x16v __attribute__((ext_vector_type(16)));
 
-template <int HD>
-struct AttnSmem {
-  float q[kAQ][HD + 1];
-  float dO[kAQ][HD + 1];
-  float k[kAK][HD + 1];
-  float v[kAK][HD + 1];
-  float p[kAQ][kAK + 1];
-  float ds[kAQ][kAK + 1];
-};
+__device__ __forceinline__ int mrow(int r, int half) { return 8 * (r >> 2) + 4 * half + (r & 3); }
+
+__device__ __forceinline__ f32x16v mfma32(float a, float b, f32x16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
 
 __device__ __forceinline__ void attn_rows(const AttnArgs& A, int32_t k, int32_t& q0, int32_t& Lq, int64_t& kv0,
                                           int32_t& Lk) {
@@ -328,181 +330,363 @@ __device__ __forceinline__ void attn_rows(const AttnArgs& A, int32_t k, int32_t&
   }
 }
 
-template <int HD>
-__global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
-  constexpr int QD = HD / 4;  // dims per thread
-  __shared__ AttnSmem<HD> sm;
-  const int32_t k = blockIdx.x, h = blockIdx.y;
-  int32_t q0, Lq, Lk;
-  int64_t kv0;
-  attn_rows(A, k, q0, Lq, kv0, Lk);
-  const int t = threadIdx.x, r = t >> 2, qd = t & 3;
-  const bool live = r < Lq;
-  for (int e = t; e < kAQ * HD; e += 256) {
-    const int rr = e / HD, c = e % HD;
-    sm.q[rr][c] = rr < Lq ? A.Q[(int64_t)(q0 + rr) * A.ldq + h * HD + c] : 0.f;
+// Stage rows j0 .. j0+63 of K and V (head h, zero past Lk) into LDS, row
+// strides SKV floats (8-byte aligned rows: float2 stores).
+template <int HD, int SKV>
+__device__ __forceinline__ void attn_stage_kv(const AttnArgs& A, int64_t kv0, int32_t Lk, int32_t j0, int h,
+                                              float* sk, float* sv) {
+  for (int e = threadIdx.x; e < 64 * HD / 4; e += 256) {
+    const int rr = e / (HD / 4), c = 4 * (e % (HD / 4));
+    float4 kq = make_float4(0.f, 0.f, 0.f, 0.f), vq = kq;
+    if (j0 + rr < Lk) {
+      const int64_t row = kv0 + j0 + rr;
+      kq = *reinterpret_cast<const float4*>(A.K + row * A.ldkv + A.kcol + h * HD + c);
+      vq = *reinterpret_cast<const float4*>(A.V + row * A.ldkv + A.vcol + h * HD + c);
+    }
+    *reinterpret_cast<float2*>(sk + rr * SKV + c) = make_float2(kq.x, kq.y);
+    *reinterpret_cast<float2*>(sk + rr * SKV + c + 2) = make_float2(kq.z, kq.w);
+    *reinterpret_cast<float2*>(sv + rr * SKV + c) = make_float2(vq.x, vq.y);
+    *reinterpret_cast<float2*>(sv + rr * SKV + c + 2) = make_float2(vq.z, vq.w);
   }
-  float o[QD];
-#pragma unroll
-  for (int i = 0; i < QD; ++i) o[i] = 0.f;
-  float m = -INFINITY, l = 0.f;
-  for (int32_t j0 = 0; j0 < Lk; j0 += kAK) {
-    __syncthreads();
-    for (int e = t; e < kAK * HD; e += 256) {
-      const int jj = e / HD, c = e % HD;
-      const bool ok = j0 + jj < Lk;
-      const int64_t row = kv0 + j0 + jj;
-      sm.k[jj][c] = ok ? A.K[row * A.ldkv + A.kcol + h * HD + c] : 0.f;
-      sm.v[jj][c] = ok ? A.V[row * A.ldkv + A.vcol + h * HD + c] : 0.f;
-    }
-    __syncthreads();
-    float s[kAK / 4];
-    float bm = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < kAK / 4; ++u) {
-      const int jj = qd + 4 * u;
-      float acc = 0.f;
-#pragma unroll 8
-      for (int c = 0; c < HD; ++c) acc = fmaf(sm.q[r][c], sm.k[jj][c], acc);
-      s[u] = (j0 + jj < Lk) ? acc * A.scale : -INFINITY;
-      bm = fmaxf(bm, s[u]);
-    }
-    bm = fmaxf(bm, __shfl_xor(bm, 1, 64));
-    bm = fmaxf(bm, __shfl_xor(bm, 2, 64));
-    const float mn = fmaxf(m, bm);
-    const float alpha = __expf(m - mn);
-    float ls = 0.f;
-#pragma unroll
-    for (int u = 0; u < kAK / 4; ++u) {
-      const float pv = __expf(s[u] - mn);
-      sm.p[r][qd + 4 * u] = pv;
-      ls += pv;
-    }
-    ls += __shfl_xor(ls, 1, 64);
-    ls += __shfl_xor(ls, 2, 64);
-    l = l * alpha + ls;
-    m = mn;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < QD; ++i) o[i] *= alpha;
-    for (int jj = 0; jj < kAK; ++jj) {
-      const float pv = sm.p[r][jj];
-#pragma unroll
-      for (int i = 0; i < QD; ++i) o[i] = fmaf(pv, sm.v[jj][qd * QD + i], o[i]);
-    }
-  }
-  if (!live) return;
-  const float inv = 1.f / l;
-  float* orow = A.O + (int64_t)(q0 + r) * A.ldo + h * HD + qd * QD;
-#pragma unroll
-  for (int i = 0; i < QD; i += 4)
-    *reinterpret_cast<float4*>(orow + i) = make_float4(o[i] * inv, o[i + 1] * inv, o[i + 2] * inv, o[i + 3] * inv);
-  if (qd == 0) A.lse[(int64_t)(q0 + r) * A.nheads + h] = m + __logf(l);
 }
 
+// Forward: one workgroup per (sample, head); wave w takes query group w & 1
+// and the 32-key blocks of parity w >> 1 of every 64-key tile; the two key
+// halves merge their (max, sum, output) at the end.
 template <int HD>
-__global__ __launch_bounds__(256) void xattn_bwd_kernel(AttnArgs A) {
-  constexpr int QD = HD / 4;
-  __shared__ AttnSmem<HD> sm;
-  const int32_t k = blockIdx.x, h = blockIdx.y;
+__global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
+  constexpr int SKV = HD + 2;  // K rows read lane-per-row: 2*row + half covers all banks
+  constexpr int NT = HD / 2, NCB = HD / 32;
+  __shared__ float smem[2 * 64 * SKV];
+  float* sk = smem;
+  float* sv = smem + 64 * SKV;
+  const int k = blockIdx.x, h = blockIdx.y;
   int32_t q0, Lq, Lk;
   int64_t kv0;
   attn_rows(A, k, q0, Lq, kv0, Lk);
-  const int t = threadIdx.x, r = t >> 2, qd = t & 3;
-  const bool live = r < Lq;
-  for (int e = t; e < kAQ * HD; e += 256) {
-    const int rr = e / HD, c = e % HD;
-    const bool ok = rr < Lq;
-    sm.q[rr][c] = ok ? A.Q[(int64_t)(q0 + rr) * A.ldq + h * HD + c] : 0.f;
-    sm.dO[rr][c] = ok ? A.dO[(int64_t)(q0 + rr) * A.ldo + h * HD + c] : 0.f;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = wave & 1, par = wave >> 1, half = lane >> 5, col = lane & 31;
+  const int q = 32 * g + col;
+  const bool qlive = q < Lq, glive = 32 * g < Lq;
+  float qreg[NT];
+  {
+    const float* qr = A.Q + (int64_t)(q0 + min(q, Lq - 1)) * A.ldq + h * HD + half;
+#pragma unroll
+    for (int i = 0; i < NT; ++i) qreg[i] = qlive ? qr[2 * i] : 0.f;
   }
-  // D_r = sum_c dO[r][c] O[r][c]
-  float Dr = 0.f;
-  if (live) {
-    const float* orow = A.O + (int64_t)(q0 + r) * A.ldo + h * HD + qd * QD;
-    const float* drow = A.dO + (int64_t)(q0 + r) * A.ldo + h * HD + qd * QD;
-#pragma unroll 8
-    for (int i = 0; i < QD; ++i) Dr = fmaf(orow[i], drow[i], Dr);
-  }
-  Dr += __shfl_xor(Dr, 1, 64);
-  Dr += __shfl_xor(Dr, 2, 64);
-  const float lse = live ? A.lse[(int64_t)(q0 + r) * A.nheads + h] : 0.f;
-  float dq[QD];
+  f32x16v o[NCB];
 #pragma unroll
-  for (int i = 0; i < QD; ++i) dq[i] = 0.f;
-  for (int32_t j0 = 0; j0 < Lk; j0 += kAK) {
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[cb][r] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  for (int32_t j0 = 0; j0 < Lk; j0 += 64) {
     __syncthreads();
-    for (int e = t; e < kAK * HD; e += 256) {
-      const int jj = e / HD, c = e % HD;
-      const bool ok = j0 + jj < Lk;
-      const int64_t row = kv0 + j0 + jj;
-      sm.k[jj][c] = ok ? A.K[row * A.ldkv + A.kcol + h * HD + c] : 0.f;
-      sm.v[jj][c] = ok ? A.V[row * A.ldkv + A.vcol + h * HD + c] : 0.f;
-    }
+    attn_stage_kv<HD, SKV>(A, kv0, Lk, j0, h, sk, sv);
     __syncthreads();
+    const int32_t kb = j0 + 32 * par;
+    if (kb >= Lk || !glive) continue;
+    f32x16v sc;
 #pragma unroll
-    for (int u = 0; u < kAK / 4; ++u) {
-      const int jj = qd + 4 * u;
-      float sacc = 0.f, pacc = 0.f;
-#pragma unroll 8
-      for (int c = 0; c < HD; ++c) {
-        sacc = fmaf(sm.q[r][c], sm.k[jj][c], sacc);
-        pacc = fmaf(sm.dO[r][c], sm.v[jj][c], pacc);
-      }
-      const bool ok = live && (j0 + jj < Lk);
-      const float pv = ok ? __expf(sacc * A.scale - lse) : 0.f;
-      sm.p[r][jj] = pv;
-      sm.ds[r][jj] = pv * (pacc - Dr);
+    for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+    const float* kr = sk + (32 * par + col) * SKV + half;
+#pragma unroll 16
+    for (int i = 0; i < NT; ++i) sc = mfma32(kr[2 * i], qreg[i], sc);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      sc[r] = (kb + mrow(r, half) < Lk) ? sc[r] * A.scale : -INFINITY;
+      mx = fmaxf(mx, sc[r]);
     }
-    __syncthreads();
-    // dQ[r] += scale * sum_j dS[r][j] K[j]
-    for (int jj = 0; jj < kAK; ++jj) {
-      const float w = sm.ds[r][jj] * A.scale;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float alpha = __expf(m - mn);
+    float ps = 0.f;
 #pragma unroll
-      for (int i = 0; i < QD; ++i) dq[i] = fmaf(w, sm.k[jj][qd * QD + i], dq[i]);
+    for (int r = 0; r < 16; ++r) {
+      sc[r] = __expf(sc[r] - mn);
+      ps += sc[r];
     }
-    // dV[j] = sum_r P[r][j] dO[r];  dK[j] = scale * sum_r dS[r][j] Q[r]
-    {
-      const int jj = t >> 3, c0 = (t & 7) * (HD / 8);
-      float dv[HD / 8], dk[HD / 8];
+    ps += __shfl_xor(ps, 32, 64);
+    l = l * alpha + ps;
+    m = mn;
 #pragma unroll
-      for (int i = 0; i < HD / 8; ++i) dv[i] = dk[i] = 0.f;
-      for (int rr = 0; rr < Lq; ++rr) {
-        const float pv = sm.p[rr][jj], dsv = sm.ds[rr][jj];
+    for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
-        for (int i = 0; i < HD / 8; ++i) {
-          dv[i] = fmaf(pv, sm.dO[rr][c0 + i], dv[i]);
-          dk[i] = fmaf(dsv, sm.q[rr][c0 + i], dk[i]);
-        }
-      }
-      if (j0 + jj < Lk) {
-        const int64_t row = kv0 + j0 + jj;
-        float* dvp = A.dV + row * A.lddkv + A.dvcol + h * HD + c0;
-        float* dkp = A.dK + row * A.lddkv + A.dkcol + h * HD + c0;
+      for (int r = 0; r < 16; ++r) o[cb][r] *= alpha;
+      const float* vr = sv + (32 * par) * SKV + 32 * cb + col;
 #pragma unroll
-        for (int i = 0; i < HD / 8; i += 4) {
-          *reinterpret_cast<float4*>(dvp + i) = make_float4(dv[i], dv[i + 1], dv[i + 2], dv[i + 3]);
-          *reinterpret_cast<float4*>(dkp + i) =
-              make_float4(dk[i] * A.scale, dk[i + 1] * A.scale, dk[i + 2] * A.scale, dk[i + 3] * A.scale);
-        }
-      }
+      for (int t = 0; t < 16; ++t) o[cb] = mfma32(vr[mrow(t, half) * SKV], sc[t], o[cb]);
     }
   }
-  if (!live) return;
-  float* qrow = A.dQ + (int64_t)(q0 + r) * A.lddq + h * HD + qd * QD;
+  // merge the two key halves of each query group
+  constexpr int MS = NCB * 16 + 2;
+  __syncthreads();
+  float* mb = smem + (g * 64 + lane) * MS;
+  if (par == 1) {
 #pragma unroll
-  for (int i = 0; i < QD; i += 4) *reinterpret_cast<float4*>(qrow + i) = make_float4(dq[i], dq[i + 1], dq[i + 2], dq[i + 3]);
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mb[cb * 16 + r] = o[cb][r];
+    mb[NCB * 16] = m;
+    mb[NCB * 16 + 1] = l;
+  }
+  __syncthreads();
+  if (par == 1 || !qlive) return;
+  {
+    const float m1 = mb[NCB * 16], l1 = mb[NCB * 16 + 1];
+    const float mn = fmaxf(m, m1);
+    const float a0 = m == -INFINITY ? 0.f : __expf(m - mn), a1 = m1 == -INFINITY ? 0.f : __expf(m1 - mn);
+    l = l * a0 + l1 * a1;
+    m = mn;
+    const float inv = 1.f / l;
+    float* orow = A.O + (int64_t)(q0 + q) * A.ldo + h * HD;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (o[cb][4 * a4 + e] * a0 + mb[cb * 16 + 4 * a4 + e] * a1) * inv;
+        *reinterpret_cast<float4*>(orow + 32 * cb + 8 * a4 + 4 * half) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    if (half == 0) A.lse[(int64_t)(q0 + q) * A.nheads + h] = m + __logf(l);
+  }
+}
+
+// Backward, query side: dQ = scale * dS K with dS = P * (dP - D), P recomputed
+// from the saved log-sum-exp, dP^T = V dO^T, D = rowsum(dO * O).  Same wave
+// roles as the forward; the key halves' partial dQ are summed at the end.
+template <int HD>
+__global__ __launch_bounds__(256) void xattn_bwd_dq_kernel(AttnArgs A) {
+  constexpr int SKV = HD + 2;
+  constexpr int NT = HD / 2, NCB = HD / 32;
+  __shared__ float smem[2 * 64 * SKV];
+  float* sk = smem;
+  float* sv = smem + 64 * SKV;
+  const int k = blockIdx.x, h = blockIdx.y;
+  int32_t q0, Lq, Lk;
+  int64_t kv0;
+  attn_rows(A, k, q0, Lq, kv0, Lk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = wave & 1, par = wave >> 1, half = lane >> 5, col = lane & 31;
+  const int q = 32 * g + col;
+  const bool qlive = q < Lq, glive = 32 * g < Lq;
+  float qreg[NT], dreg[NT];
+  float Dq = 0.f, lse = 0.f;
+  {
+    const int64_t row = q0 + min(q, Lq - 1);
+    const float* qr = A.Q + row * A.ldq + h * HD + half;
+    const float* dr = A.dO + row * A.ldo + h * HD + half;
+    const float* orr = A.O + row * A.ldo + h * HD + half;
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      qreg[i] = qlive ? qr[2 * i] : 0.f;
+      dreg[i] = qlive ? dr[2 * i] : 0.f;
+      Dq = fmaf(dreg[i], qlive ? orr[2 * i] : 0.f, Dq);
+    }
+    Dq += __shfl_xor(Dq, 32, 64);
+    lse = qlive ? A.lse[row * A.nheads + h] : 0.f;
+  }
+  f32x16v dq[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dq[cb][r] = 0.f;
+  for (int32_t j0 = 0; j0 < Lk; j0 += 64) {
+    __syncthreads();
+    attn_stage_kv<HD, SKV>(A, kv0, Lk, j0, h, sk, sv);
+    __syncthreads();
+    const int32_t kb = j0 + 32 * par;
+    if (kb >= Lk || !glive) continue;
+    f32x16v sc, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+    const float* kr = sk + (32 * par + col) * SKV + half;
+    const float* vr = sv + (32 * par + col) * SKV + half;
+#pragma unroll 16
+    for (int i = 0; i < NT; ++i) {
+      sc = mfma32(kr[2 * i], qreg[i], sc);
+      dp = mfma32(vr[2 * i], dreg[i], dp);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const bool ok = qlive && kb + mrow(r, half) < Lk;
+      const float p = ok ? __expf(sc[r] * A.scale - lse) : 0.f;
+      sc[r] = p * (dp[r] - Dq);  // dS
+    }
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const float* kc = sk + (32 * par) * SKV + 32 * cb + col;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) dq[cb] = mfma32(kc[mrow(t, half) * SKV], sc[t], dq[cb]);
+    }
+  }
+  constexpr int MS = NCB * 16;
+  __syncthreads();
+  float* mb = smem + (g * 64 + lane) * MS;
+  if (par == 1) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mb[cb * 16 + r] = dq[cb][r];
+  }
+  __syncthreads();
+  if (par == 1 || !qlive) return;
+  float* qrow = A.dQ + (int64_t)(q0 + q) * A.lddq + h * HD;
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int a4 = 0; a4 < 4; ++a4) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (dq[cb][4 * a4 + e] + mb[cb * 16 + 4 * a4 + e]) * A.scale;
+      *reinterpret_cast<float4*>(qrow + 32 * cb + 8 * a4 + 4 * half) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+}
+
+// Backward, key side: one wave per 32-key block (grid z covers the longest
+// sample); dV = P^T dO and dK = scale * dS^T Q over the sample's queries.  P
+// and dS are transposed through a per-wave LDS block so the query index can
+// be the MFMA's contraction index.
+template <int HD>
+__global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
+  constexpr int SQ = HD + 2;
+  constexpr int NT = HD / 2, NCB = HD / 32;
+  constexpr int ST = 33;  // transposition block row stride
+  __shared__ float sq[64 * SQ];
+  __shared__ float sdo[64 * SQ];
+  __shared__ float sD[64], sL[64];
+  __shared__ float sT[4][2][32 * ST];
+  const int k = blockIdx.x, h = blockIdx.y;
+  int32_t q0, Lq, Lk;
+  int64_t kv0;
+  attn_rows(A, k, q0, Lq, kv0, Lk);
+  if ((int32_t)blockIdx.z * 128 >= Lk) return;  // uniform over the workgroup
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  // queries (zero rows past Lq), dO, lse and D of the sample
+  for (int e = threadIdx.x; e < 64 * HD / 4; e += 256) {
+    const int rr = e / (HD / 4), c = 4 * (e % (HD / 4));
+    float4 qq = make_float4(0.f, 0.f, 0.f, 0.f), dd = qq;
+    if (rr < Lq) {
+      qq = *reinterpret_cast<const float4*>(A.Q + (int64_t)(q0 + rr) * A.ldq + h * HD + c);
+      dd = *reinterpret_cast<const float4*>(A.dO + (int64_t)(q0 + rr) * A.ldo + h * HD + c);
+    }
+    *reinterpret_cast<float2*>(sq + rr * SQ + c) = make_float2(qq.x, qq.y);
+    *reinterpret_cast<float2*>(sq + rr * SQ + c + 2) = make_float2(qq.z, qq.w);
+    *reinterpret_cast<float2*>(sdo + rr * SQ + c) = make_float2(dd.x, dd.y);
+    *reinterpret_cast<float2*>(sdo + rr * SQ + c + 2) = make_float2(dd.z, dd.w);
+  }
+  {
+    // D[q] = sum_c dO[q][c] O[q][c]: 4 threads per query
+    const int qq = threadIdx.x >> 2, part = threadIdx.x & 3;
+    float acc = 0.f;
+    if (qq < Lq) {
+      const float* orow = A.O + (int64_t)(q0 + qq) * A.ldo + h * HD;
+      const float* drow = A.dO + (int64_t)(q0 + qq) * A.ldo + h * HD;
+      for (int c = part; c < HD; c += 4) acc = fmaf(orow[c], drow[c], acc);
+    }
+    acc += __shfl_xor(acc, 1, 64);
+    acc += __shfl_xor(acc, 2, 64);
+    if (part == 0) {
+      sD[qq] = acc;
+      sL[qq] = qq < Lq ? A.lse[(int64_t)(q0 + qq) * A.nheads + h] : 0.f;
+    }
+  }
+  __syncthreads();
+  const int32_t kb = (int32_t)blockIdx.z * 128 + 32 * wave;
+  if (kb >= Lk) return;  // no barrier follows
+  const int32_t key = kb + col;  // this lane's key as an A row
+  float kreg[NT], vreg[NT];
+  {
+    const int64_t row = kv0 + min(key, Lk - 1);
+    const float* kr = A.K + row * A.ldkv + A.kcol + h * HD + half;
+    const float* vr = A.V + row * A.ldkv + A.vcol + h * HD + half;
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      kreg[i] = kr[2 * i];
+      vreg[i] = vr[2 * i];
+    }
+  }
+  f32x16v dk[NCB], dv[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dk[cb][r] = dv[cb][r] = 0.f;
+  float* tp = sT[wave][0];
+  float* tds = sT[wave][1];
+  for (int g = 0; 32 * g < Lq; ++g) {
+    f32x16v sc, dp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
+    const float* qr = sq + (32 * g + col) * SQ + half;
+    const float* dr = sdo + (32 * g + col) * SQ + half;
+#pragma unroll 16
+    for (int i = 0; i < NT; ++i) {
+      sc = mfma32(kreg[i], qr[2 * i], sc);
+      dp = mfma32(vreg[i], dr[2 * i], dp);
+    }
+    // sc[r] = S^T[key kb + mrow(r, half)][query 32g + col], dp[r] likewise
+    const int qq = 32 * g + col;
+    const float lq = sL[qq], dq = sD[qq];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int kr = mrow(r, half);
+      const bool ok = qq < Lq && kb + kr < Lk;
+      const float p = ok ? __expf(sc[r] * A.scale - lq) : 0.f;
+      tp[kr * ST + col] = p;
+      tds[kr * ST + col] = p * (dp[r] - dq);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's transposed blocks are written
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const int qi = 2 * t + half;  // contraction index: query 32g + qi
+        const float bdo = sdo[(32 * g + qi) * SQ + 32 * cb + col];
+        const float bq = sq[(32 * g + qi) * SQ + 32 * cb + col];
+        dv[cb] = mfma32(tp[col * ST + qi], bdo, dv[cb]);
+        dk[cb] = mfma32(tds[col * ST + qi], bq, dk[cb]);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+  }
+  // accumulator r of lane l: key kb + mrow(r, half), column 32cb + col
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int32_t kk = kb + mrow(r, half);
+      if (kk < Lk) {
+        const int64_t row = kv0 + kk;
+        A.dV[row * A.lddkv + A.dvcol + h * HD + 32 * cb + col] = dv[cb][r];
+        A.dK[row * A.lddkv + A.dkcol + h * HD + 32 * cb + col] = dk[cb][r] * A.scale;
+      }
+    }
 }
 
 hipError_t launch_xattn(hipStream_t s, const AttnArgs& A, int32_t nsamples, bool backward) {
-  if (A.Lq > kAQ || A.Lq < 1) return hipErrorInvalidValue;
-  dim3 grid(nsamples, A.nheads);
+  if (A.Lq > 64 || A.Lq < 1 || A.max_lk < 1) return hipErrorInvalidValue;
+  const dim3 grid(nsamples, A.nheads), gk(nsamples, A.nheads, (A.max_lk + 127) / 128);
   switch (A.hd) {
     case 64:
-      if (backward) xattn_bwd_kernel<64><<<grid, 256, 0, s>>>(A); else xattn_fwd_kernel<64><<<grid, 256, 0, s>>>(A);
+      if (backward) {
+        xattn_bwd_dq_kernel<64><<<grid, 256, 0, s>>>(A);
+        xattn_bwd_dkv_kernel<64><<<gk, 256, 0, s>>>(A);
+      } else {
+        xattn_fwd_kernel<64><<<grid, 256, 0, s>>>(A);
+      }
       break;
     case 128:
-      if (backward) xattn_bwd_kernel<128><<<grid, 256, 0, s>>>(A); else xattn_fwd_kernel<128><<<grid, 256, 0, s>>>(A);
+      if (backward) {
+        xattn_bwd_dq_kernel<128><<<grid, 256, 0, s>>>(A);
+        xattn_bwd_dkv_kernel<128><<<gk, 256, 0, s>>>(A);
+      } else {
+        xattn_fwd_kernel<128><<<grid, 256, 0, s>>>(A);
+      }
       break;
     default:
       return hipErrorInvalidValue;
