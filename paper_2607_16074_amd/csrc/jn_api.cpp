@@ -863,7 +863,7 @@ struct ExpPlan {
 // Workspace regions (byte offsets); per-layer saves are arrays of offsets.
 struct ExpLayout {
   size_t arena = 0, arena_bytes = 0;
-  size_t x, xf, yb, ub, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, TA, TB,
+  size_t x, xf, yb, ub, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, part, TA, TB,
       WT, dwinp, dwoutp;
   std::vector<size_t> x1, x2, x3, h1, h2, h3, qkv, os, osb, lses, qc, kv, oc, ocb, lsec, pre, mb;
   size_t total = 0;
@@ -973,6 +973,7 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.dkv = take(4 * Pz * 2 * d);
   Ly.dkvb = take(2 * Pz * 2 * d);
   Ly.gx = take(4 * Na * d);
+  Ly.part = take(4 * G * 16 * d);
   Ly.TA = take(2 * std::max<int64_t>(wmax * P.KaT, 2 * d * P.KzT));
   Ly.TB = take(2 * std::max<int64_t>(wmax * P.KaT, (int64_t)s.dp * P.KzT));
   Ly.WT = take(2 * G * std::max<int64_t>(f * d, 3 * d * d) + 2 * G * 2 * d * s.dp);
@@ -1124,7 +1125,8 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     const int64_t rows = P.Na;
     rec.ops.push_back([=](char* a) {
       return launch_xrms_bwd(s, F(x_at), (const void* const*)(a + gains_at), (const int32_t*)(a + roff_at), G,
-                             (int32_t)rows, (int32_t)d, S.eps, F(Ly.tf), F(Ly.dx), F(Ly.gx), (float* const*)(a + dg_at));
+                             (int32_t)rows, (int32_t)d, S.eps, F(Ly.tf), F(Ly.dx), F(Ly.gx), F(Ly.part),
+                             (float* const*)(a + dg_at));
     });
     rec.opcode.push_back(JN_OP_EXPERT_OTHER);
   };

@@ -147,7 +147,7 @@ struct CopyDesc {
   int64_t src_ld, dst_ld;
   int32_t rows, cols, src_rows, src_cols;
   int32_t src_bf16, dst_bf16;
-  int32_t block_start, reserved;
+  int32_t block_start, vec;  // filled by copy2d_prepare
 };
 int32_t copy2d_prepare(CopyDesc* d, int32_t n);
 hipError_t launch_copy2d(hipStream_t s, const CopyDesc* d, int32_t n, int32_t blocks);
@@ -171,9 +171,10 @@ hipError_t launch_prefix(hipStream_t s, const void* hidden, const int32_t* tenan
 // RMSNorm with per-tenant gains (rows tenant-contiguous, roff [G+1] device).
 hipError_t launch_xrms_fwd(hipStream_t s, const float* x, const void* const* gains, const int32_t* roff, int32_t G,
                            int32_t rows, int32_t d, float eps, void* h);
-// dx += dRMS(x, g) . dh ; dg[t] = column sums over tenant t's rows (gx scratch [rows][d]).
+// dx += dRMS(x, g) . dh ; dg[t] = column sums over tenant t's rows (gx scratch
+// [rows][d], part scratch [G][16][d]).
 hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gains, const int32_t* roff, int32_t G,
-                           int32_t rows, int32_t d, float eps, const float* dh, float* dx, float* gx,
+                           int32_t rows, int32_t d, float eps, const float* dh, float* dx, float* gx, float* part,
                            float* const* dg);
 
 // fp32 attention of each tenant-order sample k over its own keys: queries

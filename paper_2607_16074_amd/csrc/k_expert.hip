@@ -18,6 +18,28 @@
 namespace jnx {
 
 // ---------------------------------------------------------------- copy2d ---
+// Each block covers 2048 elements of one descriptor (row-major over rows x
+// cols).  Descriptors whose columns, leading dimensions and source width are
+// multiples of 4 move 4 elements per thread step (16-byte fp32 / 8-byte bf16
+// accesses); the rest go element by element.
+
+__device__ __forceinline__ void copy4_load(const CopyDesc& D, int64_t r, int64_t c, float (&v)[4]) {
+  if (r < D.src_rows && c < D.src_cols) {
+    const int64_t si = r * D.src_ld + c;
+    if (D.src_bf16) {
+      const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(D.src) + si);
+      v[0] = __uint_as_float(u.x << 16);
+      v[1] = __uint_as_float(u.x & 0xffff0000u);
+      v[2] = __uint_as_float(u.y << 16);
+      v[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else {
+      const float4 f = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(D.src) + si);
+      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    }
+  } else {
+    v[0] = v[1] = v[2] = v[3] = 0.f;
+  }
+}
 
 __global__ __launch_bounds__(256) void copy2d_kernel(const CopyDesc* __restrict__ descs, int32_t ndesc) {
   int32_t p = 0;
@@ -26,6 +48,24 @@ __global__ __launch_bounds__(256) void copy2d_kernel(const CopyDesc* __restrict_
   const CopyDesc D = descs[p];
   const int64_t total = (int64_t)D.rows * D.cols;
   const int64_t base = (int64_t)(b - D.block_start) * 256 * 8;
+  const bool vec = D.vec != 0;
+  if (vec) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int64_t e = base + ((int64_t)k * 256 + threadIdx.x) * 4;
+      if (e >= total) break;
+      const int64_t r = e / D.cols, c = e % D.cols;
+      float v[4];
+      copy4_load(D, r, c, v);
+      const int64_t di = r * D.dst_ld + c;
+      if (D.dst_bf16)
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(D.dst) + di) =
+            make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+      else
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(D.dst) + di) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    return;
+  }
   for (int k = 0; k < 8; ++k) {
     const int64_t e = base + (int64_t)k * 256 + threadIdx.x;
     if (e >= total) break;
@@ -46,8 +86,15 @@ __global__ __launch_bounds__(256) void copy2d_kernel(const CopyDesc* __restrict_
 int32_t copy2d_prepare(CopyDesc* d, int32_t n) {
   int32_t total = 0;
   for (int32_t i = 0; i < n; ++i) {
+    const CopyDesc& D = d[i];
+    const bool vec = D.cols % 4 == 0 && D.src_ld % 4 == 0 && D.dst_ld % 4 == 0 &&
+                     (D.src_cols % 4 == 0 || D.src_cols >= D.cols) &&
+                     (D.src == nullptr || reinterpret_cast<uintptr_t>(D.src) % 16 == 0) &&
+                     reinterpret_cast<uintptr_t>(D.dst) % 16 == 0;
+    d[i].vec = vec ? 1 : 0;
     d[i].block_start = total;
-    total += (int32_t)(((int64_t)d[i].rows * d[i].cols + 2047) / 2048);
+    // vector descriptors: 2048 elements per block as 512 threads-steps of 4
+    total += (int32_t)(((int64_t)D.rows * D.cols + 2047) / 2048);
   }
   return total;
 }
@@ -60,9 +107,12 @@ hipError_t launch_copy2d(hipStream_t s, const CopyDesc* d, int32_t n, int32_t bl
 
 // ------------------------------------------------------------- transpose ---
 // dst[c][r] = src[r][c] for r < rows, 0 for rows <= r < rows_pad; 64x64 tiles.
+// Tiles that lie wholly inside the source (and whose leading dimensions are
+// multiples of 8) move 16 bytes per thread access; edge tiles go element by
+// element.
 
 __global__ __launch_bounds__(256) void transpose_kernel(const TransDesc* __restrict__ descs, int32_t ndesc) {
-  __shared__ uint16_t tile[64][66];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
   int32_t p = 0;
   const int32_t b = blockIdx.x;
   while (p + 1 < ndesc && descs[p + 1].block_start <= b) ++p;
@@ -70,6 +120,25 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransDesc* __restr
   const int32_t tcols = (D.cols + 63) / 64;
   const int32_t local = b - D.block_start;
   const int32_t r0 = (local / tcols) * 64, c0 = (local % tcols) * 64;
+  const bool full = r0 + 64 <= D.rows && c0 + 64 <= D.cols && D.src_ld % 8 == 0 && D.dst_ld % 8 == 0 &&
+                    r0 + 64 <= D.rows_pad && reinterpret_cast<uintptr_t>(D.src) % 16 == 0 &&
+                    reinterpret_cast<uintptr_t>(D.dst) % 16 == 0;
+  if (full) {
+    // load: thread t takes row t >> 2, columns 16*(t & 3) .. +15
+    const int rr = threadIdx.x >> 2, cc = 16 * (threadIdx.x & 3);
+    const uint4* sp = reinterpret_cast<const uint4*>(D.src + (int64_t)(r0 + rr) * D.src_ld + c0 + cc);
+    *reinterpret_cast<uint4*>(&tile[rr][cc]) = sp[0];
+    *reinterpret_cast<uint4*>(&tile[rr][cc + 8]) = sp[1];
+    __syncthreads();
+    // store: thread t writes output row (input column) t >> 2, outputs 16*(t & 3) .. +15
+    uint32_t o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (uint32_t)tile[cc + 2 * i][rr] | ((uint32_t)tile[cc + 2 * i + 1][rr] << 16);
+    uint4* dp = reinterpret_cast<uint4*>(D.dst + (int64_t)(c0 + rr) * D.dst_ld + r0 + cc);
+    dp[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    dp[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    return;
+  }
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int32_t r = r0 + i, c = c0 + tx;
@@ -251,14 +320,31 @@ __global__ __launch_bounds__(256) void xrms_bwd_kernel(const float* __restrict__
   }
 }
 
-// dg_t[j] = sum over tenant t's rows of gx[row][j]  (grid: tenant x column block)
-__global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ gx, const int32_t* __restrict__ roff,
-                                                    float* const* __restrict__ out, int32_t d) {
+// dg_t[j] = sum over tenant t's rows of gx[row][j], in two fixed-order stages:
+// partial sums over kColSeg row segments, then the sum of the segments.
+constexpr int kColSeg = 16;
+
+__global__ __launch_bounds__(256) void colsum_part_kernel(const float* __restrict__ gx, const int32_t* __restrict__ roff,
+                                                          float* __restrict__ part, int32_t d) {
+  const int32_t t = blockIdx.x, seg = blockIdx.z;
+  const int32_t j = blockIdx.y * 256 + threadIdx.x;
+  if (j >= d) return;
+  const int32_t r0 = roff[t], n = roff[t + 1] - r0;
+  const int32_t per = (n + kColSeg - 1) / kColSeg;
+  const int32_t a = r0 + min(n, seg * per), b = r0 + min(n, (seg + 1) * per);
+  float s = 0.f;
+  for (int32_t r = a; r < b; ++r) s += gx[(int64_t)r * d + j];
+  part[((int64_t)t * kColSeg + seg) * d + j] = s;
+}
+
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part, float* const* __restrict__ out,
+                                                           int32_t d) {
   const int32_t t = blockIdx.x;
   const int32_t j = blockIdx.y * 256 + threadIdx.x;
   if (j >= d) return;
   float s = 0.f;
-  for (int32_t r = roff[t]; r < roff[t + 1]; ++r) s += gx[(int64_t)r * d + j];
+#pragma unroll
+  for (int seg = 0; seg < kColSeg; ++seg) s += part[((int64_t)t * kColSeg + seg) * d + j];
   out[t][j] = s;
 }
 
@@ -278,7 +364,7 @@ hipError_t launch_xrms_fwd(hipStream_t s, const float* x, const void* const* gai
 }
 
 hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gains, const int32_t* roff, int32_t G,
-                           int32_t rows, int32_t d, float eps, const float* dh, float* dx, float* gx,
+                           int32_t rows, int32_t d, float eps, const float* dh, float* dx, float* gx, float* part,
                            float* const* dg) {
   dim3 grid((rows + 3) / 4);
   auto gp = reinterpret_cast<const uint16_t* const*>(gains);
@@ -289,8 +375,9 @@ hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gai
     case 2048: xrms_bwd_kernel<8><<<grid, 256, 0, s>>>(x, gp, roff, G, rows, d, eps, dh, dx, gx); break;
     default: return hipErrorInvalidValue;
   }
-  dim3 g2(G, (d + 255) / 256);
-  colsum_kernel<<<g2, 256, 0, s>>>(gx, roff, dg, d);
+  dim3 g2(G, (d + 255) / 256, kColSeg), g3(G, (d + 255) / 256);
+  colsum_part_kernel<<<g2, 256, 0, s>>>(gx, roff, part, d);
+  colsum_final_kernel<<<g3, 256, 0, s>>>(part, dg, d);
   return hipGetLastError();
 }
 
