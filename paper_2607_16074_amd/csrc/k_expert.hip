@@ -417,8 +417,10 @@ __device__ __forceinline__ void attn_rows(const AttnArgs& A, int32_t k, int32_t&
   }
 }
 
-// Stage rows j0 .. j0+63 of K and V (head h, zero past Lk) into LDS, row
-// strides SKV floats (8-byte aligned rows: float2 stores).
+// Stage rows j0 .. j0+63 of K and V (head h, zero past Lk) into LDS with row
+// stride SKV floats.  ds_read_b32 serves each half-wave from 32 banks, so an
+// odd stride makes "one row per lane" reads conflict-free; "one column per
+// lane" reads are conflict-free for any stride.
 template <int HD, int SKV>
 __device__ __forceinline__ void attn_stage_kv(const AttnArgs& A, int64_t kv0, int32_t Lk, int32_t j0, int h,
                                               float* sk, float* sv) {
@@ -430,10 +432,21 @@ __device__ __forceinline__ void attn_stage_kv(const AttnArgs& A, int64_t kv0, in
       kq = *reinterpret_cast<const float4*>(A.K + row * A.ldkv + A.kcol + h * HD + c);
       vq = *reinterpret_cast<const float4*>(A.V + row * A.ldkv + A.vcol + h * HD + c);
     }
-    *reinterpret_cast<float2*>(sk + rr * SKV + c) = make_float2(kq.x, kq.y);
-    *reinterpret_cast<float2*>(sk + rr * SKV + c + 2) = make_float2(kq.z, kq.w);
-    *reinterpret_cast<float2*>(sv + rr * SKV + c) = make_float2(vq.x, vq.y);
-    *reinterpret_cast<float2*>(sv + rr * SKV + c + 2) = make_float2(vq.z, vq.w);
+    float* kd = sk + rr * SKV + c;
+    float* vd = sv + rr * SKV + c;
+    kd[0] = kq.x; kd[1] = kq.y; kd[2] = kq.z; kd[3] = kq.w;
+    vd[0] = vq.x; vd[1] = vq.y; vd[2] = vq.z; vd[3] = vq.w;
+  }
+}
+
+// reg[i] = row[2i + half], i < HD/2, through 16-byte loads
+template <int HD>
+__device__ __forceinline__ void attn_row_regs(const float* row, int half, float (&reg)[HD / 2]) {
+#pragma unroll
+  for (int j = 0; j < HD / 4; ++j) {
+    const float4 f = *reinterpret_cast<const float4*>(row + 4 * j);
+    reg[2 * j] = half ? f.y : f.x;
+    reg[2 * j + 1] = half ? f.w : f.z;
   }
 }
 
@@ -442,7 +455,7 @@ __device__ __forceinline__ void attn_stage_kv(const AttnArgs& A, int64_t kv0, in
 // halves merge their (max, sum, output) at the end.
 template <int HD>
 __global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
-  constexpr int SKV = HD + 2;  // K rows read lane-per-row: 2*row + half covers all banks
+  constexpr int SKV = HD + 1;
   constexpr int NT = HD / 2, NCB = HD / 32;
   __shared__ float smem[2 * 64 * SKV];
   float* sk = smem;
@@ -456,10 +469,10 @@ __global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
   const int q = 32 * g + col;
   const bool qlive = q < Lq, glive = 32 * g < Lq;
   float qreg[NT];
-  {
-    const float* qr = A.Q + (int64_t)(q0 + min(q, Lq - 1)) * A.ldq + h * HD + half;
+  attn_row_regs<HD>(A.Q + (int64_t)(q0 + min(q, Lq - 1)) * A.ldq + h * HD, half, qreg);
+  if (!qlive) {
 #pragma unroll
-    for (int i = 0; i < NT; ++i) qreg[i] = qlive ? qr[2 * i] : 0.f;
+    for (int i = 0; i < NT; ++i) qreg[i] = 0.f;
   }
   f32x16v o[NCB];
 #pragma unroll
@@ -546,7 +559,7 @@ __global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
 // roles as the forward; the key halves' partial dQ are summed at the end.
 template <int HD>
 __global__ __launch_bounds__(256) void xattn_bwd_dq_kernel(AttnArgs A) {
-  constexpr int SKV = HD + 2;
+  constexpr int SKV = HD + 1;
   constexpr int NT = HD / 2, NCB = HD / 32;
   __shared__ float smem[2 * 64 * SKV];
   float* sk = smem;
@@ -563,16 +576,21 @@ __global__ __launch_bounds__(256) void xattn_bwd_dq_kernel(AttnArgs A) {
   float Dq = 0.f, lse = 0.f;
   {
     const int64_t row = q0 + min(q, Lq - 1);
-    const float* qr = A.Q + row * A.ldq + h * HD + half;
-    const float* dr = A.dO + row * A.ldo + h * HD + half;
-    const float* orr = A.O + row * A.ldo + h * HD + half;
+    attn_row_regs<HD>(A.Q + row * A.ldq + h * HD, half, qreg);
+    attn_row_regs<HD>(A.dO + row * A.ldo + h * HD, half, dreg);
+    const float* orr = A.O + row * A.ldo + h * HD;
 #pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      qreg[i] = qlive ? qr[2 * i] : 0.f;
-      dreg[i] = qlive ? dr[2 * i] : 0.f;
-      Dq = fmaf(dreg[i], qlive ? orr[2 * i] : 0.f, Dq);
+    for (int j = 0; j < HD / 4; ++j) {
+      const float4 f = *reinterpret_cast<const float4*>(orr + 4 * j);
+      Dq = fmaf(dreg[2 * j], half ? f.y : f.x, Dq);
+      Dq = fmaf(dreg[2 * j + 1], half ? f.w : f.z, Dq);
     }
     Dq += __shfl_xor(Dq, 32, 64);
+    if (!qlive) {
+      Dq = 0.f;
+#pragma unroll
+      for (int i = 0; i < NT; ++i) qreg[i] = dreg[i] = 0.f;
+    }
     lse = qlive ? A.lse[row * A.nheads + h] : 0.f;
   }
   f32x16v dq[NCB];
@@ -633,18 +651,16 @@ __global__ __launch_bounds__(256) void xattn_bwd_dq_kernel(AttnArgs A) {
 }
 
 // Backward, key side: one wave per 32-key block (grid z covers the longest
-// sample); dV = P^T dO and dK = scale * dS^T Q over the sample's queries.  P
-// and dS are transposed through a per-wave LDS block so the query index can
-// be the MFMA's contraction index.
+// sample).  Scores are computed untransposed here, S = Q K^T (lane = key,
+// registers = queries), so P and dS are already the B operands of
+// dV^T = dO^T P and dK^T = Q^T dS with the query index permuted as in the
+// forward: nothing is transposed through memory.
 template <int HD>
 __global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
-  constexpr int SQ = HD + 2;
+  constexpr int SQ = HD + 1;
   constexpr int NT = HD / 2, NCB = HD / 32;
-  constexpr int ST = 33;  // transposition block row stride
-  __shared__ float sq[64 * SQ];
-  __shared__ float sdo[64 * SQ];
+  __shared__ float sq[64 * SQ], sdo[64 * SQ];
   __shared__ float sD[64], sL[64];
-  __shared__ float sT[4][2][32 * ST];
   const int k = blockIdx.x, h = blockIdx.y;
   int32_t q0, Lq, Lk;
   int64_t kv0;
@@ -652,7 +668,6 @@ __global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
   if ((int32_t)blockIdx.z * 128 >= Lk) return;  // uniform over the workgroup
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
-  // queries (zero rows past Lq), dO, lse and D of the sample
   for (int e = threadIdx.x; e < 64 * HD / 4; e += 256) {
     const int rr = e / (HD / 4), c = 4 * (e % (HD / 4));
     float4 qq = make_float4(0.f, 0.f, 0.f, 0.f), dd = qq;
@@ -660,19 +675,23 @@ __global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
       qq = *reinterpret_cast<const float4*>(A.Q + (int64_t)(q0 + rr) * A.ldq + h * HD + c);
       dd = *reinterpret_cast<const float4*>(A.dO + (int64_t)(q0 + rr) * A.ldo + h * HD + c);
     }
-    *reinterpret_cast<float2*>(sq + rr * SQ + c) = make_float2(qq.x, qq.y);
-    *reinterpret_cast<float2*>(sq + rr * SQ + c + 2) = make_float2(qq.z, qq.w);
-    *reinterpret_cast<float2*>(sdo + rr * SQ + c) = make_float2(dd.x, dd.y);
-    *reinterpret_cast<float2*>(sdo + rr * SQ + c + 2) = make_float2(dd.z, dd.w);
+    float* qd = sq + rr * SQ + c;
+    float* dd2 = sdo + rr * SQ + c;
+    qd[0] = qq.x; qd[1] = qq.y; qd[2] = qq.z; qd[3] = qq.w;
+    dd2[0] = dd.x; dd2[1] = dd.y; dd2[2] = dd.z; dd2[3] = dd.w;
   }
   {
-    // D[q] = sum_c dO[q][c] O[q][c]: 4 threads per query
+    // D[q] = sum_c dO[q][c] O[q][c]: 4 threads per query, 16-byte loads
     const int qq = threadIdx.x >> 2, part = threadIdx.x & 3;
     float acc = 0.f;
     if (qq < Lq) {
       const float* orow = A.O + (int64_t)(q0 + qq) * A.ldo + h * HD;
       const float* drow = A.dO + (int64_t)(q0 + qq) * A.ldo + h * HD;
-      for (int c = part; c < HD; c += 4) acc = fmaf(orow[c], drow[c], acc);
+      for (int c = 4 * part; c < HD; c += 16) {
+        const float4 o4 = *reinterpret_cast<const float4*>(orow + c);
+        const float4 d4 = *reinterpret_cast<const float4*>(drow + c);
+        acc = fmaf(o4.x, d4.x, fmaf(o4.y, d4.y, fmaf(o4.z, d4.z, fmaf(o4.w, d4.w, acc))));
+      }
     }
     acc += __shfl_xor(acc, 1, 64);
     acc += __shfl_xor(acc, 2, 64);
@@ -684,74 +703,62 @@ __global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
   __syncthreads();
   const int32_t kb = (int32_t)blockIdx.z * 128 + 32 * wave;
   if (kb >= Lk) return;  // no barrier follows
-  const int32_t key = kb + col;  // this lane's key as an A row
+  const bool kvalid = kb + col < Lk;  // this lane's key
   float kreg[NT], vreg[NT];
   {
-    const int64_t row = kv0 + min(key, Lk - 1);
-    const float* kr = A.K + row * A.ldkv + A.kcol + h * HD + half;
-    const float* vr = A.V + row * A.ldkv + A.vcol + h * HD + half;
-#pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      kreg[i] = kr[2 * i];
-      vreg[i] = vr[2 * i];
-    }
+    const int64_t row = kv0 + min(kb + col, Lk - 1);
+    attn_row_regs<HD>(A.K + row * A.ldkv + A.kcol + h * HD, half, kreg);
+    attn_row_regs<HD>(A.V + row * A.ldkv + A.vcol + h * HD, half, vreg);
   }
   f32x16v dk[NCB], dv[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dk[cb][r] = dv[cb][r] = 0.f;
-  float* tp = sT[wave][0];
-  float* tds = sT[wave][1];
   for (int g = 0; 32 * g < Lq; ++g) {
     f32x16v sc, dp;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
-    const float* qr = sq + (32 * g + col) * SQ + half;
-    const float* dr = sdo + (32 * g + col) * SQ + half;
+    const float* qa = sq + (32 * g + col) * SQ + half;
+    const float* da = sdo + (32 * g + col) * SQ + half;
 #pragma unroll 16
     for (int i = 0; i < NT; ++i) {
-      sc = mfma32(kreg[i], qr[2 * i], sc);
-      dp = mfma32(vreg[i], dr[2 * i], dp);
+      sc = mfma32(qa[2 * i], kreg[i], sc);  // S[query 32g + mrow(r)][key kb + col]
+      dp = mfma32(da[2 * i], vreg[i], dp);
     }
-    // sc[r] = S^T[key kb + mrow(r, half)][query 32g + col], dp[r] likewise
-    const int qq = 32 * g + col;
-    const float lq = sL[qq], dq = sD[qq];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int kr = mrow(r, half);
-      const bool ok = qq < Lq && kb + kr < Lk;
-      const float p = ok ? __expf(sc[r] * A.scale - lq) : 0.f;
-      tp[kr * ST + col] = p;
-      tds[kr * ST + col] = p * (dp[r] - dq);
+      const int qq = 32 * g + mrow(r, half);
+      const bool ok = kvalid && qq < Lq;
+      const float p = ok ? __expf(sc[r] * A.scale - sL[qq]) : 0.f;
+      dp[r] = p * (dp[r] - sD[qq]);  // dS
+      sc[r] = p;
     }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's transposed blocks are written
-    __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
+    for (int t = 0; t < 16; ++t) {
+      const int qr = 32 * g + mrow(t, half);
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        const int qi = 2 * t + half;  // contraction index: query 32g + qi
-        const float bdo = sdo[(32 * g + qi) * SQ + 32 * cb + col];
-        const float bq = sq[(32 * g + qi) * SQ + 32 * cb + col];
-        dv[cb] = mfma32(tp[col * ST + qi], bdo, dv[cb]);
-        dk[cb] = mfma32(tds[col * ST + qi], bq, dk[cb]);
+      for (int cb = 0; cb < NCB; ++cb) {
+        dv[cb] = mfma32(sdo[qr * SQ + 32 * cb + col], sc[t], dv[cb]);
+        dk[cb] = mfma32(sq[qr * SQ + 32 * cb + col], dp[t], dk[cb]);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_wave_barrier();
   }
-  // accumulator r of lane l: key kb + mrow(r, half), column 32cb + col
+  // dV^T / dK^T accumulators: lane = key kb + col, register r = column 32cb + mrow(r, half)
+  if (!kvalid) return;
+  const int64_t row = kv0 + kb + col;
+  float* dvr = A.dV + row * A.lddkv + A.dvcol + h * HD;
+  float* dkr = A.dK + row * A.lddkv + A.dkcol + h * HD;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int32_t kk = kb + mrow(r, half);
-      if (kk < Lk) {
-        const int64_t row = kv0 + kk;
-        A.dV[row * A.lddkv + A.dvcol + h * HD + 32 * cb + col] = dv[cb][r];
-        A.dK[row * A.lddkv + A.dkcol + h * HD + 32 * cb + col] = dk[cb][r] * A.scale;
-      }
+    for (int a4 = 0; a4 < 4; ++a4) {
+      const int c = 32 * cb + 8 * a4 + 4 * half;
+      *reinterpret_cast<float4*>(dvr + c) =
+          make_float4(dv[cb][4 * a4], dv[cb][4 * a4 + 1], dv[cb][4 * a4 + 2], dv[cb][4 * a4 + 3]);
+      *reinterpret_cast<float4*>(dkr + c) =
+          make_float4(dk[cb][4 * a4] * A.scale, dk[cb][4 * a4 + 1] * A.scale, dk[cb][4 * a4 + 2] * A.scale,
+                      dk[cb][4 * a4 + 3] * A.scale);
     }
 }
 
