@@ -122,6 +122,11 @@ def test_host_plan_errors(lib):
     with pytest.raises(lib.JNError) as e:
         lib.jn_pack_plan(_reqs(lib, [0], [[2]], [4]), T(), d, 0)
     assert e.value.status == lib._abi.JN_EINVAL
+    # a batch whose packed rows overflow 32-bit row indices (lengths only; nothing is read)
+    big = 1 << 30
+    with pytest.raises(lib.JNError) as e:
+        lib.jn_pack_plan(_reqs(lib, [0], [[big, big]], [big]), T(), d, 1)
+    assert e.value.status == lib._abi.JN_ESHAPE
 
 
 # ------------------------------------------------------ expert validation ---

@@ -4,7 +4,9 @@ The oracle runs with the GPU's rounding points (bf16 GEMM operands, see
 ``oracle.expert``) and takes the GPU's backbone rows as each sample's
 prefix, so the expert stage is checked on its own (stage-wise).  Bars: loss
 within 1e-3 relative; predictions and every weight / gain gradient within
-1e-2 relative L2 per tensor.  The 1e-2 is derived, not tuned: perturbing the
+1e-2 relative L2 per tensor (a gradient whose norm is below 1e-4 of the
+tenant's largest, e.g. one that vanishes analytically, is measured against
+that 1e-4 floor).  The 1e-2 is derived, not tuned: perturbing the
 oracle's own values by fp32-sized relative noise (2^-22) before each bf16
 rounding point moves these tensors by 1e-3 .. 5e-3 (2 to 6 layers), because
 a value that lands on the other side of a bf16 rounding boundary changes by
@@ -78,14 +80,21 @@ def check_stagewise(wl, st, targets, noisy, only=None):
         z = [hidden[cu[i]: cu[i] + sl[i]] for i in perm[tso[k]: tso[k + 1]]]
         ref = oexpert.expert_step(wl.experts[g], L, H, eps, list(noisy[g]), z, targets[g], rnd=True)
         io = st.ios[k]
+        # a gradient that vanishes analytically (e.g. the queries of a one-key
+        # attention) is compared against the tenant's gradient scale instead
+        floor = 1e-4 * max(float(np.linalg.norm(v)) for v in ref["grads"].values())
+
+        def grel(g, o):
+            o = np.asarray(o, np.float64)
+            return float(np.linalg.norm(np.asarray(g, np.float64) - o) / max(np.linalg.norm(o), floor))
         errs = {"pred": rel_l2(io.pred.cpu().numpy(), ref["pred"]),
                 "loss": abs(float(io.loss.cpu()) - ref["loss"]) / abs(ref["loss"]),
-                "w_in": rel_l2(io.dw_in.cpu().numpy(), ref["grads"]["w_in"]),
-                "w_out": rel_l2(io.dw_out.cpu().numpy(), ref["grads"]["w_out"]),
-                "gf": rel_l2(io.dgf.cpu().numpy(), ref["grads"]["gf"])}
+                "w_in": grel(io.dw_in.cpu().numpy(), ref["grads"]["w_in"]),
+                "w_out": grel(io.dw_out.cpu().numpy(), ref["grads"]["w_out"]),
+                "gf": grel(io.dgf.cpu().numpy(), ref["grads"]["gf"])}
         for l, lg in enumerate(io.layers):
             for name, t in lg.items():
-                errs[f"{l}.{name}"] = rel_l2(t.cpu().numpy(), ref["grads"][f"{l}.{name}"])
+                errs[f"{l}.{name}"] = grel(t.cpu().numpy(), ref["grads"][f"{l}.{name}"])
         _say(f"tenant {g}: " + ", ".join(f"{n}={e:.2e}" for n, e in errs.items()))
         bad = {n: e for n, e in errs.items() if not e < (LOSS_TOL if n == "loss" else TOL)}
         assert not bad, (g, bad)
@@ -109,6 +118,15 @@ def test_expert_hd128_full_chunk(jn):
     spec = expert_spec((1, 512, 4, 1024), 64, [(2, 32), (3, 1)], lo=30, hi=120, max_len=140)
     wl = W.make_workload(spec)
     _say("expert hd128 chunk64")
+    st, targets, noisy = run_experts(wl)
+    check_stagewise(wl, st, targets, noisy)
+
+
+def test_expert_degenerate_single_token(jn):
+    """One sample with a one-row prefix, one action token of width 1."""
+    spec = expert_spec((1, 256, 4, 256), 1, [(1, 1)], img=0, lo=1, hi=1, max_len=4)
+    wl = W.make_workload(spec)
+    _say("expert single token")
     st, targets, noisy = run_experts(wl)
     check_stagewise(wl, st, targets, noisy)
 

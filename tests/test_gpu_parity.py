@@ -261,6 +261,23 @@ def test_config3_sampled_end_to_end(jn):
     _say(f"  hidden {worst:.3e} on {len(keys)} samples, head grads {gw:.3e}")
 
 
+def test_single_sample_of_length_one(jn):
+    """The smallest batch: one tenant, one request, one sample of one token,
+    padded to a canonical length of 4 (degenerate attention: softmax over one
+    key; pooling over one row)."""
+    import oracle
+    ten = (W.TenantSpec(1, 0, 1, 1, 4, (128, 64, 6), 3, 2),)
+    spec = W.WorkloadSpec(92, W.BackboneSpec(2, 128, 4, 256, False), ten, 0, "single")
+    wl = W.make_workload(spec)
+    assert wl.requests[0].lengths.tolist() == [1]
+    _say("single sample, length 1")
+    st = run_group(wl, align=16)
+    _check_backbone(wl, st)
+    ref = oracle.step.isolated(wl)
+    assert maxrel(st.pooled.cpu().numpy()[0], ref["pooled"][(0, 0)]) < BF16_TOL
+    check_heads_stagewise(wl, st)
+
+
 def test_grouped_equals_isolated_bitwise(jn):
     """The defining invariant (Sec. 5.2): grouping changes no tenant's result."""
     from paper_2607_16074_amd import step as jstep
