@@ -137,6 +137,7 @@ def main():
     ap.add_argument("--align", type=int, default=1)
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-optimizer", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-kernel time shares to stderr")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a 512 MiB device copy first (reference dispatch for PMC byte counters)")
@@ -210,6 +211,28 @@ def main():
         del iso
         torch.cuda.synchronize()
 
+    # the per-tenant AdamW step over the group's tenant parameters (not part of `value`)
+    opt_stats = None
+    if not args.no_optimizer:
+        opt = jstep.TenantOptimizer(grouped, lr=1e-4, weight_decay=0.01)
+        opt.step()
+        torch.cuda.synchronize()
+        grouped.ctx.set_trace(True)
+        for _ in range(5):
+            opt.step()
+        torch.cuda.synchronize()
+        tr = [e for e in grouped.ctx.trace_read() if e[0] == "optimizer"]
+        grouped.ctx.set_trace(False)
+        ms = sum(e[4] for e in tr) / max(1, len(tr))
+        elems = sum(int(p.numel()) for ps, _, _ in opt.sets for p in ps)
+        b16 = sum(int(p.numel()) for ps, _, b in opt.sets if b is not None for p in ps)
+        nbytes = 28 * elems + 2 * b16
+        opt_stats = {"ms": ms, "params": elems, "bytes": nbytes, "GB_per_s": nbytes / (ms * 1e-3) / 1e9,
+                     "frac_of_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+        log(f"optimizer: {ms:.3f} ms for {elems} parameters ({opt_stats['GB_per_s']:.0f} GB/s)")
+        del opt
+        torch.cuda.synchronize()
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_oracle_baseline(wl)
@@ -248,6 +271,7 @@ def main():
                      "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(args.config),
                      "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},
         "gemm_by_op": gemm_stats,
+        "tenant_optimizer": opt_stats,
         "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample")},
     }
     print(json.dumps(result), flush=True)

@@ -16,6 +16,9 @@
  *                          action-head forward, loss, weight gradients (the
  *                          tenant-private decode / loss / backward of Sec. 5.2;
  *                          nothing is averaged across tenants)
+ *   jn_tenant_experts_fwd_bwd the same for tenants whose action module is a
+ *                          transformer expert reading each sample's backbone rows
+ *   jn_tenant_adamw_step   per-tenant AdamW update of the tenants' parameters
  *   jn_unpack              scatter packed rows back to the requests' own
  *                          padded buffers (the "split" by slices, App. A.3)
  *
@@ -71,7 +74,7 @@ typedef enum jn_op {
   JN_OP_PACK = 1, JN_OP_RMSNORM = 2, JN_OP_GEMM_QKV = 3, JN_OP_ATTENTION = 4, JN_OP_GEMM_O = 5,
   JN_OP_GEMM_UP = 6, JN_OP_GEMM_DOWN = 7, JN_OP_POOL = 8, JN_OP_HEAD_FWD = 9, JN_OP_LOSS = 10,
   JN_OP_HEAD_BWD = 11, JN_OP_UNPACK = 12, JN_OP_EXPERT_GEMM = 13, JN_OP_EXPERT_ATTENTION = 14,
-  JN_OP_EXPERT_OTHER = 15
+  JN_OP_EXPERT_OTHER = 15, JN_OP_OPTIMIZER = 16
 } jn_op;
 
 /* One traced kernel launch.  For GEMMs (M, N, K) is the launch shape
@@ -322,6 +325,39 @@ jn_status jn_experts_workspace_size(const jn_packed* p, const jn_expert* ex, con
  * be 16-byte aligned. */
 jn_status jn_tenant_experts_fwd_bwd(jn_ctx* ctx, const jn_packed* p, const void* hidden, const jn_expert* ex,
                                     const jn_expert_io* io, int32_t G, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------- tenant optimizer --- */
+
+/* One AdamW step for every tenant of a group: each tenant applies its own
+ * optimizer step to its own parameters and nothing is shared (Sec. 5.2,
+ * training-side group execution).  Tenant g owns n_tensors fp32 parameter
+ * tensors with their gradients and first / second moments (device pointers,
+ * same element counts, 16-byte aligned).  Per element, with t = step:
+ *   m = b1 m + (1 - b1) g;   v = b2 v + (1 - b2) g^2;
+ *   p = p (1 - lr wd) - (lr / (1 - b1^t)) m / (sqrt(v) / sqrt(1 - b2^t) + eps)
+ * `step` is this update's 1-based index, i.e. the tenant's version after it;
+ * the caller advances it only for the tenants it passes.  bf16_out (optional;
+ * NULL, or host [n] whose non-NULL entries are device bf16 tensors) receives
+ * the new parameters rounded to bf16, for tenants whose forward reads bf16
+ * copies.  One launch for all tensors of all tenants; the descriptor table
+ * goes to the caller's workspace. */
+typedef struct jn_adamw_tenant {
+  float lr, beta1, beta2, eps, weight_decay;
+  int32_t n_tensors;
+  int64_t step;
+  float* const* params;        /* host [n] of device fp32, updated in place */
+  const float* const* grads;   /* host [n] of device fp32 */
+  float* const* m;             /* host [n] of device fp32, updated in place */
+  float* const* v;             /* host [n] of device fp32, updated in place */
+  const int64_t* numel;        /* host [n] */
+  void* const* bf16_out;       /* NULL or host [n] of device bf16 (entries may be NULL) */
+} jn_adamw_tenant;
+
+jn_status jn_adamw_workspace_size(const jn_adamw_tenant* t, int32_t G, size_t* bytes);
+
+/* Errors: JN_EINVAL for null or unaligned pointers, step < 1, lr < 0,
+ * betas outside [0, 1), eps <= 0 or numel < 0; nothing is enqueued then. */
+jn_status jn_tenant_adamw_step(jn_ctx* ctx, const jn_adamw_tenant* t, int32_t G, void* ws, size_t ws_bytes);
 
 /* -------------------------------------------------------------- unpack --- */
 

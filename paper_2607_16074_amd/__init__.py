@@ -14,7 +14,7 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 from . import _abi
-from ._abi import (EXPERT_LAYER_FIELDS, JN_OK, STATUS_NAMES, jn_backbone, jn_expert, jn_expert_io,
+from ._abi import (EXPERT_LAYER_FIELDS, JN_OK, STATUS_NAMES, jn_adamw_tenant, jn_backbone, jn_expert, jn_expert_io,
                    jn_expert_layer, jn_expert_layer_grads, jn_head, jn_head_io, jn_layer, jn_pack_opts,
                    jn_pack_sizes, jn_packed, jn_request, jn_tenant)
 
@@ -25,6 +25,7 @@ __all__ = [
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group", "jn_backbone_workspace_size",
     "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
     "Expert", "ExpertIO", "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
+    "AdamWTenant", "jn_adamw_workspace_size", "jn_tenant_adamw_step",
     "lib_path",
 ]
 
@@ -372,6 +373,58 @@ def jn_tenant_experts_fwd_bwd(ctx: Context, packed: Packed, hidden, ex: Sequence
     ea, ia = _expert_arrays(ex, ios)
     _check(_lib.jn_tenant_experts_fwd_bwd(ctx.handle, C.byref(packed.struct), _ptr(hidden), ea, ia, len(ex),
                                           _ptr(ws), ws.numel() * ws.element_size()), ctx)
+
+
+# ---------------------------------------------------- tenant optimizer ------
+
+class AdamWTenant:
+    """One tenant's AdamW step: lists of device fp32 tensors (params, grads,
+    first and second moments), optional bf16 copies (None entries allowed),
+    hyperparameters and the 1-based index of this step."""
+
+    def __init__(self, params: list, grads: list, m: list, v: list, step: int, lr: float, beta1: float = 0.9,
+                 beta2: float = 0.999, eps: float = 1e-8, weight_decay: float = 0.0, bf16_out: Optional[list] = None):
+        self.tensors = (params, grads, m, v, bf16_out)
+        n = len(params)
+        import torch
+        if not (len(grads) == len(m) == len(v) == n) or (bf16_out is not None and len(bf16_out) != n):
+            raise ValueError("params, grads, m, v (and bf16_out) must have one entry per tensor")
+        for i in range(n):
+            for name, t in (("params", params[i]), ("grads", grads[i]), ("m", m[i]), ("v", v[i])):
+                if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != params[i].numel():
+                    raise TypeError(f"{name}[{i}] must be a contiguous float32 tensor of {params[i].numel()} elements")
+            if bf16_out is not None and bf16_out[i] is not None:
+                b = bf16_out[i]
+                if b.dtype != torch.bfloat16 or not b.is_contiguous() or b.numel() != params[i].numel():
+                    raise TypeError(f"bf16_out[{i}] must be a contiguous bfloat16 tensor of {params[i].numel()} elements")
+        s = jn_adamw_tenant()
+        s.lr, s.beta1, s.beta2, s.eps, s.weight_decay = float(lr), float(beta1), float(beta2), float(eps), float(weight_decay)
+        s.n_tensors = n
+        s.step = int(step)
+        mk = lambda xs: (C.c_void_p * max(n, 1))(*[_ptr(x) for x in xs])  # noqa: E731
+        self._p, self._g, self._m, self._v = mk(params), mk(grads), mk(m), mk(v)
+        self._n = (C.c_int64 * max(n, 1))(*[int(x.numel()) for x in params])
+        s.params = C.cast(self._p, C.POINTER(C.c_void_p))
+        s.grads = C.cast(self._g, C.POINTER(C.c_void_p))
+        s.m = C.cast(self._m, C.POINTER(C.c_void_p))
+        s.v = C.cast(self._v, C.POINTER(C.c_void_p))
+        s.numel = C.cast(self._n, C.POINTER(C.c_int64))
+        if bf16_out is not None:
+            self._b = (C.c_void_p * max(n, 1))(*[_ptr(x) if x is not None else None for x in bf16_out])
+            s.bf16_out = C.cast(self._b, C.POINTER(C.c_void_p))
+        self.struct = s
+
+
+def jn_adamw_workspace_size(tenants: Sequence[AdamWTenant]) -> int:
+    arr = (jn_adamw_tenant * len(tenants))(*[t.struct for t in tenants])
+    n = C.c_size_t()
+    _check(_lib.jn_adamw_workspace_size(arr, len(tenants), C.byref(n)), what="jn_adamw_workspace_size")
+    return int(n.value)
+
+
+def jn_tenant_adamw_step(ctx: Context, tenants: Sequence[AdamWTenant], ws):
+    arr = (jn_adamw_tenant * len(tenants))(*[t.struct for t in tenants])
+    _check(_lib.jn_tenant_adamw_step(ctx.handle, arr, len(tenants), _ptr(ws), ws.numel() * ws.element_size()), ctx)
 
 
 # -------------------------------------------------------------- unpack ------

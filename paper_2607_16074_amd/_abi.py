@@ -24,13 +24,14 @@ EXPORTS = (
     "jn_backbone_workspace_size", "jn_backbone_forward",
     "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd",
     "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
+    "jn_adamw_workspace_size", "jn_tenant_adamw_step",
     "jn_unpack",
 )
 
 
 OPS = {1: "pack", 2: "rmsnorm", 3: "gemm_qkv", 4: "attention", 5: "gemm_o", 6: "gemm_up", 7: "gemm_down",
        8: "pool", 9: "head_fwd", 10: "loss", 11: "head_bwd", 12: "unpack", 13: "expert_gemm",
-       14: "expert_attention", 15: "expert_other"}
+       14: "expert_attention", 15: "expert_other", 16: "optimizer"}
 
 
 class jn_trace_entry(C.Structure):
@@ -121,6 +122,13 @@ class jn_expert_io(C.Structure):
                 ("layers", C.POINTER(jn_expert_layer_grads))]
 
 
+class jn_adamw_tenant(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("n_tensors", C.c_int32), ("step", C.c_int64),
+                ("params", C.POINTER(C.c_void_p)), ("grads", C.POINTER(C.c_void_p)), ("m", C.POINTER(C.c_void_p)),
+                ("v", C.POINTER(C.c_void_p)), ("numel", C.POINTER(C.c_int64)), ("bf16_out", C.POINTER(C.c_void_p))]
+
+
 _lib = None
 
 
@@ -157,6 +165,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
                                                 P(C.c_size_t)]),
         "jn_tenant_experts_fwd_bwd": (C.c_int, [V, P(jn_packed), V, P(jn_expert), P(jn_expert_io), C.c_int32, V,
                                                 C.c_size_t]),
+        "jn_adamw_workspace_size": (C.c_int, [P(jn_adamw_tenant), C.c_int32, P(C.c_size_t)]),
+        "jn_tenant_adamw_step": (C.c_int, [V, P(jn_adamw_tenant), C.c_int32, V, C.c_size_t]),
         "jn_unpack": (C.c_int, [V, P(jn_packed), P(jn_request), C.c_int32, V, C.c_size_t, P(V)]),
     }
     for name, (res, args) in sig.items():

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libjoynexus.so")
 OBJDIR = os.path.join(HERE, "_build")
 
-SOURCES = ["jn_api.cpp", "k_pack.hip", "k_norm.hip", "k_gemm.hip", "k_attn.hip", "k_heads.hip", "k_expert.hip"]
+SOURCES = ["jn_api.cpp", "k_pack.hip", "k_norm.hip", "k_gemm.hip", "k_attn.hip", "k_heads.hip", "k_expert.hip", "k_optim.hip"]
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]

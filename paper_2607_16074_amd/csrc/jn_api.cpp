@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -1491,6 +1492,94 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     auto& op = rec.ops[i];
     JN_TRACED(c, rec.opcode[i], P.Na, d, 0, op(darena), "expert launch");
   }
+  return JN_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------ optimizer ---
+
+namespace {
+
+jn_status adamw_check(jn_ctx* c, const jn_adamw_tenant* t, int32_t G, int32_t* ntensors) {
+  if (!t || G < 1) return fail(c, JN_EINVAL, "null tenants or G < 1");
+  int64_t n = 0;
+  auto aligned = [](const void* q) { return q && ((uintptr_t)q) % 16 == 0; };
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_adamw_tenant& T = t[g];
+    if (T.n_tensors < 0) return fail(c, JN_EINVAL, "tenant %d: n_tensors < 0", g);
+    if (T.step < 1) return fail(c, JN_EINVAL, "tenant %d: step %lld < 1", g, (long long)T.step);
+    if (!(T.lr >= 0.f) || !(T.beta1 >= 0.f && T.beta1 < 1.f) || !(T.beta2 >= 0.f && T.beta2 < 1.f) ||
+        !(T.eps > 0.f) || !(T.weight_decay >= 0.f))
+      return fail(c, JN_EINVAL, "tenant %d: hyperparameters out of range", g);
+    if (T.n_tensors > 0 && (!T.params || !T.grads || !T.m || !T.v || !T.numel))
+      return fail(c, JN_EINVAL, "tenant %d: null table", g);
+    for (int32_t i = 0; i < T.n_tensors; ++i) {
+      if (T.numel[i] < 0) return fail(c, JN_EINVAL, "tenant %d tensor %d: numel < 0", g, i);
+      if (T.numel[i] == 0) continue;
+      if (!aligned(T.params[i]) || !aligned(T.grads[i]) || !aligned(T.m[i]) || !aligned(T.v[i]))
+        return fail(c, JN_EINVAL, "tenant %d tensor %d: null or unaligned pointer", g, i);
+      if (T.bf16_out && T.bf16_out[i] && ((uintptr_t)T.bf16_out[i]) % 8 != 0)
+        return fail(c, JN_EINVAL, "tenant %d tensor %d: bf16 copy not 8-byte aligned", g, i);
+      if ((T.numel[i] + kAdamwBlockElems - 1) / kAdamwBlockElems >= (1ll << 30))
+        return fail(c, JN_ESHAPE, "tenant %d tensor %d too large", g, i);
+    }
+    n += T.n_tensors;
+  }
+  if (n >= (1 << 24)) return fail(c, JN_ESHAPE, "too many tensors");
+  *ntensors = (int32_t)n;
+  return JN_OK;
+}
+
+size_t adamw_ws(int32_t n, int32_t G) {
+  return align_up(sizeof(AdamwTensor) * (size_t)std::max(n, 1), 256) + align_up(sizeof(AdamwTenant) * G, 256);
+}
+
+}  // namespace
+
+extern "C" {
+
+jn_status jn_adamw_workspace_size(const jn_adamw_tenant* t, int32_t G, size_t* bytes) {
+  if (!bytes) return JN_EINVAL;
+  int32_t n = 0;
+  jn_status st = adamw_check(nullptr, t, G, &n);
+  if (st != JN_OK) return st;
+  *bytes = adamw_ws(n, G);
+  return JN_OK;
+}
+
+jn_status jn_tenant_adamw_step(jn_ctx* c, const jn_adamw_tenant* t, int32_t G, void* ws, size_t ws_bytes) {
+  if (!c) return JN_EINVAL;
+  int32_t n = 0;
+  jn_status st = adamw_check(c, t, G, &n);
+  if (st != JN_OK) return st;
+  if (!ws || ((uintptr_t)ws) % 256 != 0) return fail(c, JN_EINVAL, "workspace null or not 256-byte aligned");
+  const size_t need = adamw_ws(n, G);
+  if (ws_bytes < need) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, need);
+  const size_t ten_off = align_up(sizeof(AdamwTensor) * (size_t)std::max(n, 1), 256);
+  std::vector<char> img(need, 0);
+  AdamwTensor* tt = reinterpret_cast<AdamwTensor*>(img.data());
+  AdamwTenant* th = reinterpret_cast<AdamwTenant*>(img.data() + ten_off);
+  int32_t k = 0;
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_adamw_tenant& T = t[g];
+    const double bc1 = 1.0 - std::pow((double)T.beta1, (double)T.step);
+    const double bc2 = 1.0 - std::pow((double)T.beta2, (double)T.step);
+    th[g] = AdamwTenant{(float)(1.0 - (double)T.lr * T.weight_decay), (float)(T.lr / bc1), (float)(1.0 / std::sqrt(bc2)),
+                        T.eps, T.beta1, T.beta2, 0.f, 0.f};
+    for (int32_t i = 0; i < T.n_tensors; ++i, ++k) {
+      tt[k] = AdamwTensor{T.params[i], T.grads[i], T.m[i], T.v[i],
+                          (uint16_t*)(T.bf16_out ? T.bf16_out[i] : nullptr), T.numel[i], g, 0};
+    }
+  }
+  const int32_t blocks = adamw_prepare(tt, n);
+  if (blocks == 0) return JN_OK;
+  st = stage_copy(c, ws, img.data(), need);
+  if (st != JN_OK) return st;
+  char* w = (char*)ws;
+  JN_TRACED(c, JN_OP_OPTIMIZER, n, G, 0,
+            launch_adamw(c->stream, (const AdamwTensor*)w, n, (const AdamwTenant*)(w + ten_off), blocks),
+            "adamw kernel");
   return JN_OK;
 }
 

@@ -208,4 +208,23 @@ struct XLossDesc {
 hipError_t launch_xloss(hipStream_t s, const XLossDesc* d, const int32_t* roff, int32_t G, const float* pred_pad,
                         int32_t ldp, float* dpred_pad);
 
+// ------------------------------------------------------------ optimizer ---
+
+struct AdamwTensor {
+  float* p;
+  const float* g;
+  float* m;
+  float* v;
+  uint16_t* b16;        // optional bf16 copy of the new parameters
+  int64_t numel;
+  int32_t tenant, block_start;
+};
+// per tenant: p = p * decay - step_size * m / (sqrt(v) * inv_sqrt_bc2 + eps)
+struct AdamwTenant {
+  float decay, step_size, inv_sqrt_bc2, eps, b1, b2, reserved0, reserved1;
+};
+constexpr int64_t kAdamwBlockElems = 4096;
+int32_t adamw_prepare(AdamwTensor* t, int32_t n);  // fills block_start, returns the block count
+hipError_t launch_adamw(hipStream_t s, const AdamwTensor* t, int32_t n, const AdamwTenant* ten, int32_t blocks);
+
 }  // namespace jnx

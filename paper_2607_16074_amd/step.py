@@ -20,10 +20,10 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from . import (EXPERT_LAYER_FIELDS, Backbone, Context, Expert, ExpertIO, Head, HeadIO, Request, Tenant,
-               jn_backbone_forward, jn_backbone_workspace_size, jn_experts_workspace_size, jn_heads_workspace_size,
-               jn_pack_group, jn_pack_plan, jn_pack_tenant_sizes, jn_tenant_experts_fwd_bwd, jn_tenant_heads_fwd_bwd,
-               jn_unpack)
+from . import (EXPERT_LAYER_FIELDS, AdamWTenant, Backbone, Context, Expert, ExpertIO, Head, HeadIO, Request, Tenant,
+               jn_adamw_workspace_size, jn_backbone_forward, jn_backbone_workspace_size, jn_experts_workspace_size,
+               jn_heads_workspace_size, jn_pack_group, jn_pack_plan, jn_pack_tenant_sizes, jn_tenant_adamw_step,
+               jn_tenant_experts_fwd_bwd, jn_tenant_heads_fwd_bwd, jn_unpack)
 
 
 def _dev_bf16(bits: np.ndarray, device):
@@ -162,6 +162,50 @@ class GroupStep:
         self.backbone()
         self.heads_fwd_bwd()
         self.unpack()
+
+
+class TenantOptimizer:
+    """Per-tenant AdamW over the tenants of one ``GroupStep``: after the
+    group's tenant stage, ``step()`` updates every tenant's own parameters
+    from its own gradients in one launch and advances only those tenants'
+    versions.  MLP heads are updated in place (fp32); an action expert keeps
+    fp32 master weights here and its bf16 weights receive the rounded update.
+    Moments start at zero."""
+
+    def __init__(self, group: "GroupStep", lr: float = 1e-4, betas=(0.9, 0.999), eps: float = 1e-8,
+                 weight_decay: float = 0.0):
+        import torch
+        self.group = group
+        self.hyper = dict(lr=lr, beta1=betas[0], beta2=betas[1], eps=eps, weight_decay=weight_decay)
+        self.versions = {g: 0 for g in group.tenants}
+        self.sets = []   # per tenant: (params, grads, bf16 copies or None)
+        for k, g in enumerate(group.tenants):
+            if group.use_experts:
+                e, io = group.experts[k], group.ios[k]
+                pairs = [(e.w_in, io.dw_in), (e.w_out, io.dw_out), (e.gf, io.dgf)]
+                for L, Lg in zip(e.layers, io.layers):
+                    pairs += [(L[n], Lg[n]) for n in EXPERT_LAYER_FIELDS]
+                masters = [w.float().contiguous() for w, _ in pairs]
+                self.sets.append((masters, [gr for _, gr in pairs], [w for w, _ in pairs]))
+            else:
+                h, io = group.heads[k], group.ios[k]
+                self.sets.append((list(h.W) + list(h.b), list(io.dW) + list(io.db), None))
+        self.m = [[torch.zeros_like(p) for p in ps] for ps, _, _ in self.sets]
+        self.v = [[torch.zeros_like(p) for p in ps] for ps, _, _ in self.sets]
+        self.ws = torch.empty(jn_adamw_workspace_size(self._tenants(1)), dtype=torch.uint8, device=group.tokens.device)
+
+    def _tenants(self, bump: int):
+        out = []
+        for k, g in enumerate(self.group.tenants):
+            ps, gs, b16 = self.sets[k]
+            out.append(AdamWTenant(ps, gs, self.m[k], self.v[k], self.versions[g] + bump, bf16_out=b16, **self.hyper))
+        return out
+
+    def step(self):
+        ten = self._tenants(1)
+        jn_tenant_adamw_step(self.group.ctx, ten, self.ws)
+        for g in self.group.tenants:
+            self.versions[g] += 1
 
 
 def isolated_runs(model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],

@@ -39,7 +39,7 @@ def test_struct_layout_matches_c(tmp_path, lib):
                "jn_backbone": _abi.jn_backbone, "jn_head": _abi.jn_head, "jn_head_io": _abi.jn_head_io,
                "jn_expert_layer": _abi.jn_expert_layer, "jn_expert": _abi.jn_expert,
                "jn_expert_layer_grads": _abi.jn_expert_layer_grads, "jn_expert_io": _abi.jn_expert_io,
-               "jn_trace_entry": _abi.jn_trace_entry}
+               "jn_trace_entry": _abi.jn_trace_entry, "jn_adamw_tenant": _abi.jn_adamw_tenant}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "joynexus.h"', "int main(void){"]
     for name, cls in structs.items():
         lines.append(f'printf("{name} %zu\\n", sizeof({name}));')
@@ -213,4 +213,22 @@ def test_experts_workspace_validation(lib):
     io_un._layers[0].w_up = io_un._layers[0].w_up + 4
     with pytest.raises(lib.JNError) as e:
         lib.jn_experts_workspace_size(p, ex, [io_un, ios[1]])
+    assert e.value.status == E.JN_EINVAL
+
+
+def test_adamw_validation(lib):
+    import torch
+    z = lambda n: torch.zeros(n, dtype=torch.float32)  # noqa: E731
+    good = lambda **kw: lib.AdamWTenant([z(8)], [z(8)], [z(8)], [z(8)], **{"step": 1, "lr": 1e-3, **kw})  # noqa: E731
+    assert lib.jn_adamw_workspace_size([good(), good(step=3)]) > 0
+    E = lib._abi
+    for kw in ({"step": 0}, {"beta1": 1.0}, {"beta2": -0.1}, {"eps": 0.0}, {"lr": -1.0}):
+        with pytest.raises(lib.JNError) as e:
+            lib.jn_adamw_workspace_size([good(**kw)])
+        assert e.value.status == E.JN_EINVAL, kw
+    # an unaligned parameter pointer
+    t = good()
+    t._p[0] = t._p[0] + 4
+    with pytest.raises(lib.JNError) as e:
+        lib.jn_adamw_workspace_size([t])
     assert e.value.status == E.JN_EINVAL
