@@ -12,7 +12,8 @@
 // operand layout of O^T += V^T P^T (a permutation of the 16-key contraction
 // index that is applied identically to both operands), so P never goes
 // through LDS.  K is staged row-major and V transposed in LDS, 64 keys per
-// step; statistics in fp32, P rounded to bf16 for the second MFMA.
+// step (V keys reordered so each P^T-matching operand is one 16-byte read);
+// statistics in fp32, P rounded to bf16 for the second MFMA.
 #include "jn_device.h"
 #include "jn_internal.h"
 
@@ -23,6 +24,15 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kQRows = 128;  // query rows per workgroup (4 waves x 32)
 constexpr int kKeys = 64;    // keys per step
+
+// Column of key k (0..63) in a transposed-V row: within each 16-key chunk the
+// keys a lane pairs with one P^T operand (chunk + hi*4 + 0..3 and
+// chunk + 8 + hi*4 + 0..3, hi = lane >> 5) are stored contiguously, so the
+// operand is one 16-byte read.  Adjacent even/odd keys stay adjacent.
+__device__ __forceinline__ int vt_pos(int k) {
+  const int within = k & 15, blk = within >> 3, sub = within & 7;
+  return (k & ~15) + (sub >> 2) * 8 + blk * 4 + (sub & 3);
+}
 
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(const uint16_t* __restrict__ qkv,
@@ -83,18 +93,21 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(const uint16_t* __rest
       *reinterpret_cast<uint4*>(&Ks[kr][c8]) =
           *reinterpret_cast<const uint4*>(Kg + (int64_t)(base + key) * ld + c8);
     }
-    // V transposed: a thread takes two adjacent keys of one 8-wide chunk and
-    // writes 8 packed key pairs
+    // V transposed, keys in the order the P^T operand uses (see vt_pos): a
+    // thread takes two adjacent keys of one 8-wide head-dim chunk and writes
+    // 8 packed key pairs; the 32 lanes of a half-wave cover the 32 key pairs
+    // of one chunk, so each row write hits 32 distinct banks
     for (int e = tid; e < (kKeys / 2) * (HD / 8); e += 256) {
-      const int kp = e / (HD / 8), c8 = (e % (HD / 8)) * 8;
+      const int kp = e % (kKeys / 2), c8 = (e / (kKeys / 2)) * 8;
       const int32_t k0 = min(kb + 2 * kp, L - 1), k1 = min(kb + 2 * kp + 1, L - 1);
       const uint4 a = *reinterpret_cast<const uint4*>(Vg + (int64_t)(base + k0) * ld + c8);
       const uint4 b = *reinterpret_cast<const uint4*>(Vg + (int64_t)(base + k1) * ld + c8);
       const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+      const int pos = vt_pos(2 * kp);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w][2 * kp]) = (aw[w] & 0xffffu) | (bw[w] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w + 1][2 * kp]) = (aw[w] >> 16) | (bw[w] & 0xffff0000u);
+        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w][pos]) = (aw[w] & 0xffffu) | (bw[w] << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w + 1][pos]) = (aw[w] >> 16) | (bw[w] & 0xffff0000u);
       }
     }
     __syncthreads();
@@ -154,10 +167,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(const uint16_t* __rest
       const uint16_t* vrow = &Vt[t * 32 + (lane & 31)][0];
 #pragma unroll
       for (int kc = 0; kc < 4; ++kc) {
-        const uint2 lo = *reinterpret_cast<const uint2*>(vrow + kc * 16 + hi4);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + kc * 16 + 8 + hi4);
-        const uint4 w = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+        // keys kc*16 + hi4 + 0..3 and kc*16 + 8 + hi4 + 0..3, contiguous in vt_pos order
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vrow + kc * 16 + 2 * hi4);
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kc], o[t], 0, 0, 0);
       }
     }
