@@ -128,6 +128,36 @@ def cpu_oracle_baseline(wl, budget_s=25.0):
             "seconds": dt, "host_cpus": os.cpu_count()}
 
 
+def local_batch_sweep(model, reqs, targets, steps, warmup, tenants_list=(2, 4, 6, 8), batches=(1, 2, 4, 8)):
+    """Grouped vs isolated step time over tenants x local batch on one model:
+    the first G tenants each submit their first n samples."""
+    import torch
+    from paper_2607_16074_amd import Context, Request
+    from paper_2607_16074_amd import step as jstep
+    ctx = Context()
+    rows = []
+    for G in tenants_list:
+        for n in batches:
+            sub = [Request(r.tenant, r.embeds[:n], r.lengths[:n]) for r in reqs if r.tenant < G]
+            tg = {g: targets[g][:n] for g in range(G)}
+            grouped = jstep.GroupStep(model, sub, tg, list(range(G)), 1, ctx)
+            iso = jstep.isolated_runs(model, sub, tg, list(range(G)), 1, ctx)
+            torch.cuda.synchronize()
+            tg_s, _ = time_steps(steps, grouped.run, ctx, warmup)
+
+            def run_iso():
+                for st in iso:
+                    st.run()
+            ti_s, _ = time_steps(steps, run_iso, ctx, warmup)
+            rows.append({"tenants": G, "local_batch": n, "grouped_ms": tg_s * 1e3, "isolated_ms": ti_s * 1e3,
+                         "speedup": ti_s / tg_s})
+            log(f"sweep G={G} n={n}: grouped {tg_s * 1e3:.2f} ms, isolated {ti_s * 1e3:.2f} ms, "
+                f"{ti_s / tg_s:.2f}x")
+            del grouped, iso
+            torch.cuda.synchronize()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -139,6 +169,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-optimizer", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-kernel time shares to stderr")
+    ap.add_argument("--sweep", action="store_true",
+                    help="grouped vs isolated over tenants {2,4,6,8} x local batch {1,2,4,8} (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a 512 MiB device copy first (reference dispatch for PMC byte counters)")
     args = ap.parse_args()
@@ -159,6 +191,11 @@ def main():
     spec = wl.spec
     log(f"workload cfg{args.config} drawn in {time.perf_counter() - t0:.1f}s: {spec.name}")
     model, reqs, targets, noisy = jstep.from_workload(wl, "cuda", with_noisy=True)
+    if args.sweep:
+        rows = local_batch_sweep(model, reqs, targets, args.steps, args.warmup)
+        print(json.dumps({"sweep": "grouped vs isolated step time, tenants x local batch",
+                          "config": f"config {args.config}: {spec.name}", "rows": rows}), flush=True)
+        return
     G = spec.G
     experts = spec.tenants[0].expert is not None
     grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align, noisy=noisy)
