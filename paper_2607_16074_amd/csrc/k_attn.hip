@@ -4,77 +4,153 @@
 // crosses a sample (hence a tenant) boundary and alignment rows are neither
 // keys nor queries (their output rows are written as zero).
 //
-// Grid (query tile, sample, head); a workgroup = 4 wavefronts x 32 query rows.
-// The kernel computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane
-// holds one query row's scores for 16 of every 32 keys: the online-softmax
-// row max / row sum need only the lane's registers plus one exchange with the
-// partner lane (lane ^ 32).  The probabilities then already sit in the
-// operand layout of O^T += V^T P^T (a permutation of the 16-key contraction
-// index that is applied identically to both operands), so P never goes
-// through LDS.  K is staged row-major and V transposed in LDS, 64 keys per
-// step (V keys reordered so each P^T-matching operand is one 16-byte read);
-// statistics in fp32, P rounded to bf16 for the second MFMA.
+// Work item = (sample, head, 128-query tile); a workgroup = 4 wavefronts x 32
+// query rows.  (sample, head) groups are dealt round-robin to the 8 XCDs
+// (hardware places workgroup b on XCD b % 8) with all query tiles of a group
+// on one XCD: they share its L2 for the group's keys and values, and a run of
+// long samples (one tenant's) is spread over every XCD.
+//
+// Per step of KB keys, the K and V tiles ([KB][HD] bf16, row-major) are
+// moved global -> LDS by direct DMA (global_load_lds_dwordx4), double
+// buffered: the DMA of step j+1 runs under the compute of step j, one
+// workgroup barrier per step.  Each LDS row is a permutation of its 16-byte
+// chunks (chunk c stored at c ^ swz(row)), chosen per head width so that
+// both reads below touch every LDS bank once per 256 bytes.
+//
+// Scores: S^T = K Q^T with v_mfma_f32_32x32x16_bf16, K the "A" operand
+// (16-byte LDS reads), Q held in registers as "B", so each lane owns one
+// query row's scores for 16 of every 32 keys and the online-softmax row
+// max / sum need only its registers plus one exchange with lane ^ 32.  The
+// probabilities then sit in the operand layout of O^T += V^T P^T (keys
+// contracted in the permuted order the score layout gives), so P stays in
+// registers.  The V^T operand is read from the row-major V tile with
+// ds_read_b64_tr_b16: in each 16-lane group, lane j addresses 4 elements of
+// key row k0 + j/4 at column n0 + 4(j%4) and receives, transposed, the
+// column n0 + (lane % 16) of rows k0..k0+3 -- 4 consecutive keys of one
+// head-dim row, as the MFMA wants.  Statistics in fp32, P rounded to bf16.
 #include "jn_device.h"
 #include "jn_internal.h"
 
 namespace jnx {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kQRows = 128;  // query rows per workgroup (4 waves x 32)
-constexpr int kKeys = 64;    // keys per step
+#define JN_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
+#define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-// Column of key k (0..63) in a transposed-V row: within each 16-key chunk the
-// keys a lane pairs with one P^T operand (chunk + hi*4 + 0..3 and
-// chunk + 8 + hi*4 + 0..3, hi = lane >> 5) are stored contiguously, so the
-// operand is one 16-byte read.  Adjacent even/odd keys stay adjacent.
-__device__ __forceinline__ int vt_pos(int k) {
-  const int within = k & 15, blk = within >> 3, sub = within & 7;
-  return (k & ~15) + (sub >> 2) * 8 + blk * 4 + (sub & 3);
+constexpr int kQRows = 128;  // query rows per workgroup (4 waves x 32)
+constexpr float kRescale = 8.0f;  // log2 headroom before the running max is moved
+constexpr int kKeys = 64;    // keys per step (64 measured best for head widths 64 and 256)
+
+// Chunk permutation of LDS row r (HD/8 chunks of 16 bytes per row).  K
+// fragment reads touch 16 consecutive rows (one chunk each) per 16 lanes;
+// transposed V reads touch rows k0..k0+3 (k0 % 4 == 0) x 4 adjacent chunks
+// per 16 lanes.  Both cover 16 distinct 16-byte bank slots with:
+//   HD 32  (4 rows per 256-byte bank row): (r >> 2) & 3
+//   HD 64  (2 rows per bank row):          bit-reversed ((r >> 1) & 7)
+//   HD 128/256:                            4 * (r & 3) + ((r >> 2) & 3)
+template <int HD>
+__device__ __forceinline__ int attn_swz(int r) {
+  if constexpr (HD == 32) {
+    return (r >> 2) & 3;
+  } else if constexpr (HD == 64) {
+    const int x = (r >> 1) & 7;
+    return ((x & 1) << 2) | (x & 2) | (x >> 2);
+  } else {
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  }
 }
 
-template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(const uint16_t* __restrict__ qkv,
-                                                          uint16_t* __restrict__ out,
-                                                          const int32_t* __restrict__ seqlens,
-                                                          const int32_t* __restrict__ cu_seqlens, int32_t d,
-                                                          float scale_log2) {
-  constexpr int KLD = HD + 8;     // K row pitch in LDS (elements)
-  constexpr int VLD = kKeys + 8;  // V^T row pitch in LDS (elements)
-  constexpr int NQC = HD / 16;    // 16-wide head-dim chunks
-  constexpr int NOT = HD / 32;    // 32-row tiles of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeys][KLD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD][VLD];
+template <int N>
+__device__ __forceinline__ void attn_wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(N | (7 << 4) | (15 << 8) | (0 << 14));
+}
 
-  const int32_t i = blockIdx.y, h = blockIdx.z;
+template <int HD, int KB>
+__global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd_kernel(
+    const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out, const int32_t* __restrict__ seqlens,
+    const int32_t* __restrict__ cu_seqlens, int32_t d, int32_t n_heads, int32_t qtiles, int32_t total,
+    float scale_log2) {
+  constexpr int CPR = HD / 8;            // 16-byte chunks per row
+  constexpr int TILE = KB * HD;          // elements of one K (or V) tile
+  constexpr int NDMA = 2 * TILE / 512;   // 1 KB DMA instructions per stage (K tile, then V tile)
+  constexpr int DPW = NDMA / 4;          // per wavefront
+  constexpr int RPI = 512 / HD;          // rows per DMA instruction
+  constexpr int NQC = HD / 16;           // 16-wide head-dim chunks (score contraction)
+  constexpr int NOT = HD / 32;           // 32-row tiles of O^T
+  constexpr int NKT = KB / 32;           // 32-key score tiles per step
+  constexpr int NKC = KB / 16;           // 16-key P^T operands per step
+  static_assert(NDMA % 4 == 0 && KB % 32 == 0, "tile shape");
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2 * TILE];
+
+  // XCD-aware work mapping: (sample, head) group g goes to XCD g % 8, and
+  // its query tiles to consecutive slots of that XCD (block b runs on XCD
+  // b % 8, slot b / 8).  Groups interleave across XCDs, so samples of very
+  // different lengths spread evenly, while each group's keys and values are
+  // read by one XCD only.
+  const int32_t b = blockIdx.x;
+  const int32_t slot = b >> 3;
+  const int32_t ih = (slot / qtiles) * 8 + (b & 7);
+  const int32_t qt = slot % qtiles;
+  if (ih >= total) return;
+  const int32_t h = ih % n_heads, i = ih / n_heads;
   const int32_t L = seqlens[i];
   const int32_t base = cu_seqlens[i];
-  const int32_t q0 = blockIdx.x * kQRows;
-  const int64_t ld = 3 * (int64_t)d;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  if (blockIdx.x == 0) {  // alignment rows of this sample: zero output
+  if (qt == 0) {  // alignment rows of this sample: zero output
     const int32_t pad = cu_seqlens[i + 1] - base - L;
     for (int32_t e = tid; e < pad * (HD / 8); e += 256) {
       const int32_t row = base + L + e / (HD / 8);
       *reinterpret_cast<uint4*>(out + (int64_t)row * d + h * HD + (e % (HD / 8)) * 8) = make_uint4(0, 0, 0, 0);
     }
   }
+  const int32_t q0 = qt * kQRows;
   if (q0 >= L) return;
 
+  const int64_t ld = 3 * (int64_t)d;
   const uint16_t* Qg = qkv + h * HD;
   const uint16_t* Kg = qkv + d + h * HD;
   const uint16_t* Vg = qkv + 2 * d + h * HD;
 
+  // this wave's DMA instructions u = wave*DPW + k fill 1 KB each; lane ->
+  // row (v*RPI + lane / CPR) of the K or V tile, physical chunk lane % CPR,
+  // which holds logical chunk (lane % CPR) ^ swz(row)
+  auto issue_stage = [&](int32_t kb, int stage) {
+#pragma unroll
+    for (int k = 0; k < DPW; ++k) {
+      const int u = wave * DPW + k;
+      const bool isv = u >= NDMA / 2;
+      const int v = isv ? u - NDMA / 2 : u;
+      const int r = v * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ attn_swz<HD>(r);
+      const int32_t key = min(kb + r, L - 1);
+      const uint16_t* src = (isv ? Vg : Kg) + (int64_t)(base + key) * ld + c * 8;
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src), JN_LPTR(&lds[stage][u * 512]), 16, 0, 0);
+    }
+  };
+
   const int32_t qw = q0 + wave * 32;  // this wave's first query row
   const bool active = qw < L;
   const int32_t qrow = min(qw + (lane & 31), L - 1);
-  const int fk = (lane >> 5) * 8;
+  const int half = lane >> 5;
   bf16x8 qf[NQC];
 #pragma unroll
   for (int c = 0; c < NQC; ++c)
-    qf[c] = *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(base + qrow) * ld + c * 16 + fk);
+    qf[c] = *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(base + qrow) * ld + c * 16 + half * 8);
+
+  // per-lane LDS offsets: K fragment rows kt*32 + lane%32 (swizzle period 16)
+  const int krow = lane & 31;
+  const int kswz = attn_swz<HD>(krow);
+  // transposed V reads: 16-lane group gq = lane / 16, j = lane % 16
+  const int j16 = lane & 15;
+  const int vrow0 = 4 * half + (j16 >> 2);                           // + kc*16 (+8)
+  const int vcol = ((lane >> 4) & 1) * 16 + 4 * (j16 & 3);           // + t*32
+  const int vswz0 = attn_swz<HD>(vrow0), vswz1 = attn_swz<HD>(vrow0 + 8);
 
   f32x16 o[NOT];
 #pragma unroll
@@ -82,93 +158,92 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(const uint16_t* __rest
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[t][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  const int hi4 = (lane >> 5) * 4;
+  const int hi4 = half * 4;
 
-  for (int32_t kb = 0; kb < L; kb += kKeys) {
-    __syncthreads();  // previous step's readers are done with Ks / Vt
-    // K: 64 rows x HD, 16-byte chunks
-    for (int e = tid; e < kKeys * (HD / 8); e += 256) {
-      const int kr = e / (HD / 8), c8 = (e % (HD / 8)) * 8;
-      const int32_t key = min(kb + kr, L - 1);
-      *reinterpret_cast<uint4*>(&Ks[kr][c8]) =
-          *reinterpret_cast<const uint4*>(Kg + (int64_t)(base + key) * ld + c8);
-    }
-    // V transposed, keys in the order the P^T operand uses (see vt_pos): a
-    // thread takes two adjacent keys of one 8-wide head-dim chunk and writes
-    // 8 packed key pairs; the 32 lanes of a half-wave cover the 32 key pairs
-    // of one chunk, so each row write hits 32 distinct banks
-    for (int e = tid; e < (kKeys / 2) * (HD / 8); e += 256) {
-      const int kp = e % (kKeys / 2), c8 = (e / (kKeys / 2)) * 8;
-      const int32_t k0 = min(kb + 2 * kp, L - 1), k1 = min(kb + 2 * kp + 1, L - 1);
-      const uint4 a = *reinterpret_cast<const uint4*>(Vg + (int64_t)(base + k0) * ld + c8);
-      const uint4 b = *reinterpret_cast<const uint4*>(Vg + (int64_t)(base + k1) * ld + c8);
-      const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
-      const int pos = vt_pos(2 * kp);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w][pos]) = (aw[w] & 0xffffu) | (bw[w] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[c8 + 2 * w + 1][pos]) = (aw[w] >> 16) | (bw[w] & 0xffff0000u);
-      }
-    }
-    __syncthreads();
+  issue_stage(0, 0);
+  const int32_t nsteps = (L + KB - 1) / KB;
+  for (int32_t jstep = 0; jstep < nsteps; ++jstep) {
+    const int32_t kb = jstep * KB;
+    attn_wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();  // step j's tiles landed; step j-1's buffer is free
+    if (jstep + 1 < nsteps) issue_stage(kb + KB, (jstep + 1) & 1);
     if (!active) continue;
+    const uint16_t* Ks = &lds[jstep & 1][0];
+    const uint16_t* Vs = &lds[jstep & 1][TILE];
 
-    // S^T for two 32-key tiles
-    f32x16 s[2];
+    // S^T for NKT 32-key tiles
+    f32x16 s[NKT];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
+    for (int kt = 0; kt < NKT; ++kt) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
 #pragma unroll
       for (int c = 0; c < NQC; ++c) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[kt * 32 + (lane & 31)][c * 16 + fk]);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + (kt * 32 + krow) * HD + (((2 * c + half) ^ kswz) * 8));
         s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], s[kt], 0, 0, 0);
       }
     }
-    // scale, mask keys past the sample, running max
+    // Online softmax in the log2 domain (scores scaled by log2(e)/sqrt(hd)).
+    // The running max m only moves when some query of the wave gains more
+    // than kRescale (2^8 headroom for p = 2^(s - m) in fp32 and bf16); O and
+    // the running sum l always share the same m, so the final O / l is exact
+    // whichever m was used.  Keys past the sample are masked in the last step
+    // only (wave-uniform branch).
     float mloc = -INFINITY;
+    if (kb + KB > L) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int32_t key = kb + kt * 32 + (r >> 2) * 8 + hi4 + (r & 3);
-        const float v = key < L ? s[kt][r] * scale_log2 : -INFINITY;
-        s[kt][r] = v;
-        mloc = fmaxf(mloc, v);
-      }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = exp2f(m_run - m_new);
+        for (int r = 0; r < 16; ++r) {
+          const int32_t key = kb + kt * 32 + (r >> 2) * 8 + hi4 + (r & 3);
+          if (key >= L) s[kt][r] = -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[kt][r]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
+    if (__any(mloc > m_run + kRescale)) {
+      const float m_new = fmaxf(m_run, mloc);
+      const float alpha = exp2f(m_run - m_new);
+      l_run *= alpha;
+      m_run = m_new;
+#pragma unroll
+      for (int t = 0; t < NOT; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+    }
     float lsum = 0.f;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kt][r] - m_new);
+        const float p = exp2f(fmaf(s[kt][r], scale_log2, -m_run));
         s[kt][r] = p;
         lsum += p;
       }
     lsum += __shfl_xor(lsum, 32, 64);
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < NOT; ++t)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+    l_run += lsum;
 
-    // P^T operands: 16-key chunk kc holds registers 8*(kc&1) .. +7 of tile kc>>1
-    bf16x8 pf[4];
+    // P^T operands: 16-key chunk kc holds registers 8*(kc&1) .. +7 of tile kc>>1,
+    // i.e. keys kc*16 + 4*half + 0..3 and kc*16 + 8 + 4*half + 0..3
+    bf16x8 pf[NKC];
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
+    for (int kc = 0; kc < NKC; ++kc)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[kc][e] = (__bf16)s[kc >> 1][(kc & 1) * 8 + e];
 #pragma unroll
     for (int t = 0; t < NOT; ++t) {
-      const uint16_t* vrow = &Vt[t * 32 + (lane & 31)][0];
+      const int col = t * 32 + vcol;
 #pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
-        // keys kc*16 + hi4 + 0..3 and kc*16 + 8 + hi4 + 0..3, contiguous in vt_pos order
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vrow + kc * 16 + 2 * hi4);
+      for (int kc = 0; kc < NKC; ++kc) {
+        const int r0 = kc * 16 + vrow0;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4*)(Vs + r0 * HD + (((col >> 3) ^ vswz0) * 8) + (col & 7)));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4*)(Vs + (r0 + 8) * HD + (((col >> 3) ^ vswz1) * 8) + (col & 7)));
+        const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kc], o[t], 0, 0, 0);
       }
     }
@@ -195,15 +270,20 @@ hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int
                             int32_t align) {
   (void)align;
   const int hd = d / n_heads;
-  dim3 grid((max_seqlen + kQRows - 1) / kQRows, N, n_heads);
+  const int32_t qtiles = (max_seqlen + kQRows - 1) / kQRows;
+  const int64_t total = (int64_t)N * n_heads;  // (sample, head) groups
+  const int64_t blocks = (total + 7) / 8 * 8 * qtiles;
+  if (total <= 0 || blocks > (1LL << 30)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   auto Q = reinterpret_cast<const uint16_t*>(qkv);
   auto O = reinterpret_cast<uint16_t*>(out);
+  const int32_t tot = (int32_t)total;
   switch (hd) {
-    case 32: attn_fwd_kernel<32><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, scale_log2); break;
-    case 64: attn_fwd_kernel<64><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, scale_log2); break;
-    case 128: attn_fwd_kernel<128><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, scale_log2); break;
-    case 256: attn_fwd_kernel<256><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, scale_log2); break;
+    case 32: attn_fwd_kernel<32, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
+    case 64: attn_fwd_kernel<64, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
+    case 128: attn_fwd_kernel<128, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
+    case 256: attn_fwd_kernel<256, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -295,6 +295,167 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_grouped_kernel(const G
   gemm_tile<BN, BM, WGN, WGM, EPI>(g, b - g.tile_start, lds);
 }
 
+
+// Ping-pong variant of the 256x256 tile (8 wavefronts), used for the plain
+// bf16 and fp32-residual epilogues.  Waves w and w+4 share a SIMD; group 0
+// (waves 0-3) and group 1 (waves 4-7) alternate between a memory phase (all
+// 24 fragments of one K=64 slab from LDS, plus their share of a later slab's
+// DMA) and a compute phase (the slab's 32 MFMAs, which only read registers),
+// one workgroup barrier per phase, group 1 one phase behind group 0.  Slab
+// kt+1 is fetched by group 0 during its memory phase of slab kt and by group
+// 1 during its compute phase of slab kt-1; every wave waits for its own DMA
+// before the barrier that precedes the first read of that slab.  Per output
+// element the MFMA sequence (K order, operand lane layout) equals the
+// non-ping-pong kernel's, so both produce identical bits.  Measured against
+// the interleaved loop: +9.5% on the K=16384 residual projection, +4% on the
+// K=2048 one, equal or slightly better elsewhere; the GeGLU projection is 4%
+// slower with it and keeps the interleaved loop.
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs g) {
+  constexpr int BN = 256, BM = 256, WGN = 2, WGM = 4;
+  constexpr int NW = WGN * WGM;
+  constexpr int WN = BN / WGN, WM = BM / WGM;
+  constexpr int TN = WN / 32, TM = WM / 32;
+  constexpr int ROWS = BN + BM;
+  constexpr int NI = ROWS / (8 * NW);
+  constexpr int STAGE = ROWS * kBK;
+  static_assert(EPI == EPI_BF16 || EPI == EPI_RESID_F32, "ping-pong epilogues");
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * ROWS * kBK];
+  const uint16_t* __restrict__ X = g.X;
+  const uint16_t* __restrict__ W = g.W;
+  void* __restrict__ C = g.C;
+  const int64_t ldx = g.ldx, ldw = g.ldw, ldc = g.ldc;
+  const int32_t M = g.M, N = g.N, K = g.K, tiles_n = g.tiles_n, tiles_m = g.tiles_m;
+  const int32_t pid = blockIdx.x;
+
+  const int32_t per_group = kGroupM * tiles_n;
+  const int32_t group = pid / per_group;
+  const int32_t first_m = group * kGroupM;
+  const int32_t gsize = min(tiles_m - first_m, kGroupM);
+  const int32_t tm = first_m + (pid % per_group) % gsize;
+  const int32_t tn = (pid % per_group) / gsize;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wn = wave / WGM, wm = wave % WGM;
+  const int grp = wave >> 2;
+
+  const uint16_t* src[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int row = 8 * (wave * NI + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ lds_swz(row);
+    if (row < BN)
+      src[i] = W + (int64_t)min(tn * BN + row, N - 1) * ldw + chunk * 8;
+    else
+      src[i] = X + (int64_t)min(tm * BM + row - BN, M - 1) * ldx + chunk * 8;
+  }
+  uint16_t* const dst0 = lds + wave * NI * 512;
+
+  f32x16 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int KT = K / kBK;
+  const int sw = lds_swz(lane & 31), half = lane >> 5;
+  const int wrow = wn * WN + (lane & 31), xrow = BN + wm * WM + (lane & 31);
+
+  // slab 0 from every wave; group 1 also issues its share of slab 1 and then
+  // waits one extra barrier, which puts it one phase behind group 0
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+    __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(dst0 + i * 512), 16, 0, 0);
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  if (grp == 1) {
+    if (KT > 1) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(dst0 + STAGE + i * 512), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_barrier();
+  }
+
+  bf16x8 fw[4][TN], fx[4][TM];
+  for (int kt = 0; kt < KT; ++kt) {
+    const uint16_t* cur = lds + (kt & 1) * STAGE;
+    // ---- memory phase: slab kt's fragments (+ group 0's share of slab kt+1)
+    __builtin_amdgcn_sched_barrier(0);
+    if (grp == 0 && kt + 1 < KT) {
+      uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + 1) * kBK), JN_LPTR(fdst + i * 512), 16, 0, 0);
+    }
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+      const int pos = (2 * step + half) ^ sw;
+      gemm_frags<TN>(fw[step], cur, wrow, pos);
+      gemm_frags<TM>(fx[step], cur, xrow, pos);
+    }
+    wait_lgkmcnt<0>();
+    if (grp == 1) wait_vmcnt<0>();  // group 1's share of slab kt+1 (issued a phase earlier)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- compute phase: 32 MFMAs from registers (+ group 1's share of slab kt+2)
+    const bool fill = grp == 1 && kt + 2 < KT;
+    uint16_t* const gdst = dst0 + (kt & 1) * STAGE;
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+#pragma unroll
+      for (int q = 0; q < TN * TM; ++q) {
+        const int i = q / TM, j = q % TM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[step][i], fx[step][j], acc[i][j], 0, 0, 0);
+        const int d = step * TN * TM + q;
+        if ((d & 3) == 3 && fill)
+          __builtin_amdgcn_global_load_lds(JN_GPTR(src[d >> 2] + (kt + 2) * kBK), JN_LPTR(gdst + (d >> 2) * 512),
+                                           16, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (grp == 0) wait_vmcnt<0>();  // group 0's share of slab kt+1
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (grp == 0) __builtin_amdgcn_s_barrier();  // equal barrier counts in both groups
+
+  const int hi4 = (lane >> 5) * 4;
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int32_t m = tm * BM + wm * WM + j * 32 + (lane & 31);
+    if (m >= M) continue;
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int32_t n = tn * BN + wn * WN + i * 32 + rr * 8 + hi4;
+        if (n >= N) continue;
+        float a[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[e] = acc[i][j][rr * 4 + e];
+        if constexpr (EPI == EPI_RESID_F32) {
+          float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
+          float4 o = *p;
+          o.x += a[0];
+          o.y += a[1];
+          o.z += a[2];
+          o.w += a[3];
+          *p = o;
+        } else {
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+              make_uint2(pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]));
+        }
+      }
+    }
+  }
+}
+
 template <int BN, int BM, int WGN, int WGM>
 static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g) {
   const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
@@ -374,7 +535,18 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
   g.K = K;
   const int t = tile_hint > 0 ? tile_hint - 1 : gemm_pick_tile(epi, M, N);
   switch (t) {
-    case 0: return launch_tile<256, 256, 2, 4>(s, epi, g);
+    case 0:
+      if (epi == EPI_BF16 || epi == EPI_RESID_F32) {
+        g.tiles_m = (g.M + 255) / 256;
+        g.tiles_n = (g.N + 255) / 256;
+        g.tile_start = 0;
+        if (epi == EPI_BF16)
+          gemm_pp_kernel<EPI_BF16><<<dim3(g.tiles_m * g.tiles_n), dim3(512), 0, s>>>(g);
+        else
+          gemm_pp_kernel<EPI_RESID_F32><<<dim3(g.tiles_m * g.tiles_n), dim3(512), 0, s>>>(g);
+        return hipGetLastError();
+      }
+      return launch_tile<256, 256, 2, 4>(s, epi, g);
     case 1: return launch_tile<256, 128, 4, 2>(s, epi, g);
     default: return launch_tile<128, 128, 2, 2>(s, epi, g);
   }
