@@ -158,6 +158,52 @@ def local_batch_sweep(model, reqs, targets, steps, warmup, tenants_list=(2, 4, 6
     return rows
 
 
+def infer_latency(model, reqs, steps, warmup, tenants_list=(1, 2, 4, 8), per_tenant=(1, 4)):
+    """Decode-only step latency (launch to completion, host clock) of a group
+    of G tenants x n samples: eager launch vs replay of the captured HIP
+    graph, and the same requests as G single-tenant steps (each replayed)."""
+    import torch
+    from paper_2607_16074_amd import Request
+    from paper_2607_16074_amd import step as jstep
+
+    def lat(fn, sync):
+        for _ in range(warmup):
+            fn()
+        sync()
+        ts = []
+        for _ in range(steps):
+            t0 = time.perf_counter()
+            fn()
+            sync()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts)) * 1e3
+
+    rows = []
+    for G in tenants_list:
+        for n in per_tenant:
+            sub = [Request(r.tenant, r.embeds[:n], r.lengths[:n]) for r in reqs if r.tenant < G]
+            grp = jstep.InferStep(model, sub, list(range(G)))
+            eager = lat(grp.launch, grp.synchronize)
+            grp.capture()
+            graph = lat(grp.replay, grp.synchronize)
+            iso = []
+            for g in range(G):
+                st = jstep.InferStep(model, [q for q in sub if q.tenant == g], [g], stream=grp.stream)
+                st.capture()
+                iso.append(st)
+
+            def run_iso():
+                for st in iso:
+                    st.replay()
+            iso_ms = lat(run_iso, grp.synchronize)
+            rows.append({"tenants": G, "samples_per_tenant": n, "eager_ms": eager, "graph_ms": graph,
+                         "isolated_graph_ms": iso_ms, "speedup_vs_isolated": iso_ms / graph})
+            log(f"infer G={G} n={n}: eager {eager:.2f} ms, graph {graph:.2f} ms, isolated (graphs) {iso_ms:.2f} ms")
+            del grp, iso
+            torch.cuda.synchronize()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -171,6 +217,8 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="print per-kernel time shares to stderr")
     ap.add_argument("--sweep", action="store_true",
                     help="grouped vs isolated over tenants {2,4,6,8} x local batch {1,2,4,8} (one JSON line)")
+    ap.add_argument("--infer", action="store_true",
+                    help="decode-only step latency of small groups: eager vs HIP-graph replay vs isolated (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a 512 MiB device copy first (reference dispatch for PMC byte counters)")
     args = ap.parse_args()
@@ -191,6 +239,11 @@ def main():
     spec = wl.spec
     log(f"workload cfg{args.config} drawn in {time.perf_counter() - t0:.1f}s: {spec.name}")
     model, reqs, targets, noisy = jstep.from_workload(wl, "cuda", with_noisy=True)
+    if args.infer:
+        rows = infer_latency(model, reqs, args.steps, args.warmup)
+        print(json.dumps({"infer_latency": "decode-only step, launch to completion (host clock, median)",
+                          "config": f"config {args.config}: {spec.name}", "rows": rows}), flush=True)
+        return
     if args.sweep:
         rows = local_batch_sweep(model, reqs, targets, args.steps, args.warmup)
         print(json.dumps({"sweep": "grouped vs isolated step time, tenants x local batch",

@@ -21,6 +21,10 @@
  *   jn_tenant_adamw_step   per-tenant AdamW update of the tenants' parameters
  *   jn_unpack              scatter packed rows back to the requests' own
  *                          padded buffers (the "split" by slices, App. A.3)
+ *   jn_collector_*         the inference queue's FIFO-compatible-prefix
+ *                          batching under a maximum batch size and a timeout
+ *   jn_infer_plan_*        a resident decode-only step over one physical
+ *                          batch, launchable eagerly or as a HIP graph
  *
  * Conventions
  *   - bf16 is the IEEE-754 binary32 upper half (bfloat16), stored as 2 bytes.
@@ -367,6 +371,74 @@ jn_status jn_tenant_adamw_step(jn_ctx* ctx, const jn_adamw_tenant* t, int32_t G,
  * device buffers [n_r][max_len_r][row_bytes]; row_bytes a multiple of 4. */
 jn_status jn_unpack(jn_ctx* ctx, const jn_packed* p, const jn_request* req, int32_t R,
                     const void* rows, size_t row_bytes, void* const* req_out);
+
+
+/* ----------------------------------------- inference-side group batching --- */
+
+/* Request collector of the inference queue (App. A.3 "Inference Queue
+ * Composition": requests are examined in arrival order and the largest FIFO
+ * prefix that is compatible at the shared frozen-prefix boundary is formed,
+ * bounded by the batching timeout and the maximum batch size).  Host only;
+ * no device work.  Times are caller-supplied microseconds (any monotonic
+ * clock), so the collector is deterministic.
+ *
+ * The prefix starts at the oldest queued request and takes whole requests in
+ * arrival order while (a) each has the oldest request's prefix signature and
+ * feature width -- compatibility is decided by the interface, not by tenant
+ * identity -- and (b) the total sample count stays <= max_batch_samples (the
+ * oldest request is always taken, even if larger).  It is released when it
+ * can no longer grow (it holds max_batch_samples samples, or the next queued
+ * request is incompatible or would overflow it) or when the oldest request
+ * has waited timeout_us.  An incompatible request is never skipped: it heads
+ * a later batch. */
+typedef struct jn_collector jn_collector;
+/* max_batch_samples >= 1, timeout_us >= 0, else JN_EINVAL. */
+jn_status jn_collector_create(jn_collector** out, int32_t max_batch_samples, int64_t timeout_us);
+void jn_collector_destroy(jn_collector* c);
+/* Queue one request (metadata only).  arrival_us must not precede the last
+ * queued request's (JN_EINVAL); n_samples, d_model >= 1. */
+jn_status jn_collector_submit(jn_collector* c, int64_t request_id, uint64_t prefix_sig, int32_t d_model,
+                              int32_t n_samples, int64_t arrival_us);
+/* If a batch is ready at now_us, move its request ids (arrival order) to
+ * ids[0 .. *n) and remove them from the queue; otherwise *n = 0.  JN_ENOSPACE
+ * (queue untouched) if the ready batch has more than `cap` requests. */
+jn_status jn_collector_poll(jn_collector* c, int64_t now_us, int64_t* ids, int32_t cap, int32_t* n);
+/* Queued request count, and the time at which the current prefix becomes
+ * ready (-1 if the queue is empty; the oldest arrival if it is ready already). */
+jn_status jn_collector_status(const jn_collector* c, int32_t* pending, int64_t* deadline_us);
+
+/* Resident inference plan for one physical batch: canonicalize + pad, shared
+ * encode, split, per-tenant decode (App. A.3), with MLP heads run forward
+ * only.  Creation validates everything, carves `ws` (caller-owned device
+ * memory, jn_infer_workspace_size bytes, 256-byte aligned) and uploads every
+ * index map and head descriptor once.  A launch then enqueues kernels only --
+ * pack, backbone, pool, head forward -- reading the requests' `embeds`
+ * buffers as they are at that time and writing actions[g] (device fp32
+ * [n_g][action_dim * chunk], rows in tenant g's arrival order).  Because a
+ * launch allocates, copies and synchronizes nothing, it can be recorded into
+ * a HIP graph (jn_infer_plan_capture) and replayed with new observations
+ * written into the same `embeds` buffers.  The plan keeps the device
+ * pointers it was given (embeds, weights, actions, ws): they must stay valid
+ * until jn_infer_plan_destroy.  Error statuses enqueue nothing. */
+typedef struct jn_infer_plan jn_infer_plan;
+jn_status jn_infer_workspace_size(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                                  const jn_pack_opts* opts, const jn_backbone* bb, const jn_head* heads,
+                                  size_t* bytes);
+jn_status jn_infer_plan_create(jn_ctx* ctx, const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                               const jn_pack_opts* opts, const jn_backbone* bb, const jn_head* heads,
+                               float* const* actions, void* ws, size_t ws_bytes, jn_infer_plan** out);
+/* The plan's physical batch (device pointers into ws) and its hidden rows
+ * (device bf16 [T][d]), e.g. for jn_unpack. */
+jn_status jn_infer_plan_packed(const jn_infer_plan* plan, jn_packed* out, void** hidden);
+/* Enqueue one inference step on the context stream (kernels only). */
+jn_status jn_infer_plan_launch(jn_ctx* ctx, const jn_infer_plan* plan);
+/* Record one launch into a HIP graph on the context stream, which must not
+ * be the null stream and must not have the launch trace enabled
+ * (JN_EUNSUPPORTED); replaces a previously captured graph. */
+jn_status jn_infer_plan_capture(jn_ctx* ctx, jn_infer_plan* plan);
+/* Launch the captured graph on the context stream (JN_EINVAL if none). */
+jn_status jn_infer_plan_replay(jn_ctx* ctx, const jn_infer_plan* plan);
+void jn_infer_plan_destroy(jn_infer_plan* plan);
 
 #ifdef __cplusplus
 }

@@ -23,9 +23,10 @@ Modules
   expert    -- per-tenant action expert (config 4) forward, loss, gradients
   optim     -- per-tenant AdamW optimizer step
   step      -- the isolated-execution reference of the whole step
+  batching  -- the inference queue's FIFO-compatible-prefix batching
 
 Pins: every function here is checked in ``tests/test_oracle_pins.py``
 against closed forms, invariants, special cases that reduce to library
 routines, brute force on tiny inputs and finite differences.
 """
-from . import plan, backbone, heads, step, expert, optim  # noqa: F401
+from . import plan, backbone, heads, step, expert, optim, batching  # noqa: F401

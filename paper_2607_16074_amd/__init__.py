@@ -26,6 +26,7 @@ __all__ = [
     "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
     "Expert", "ExpertIO", "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
     "AdamWTenant", "jn_adamw_workspace_size", "jn_tenant_adamw_step",
+    "Collector", "InferPlan", "jn_infer_workspace_size",
     "lib_path",
 ]
 
@@ -433,3 +434,101 @@ def jn_unpack(ctx: Context, packed: Packed, reqs: Sequence[Request], rows, row_b
     ra, keep = _requests(reqs)
     oa = (C.c_void_p * len(outs))(*[_ptr(o) for o in outs])
     _check(_lib.jn_unpack(ctx.handle, C.byref(packed.struct), ra, len(reqs), _ptr(rows), int(row_bytes), oa), ctx)
+
+
+# ------------------------------------------------ inference-side batching ---
+
+class Collector:
+    """The inference queue's FIFO-compatible-prefix collector (host only):
+    ``jn_collector_create / submit / poll / status``."""
+
+    def __init__(self, max_batch_samples: int, timeout_us: int):
+        h = C.c_void_p()
+        _check(_lib.jn_collector_create(C.byref(h), int(max_batch_samples), int(timeout_us)),
+               what="jn_collector_create")
+        self.handle = h
+
+    def submit(self, request_id: int, prefix_sig: int, d_model: int, n_samples: int, arrival_us: int):
+        _check(_lib.jn_collector_submit(self.handle, int(request_id), int(prefix_sig), int(d_model), int(n_samples),
+                                        int(arrival_us)), what="jn_collector_submit")
+
+    def poll(self, now_us: int, cap: int = 4096) -> list:
+        """Request ids of the batch ready at ``now_us`` (empty if none)."""
+        ids = (C.c_int64 * max(cap, 1))()
+        n = C.c_int32()
+        _check(_lib.jn_collector_poll(self.handle, int(now_us), ids, int(cap), C.byref(n)), what="jn_collector_poll")
+        return list(ids[: n.value])
+
+    def status(self):
+        """(queued requests, time the current prefix becomes ready or -1)."""
+        n, t = C.c_int32(), C.c_int64()
+        _check(_lib.jn_collector_status(self.handle, C.byref(n), C.byref(t)), what="jn_collector_status")
+        return int(n.value), int(t.value)
+
+    def close(self):
+        if self.handle:
+            _lib.jn_collector_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def jn_infer_workspace_size(reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int, bb: Backbone,
+                            heads: Sequence[Head]) -> int:
+    ra, keep = _requests(reqs)
+    ha, _ = _head_arrays(heads)
+    o = _opts(d, align)
+    n = C.c_size_t()
+    _check(_lib.jn_infer_workspace_size(ra, len(reqs), _tenants(tenants), len(tenants), C.byref(o),
+                                        C.byref(bb.struct), ha, C.byref(n)), what="jn_infer_workspace_size")
+    return int(n.value)
+
+
+class InferPlan:
+    """``jn_infer_plan_*``: a resident decode-only step over one physical batch
+    (device buffers stay referenced here for the plan's lifetime)."""
+
+    def __init__(self, ctx: Context, reqs: Sequence[Request], tenants: Sequence[Tenant], d: int, align: int,
+                 bb: Backbone, heads: Sequence[Head], actions: Sequence, ws):
+        ra, keep = _requests(reqs)
+        ha, _ = _head_arrays(heads)
+        o = _opts(d, align)
+        acts = (C.c_void_p * len(actions))(*[_ptr(a) for a in actions])
+        h = C.c_void_p()
+        _check(_lib.jn_infer_plan_create(ctx.handle, ra, len(reqs), _tenants(tenants), len(tenants), C.byref(o),
+                                         C.byref(bb.struct), ha, acts, _ptr(ws), ws.numel() * ws.element_size(),
+                                         C.byref(h)), ctx)
+        self.handle = h
+        self.ctx = ctx
+        self._keep = (reqs, bb, heads, actions, ws)
+
+    def packed(self):
+        """(jn_packed struct, hidden device pointer) of the plan's batch."""
+        s = jn_packed()
+        hid = C.c_void_p()
+        _check(_lib.jn_infer_plan_packed(self.handle, C.byref(s), C.byref(hid)), what="jn_infer_plan_packed")
+        return s, hid.value
+
+    def launch(self):
+        _check(_lib.jn_infer_plan_launch(self.ctx.handle, self.handle), self.ctx)
+
+    def capture(self):
+        _check(_lib.jn_infer_plan_capture(self.ctx.handle, self.handle), self.ctx)
+
+    def replay(self):
+        _check(_lib.jn_infer_plan_replay(self.ctx.handle, self.handle), self.ctx)
+
+    def close(self):
+        if self.handle:
+            _lib.jn_infer_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -26,6 +26,10 @@ EXPORTS = (
     "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
     "jn_adamw_workspace_size", "jn_tenant_adamw_step",
     "jn_unpack",
+    "jn_collector_create", "jn_collector_destroy", "jn_collector_submit", "jn_collector_poll",
+    "jn_collector_status",
+    "jn_infer_workspace_size", "jn_infer_plan_create", "jn_infer_plan_packed", "jn_infer_plan_launch",
+    "jn_infer_plan_capture", "jn_infer_plan_replay", "jn_infer_plan_destroy",
 )
 
 
@@ -168,6 +172,20 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "jn_adamw_workspace_size": (C.c_int, [P(jn_adamw_tenant), C.c_int32, P(C.c_size_t)]),
         "jn_tenant_adamw_step": (C.c_int, [V, P(jn_adamw_tenant), C.c_int32, V, C.c_size_t]),
         "jn_unpack": (C.c_int, [V, P(jn_packed), P(jn_request), C.c_int32, V, C.c_size_t, P(V)]),
+        "jn_collector_create": (C.c_int, [P(V), C.c_int32, C.c_int64]),
+        "jn_collector_destroy": (None, [V]),
+        "jn_collector_submit": (C.c_int, [V, C.c_int64, C.c_uint64, C.c_int32, C.c_int32, C.c_int64]),
+        "jn_collector_poll": (C.c_int, [V, C.c_int64, P(C.c_int64), C.c_int32, P(C.c_int32)]),
+        "jn_collector_status": (C.c_int, [V, P(C.c_int32), P(C.c_int64)]),
+        "jn_infer_workspace_size": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                              P(jn_backbone), P(jn_head), P(C.c_size_t)]),
+        "jn_infer_plan_create": (C.c_int, [V, P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
+                                           P(jn_backbone), P(jn_head), P(V), V, C.c_size_t, P(V)]),
+        "jn_infer_plan_packed": (C.c_int, [V, P(jn_packed), P(V)]),
+        "jn_infer_plan_launch": (C.c_int, [V, V]),
+        "jn_infer_plan_capture": (C.c_int, [V, V]),
+        "jn_infer_plan_replay": (C.c_int, [V, V]),
+        "jn_infer_plan_destroy": (None, [V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

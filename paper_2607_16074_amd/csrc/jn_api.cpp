@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <functional>
 #include <new>
 #include <string>
@@ -441,7 +442,7 @@ jn_status jn_pack_group(jn_ctx* c, const jn_request* req, int32_t R, const jn_te
 namespace {
 
 struct BbLayout {
-  size_t x, h, qkv, att, mid, total;
+  size_t x, h, qkv, att, mid, split, split_bytes, total;
 };
 
 BbLayout bb_layout(const jn_backbone* bb, int64_t T) {
@@ -458,6 +459,14 @@ BbLayout bb_layout(const jn_backbone* bb, int64_t T) {
   L.qkv = take(2 * T * 3 * d);
   L.att = take(2 * T * d);
   L.mid = take(2 * T * f);
+  // fp32 partials of the split-K launches (short batches only)
+  const bool glu = bb->layers && bb->layers[0].w_gate != nullptr;
+  size_t sb = std::max(gemm_split_bytes(EPI_BF16, (int32_t)T, (int32_t)(3 * d), (int32_t)d),
+                       gemm_split_bytes(EPI_RESID_F32, (int32_t)T, (int32_t)d, (int32_t)d));
+  sb = std::max(sb, gemm_split_bytes(EPI_RESID_F32, (int32_t)T, (int32_t)d, (int32_t)f));
+  if (!glu) sb = std::max(sb, gemm_split_bytes(EPI_GELU_BF16, (int32_t)T, (int32_t)f, (int32_t)d));
+  L.split_bytes = sb;
+  L.split = take(sb);
   L.total = o;
   return L;
 }
@@ -514,6 +523,8 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
   void* qkv = w + L.qkv;
   void* att = w + L.att;
   void* mid = w + L.mid;
+  void* sp = w + L.split;
+  const size_t spb = L.split_bytes;
   const bool glu = bb->layers[0].w_gate != nullptr;
   hipStream_t s = c->stream;
   for (int l = 0; l < bb->n_layers; ++l) {
@@ -523,22 +534,22 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
     else
       JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
     JN_TRACED(c, JN_OP_GEMM_QKV, T, 3 * d, d,
-              launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0), "gemm qkv");
+              launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0, sp, spb), "gemm qkv");
     JN_TRACED(c, JN_OP_ATTENTION, T, d, bb->n_heads,
               launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, p->max_seqlen,
                                p->align),
               "attention");
-    JN_TRACED(c, JN_OP_GEMM_O, T, d, d, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0),
+    JN_TRACED(c, JN_OP_GEMM_O, T, d, d, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0, sp, spb),
               "gemm o");
     JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, Ly.g2, h, T, d, bb->eps), "rmsnorm");
     if (glu)
       JN_TRACED(c, JN_OP_GEMM_UP, T, 2 * f, d,
                 launch_gemm(s, EPI_GEGLU_BF16, h, d, Ly.w_gate, Ly.w_up, d, mid, f, T, f, d, 0), "gemm geglu");
     else
-      JN_TRACED(c, JN_OP_GEMM_UP, T, f, d, launch_gemm(s, EPI_GELU_BF16, h, d, Ly.w_up, nullptr, d, mid, f, T, f, d, 0),
+      JN_TRACED(c, JN_OP_GEMM_UP, T, f, d, launch_gemm(s, EPI_GELU_BF16, h, d, Ly.w_up, nullptr, d, mid, f, T, f, d, 0, sp, spb),
                 "gemm up");
     JN_TRACED(c, JN_OP_GEMM_DOWN, T, d, f,
-              launch_gemm(s, EPI_RESID_F32, mid, f, Ly.w_down, nullptr, f, x, d, T, d, f, 0), "gemm down");
+              launch_gemm(s, EPI_RESID_F32, mid, f, Ly.w_down, nullptr, f, x, d, T, d, f, 0, sp, spb), "gemm down");
   }
   JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, bb->gf, hidden, T, d, bb->eps), "final rmsnorm");
   return JN_OK;
@@ -645,6 +656,8 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hid
   if (!c) return JN_EINVAL;
   if (!valid_packed(p)) return fail(c, JN_EINVAL, "invalid packed batch");
   if (!hidden || !io || !ws) return fail(c, JN_EINVAL, "null hidden, io or workspace");
+  if (((uintptr_t)hidden) % 16 != 0 || p->d % 8 != 0)
+    return fail(c, JN_EUNSUPPORTED, "hidden must be 16-byte aligned and d a multiple of 8");
   jn_status st = check_heads(c, p, heads, G);
   if (st != JN_OK) return st;
   for (int32_t g = 0; g < G; ++g) {
@@ -1581,6 +1594,421 @@ jn_status jn_tenant_adamw_step(jn_ctx* c, const jn_adamw_tenant* t, int32_t G, v
             launch_adamw(c->stream, (const AdamwTensor*)w, n, (const AdamwTenant*)(w + ten_off), blocks),
             "adamw kernel");
   return JN_OK;
+}
+
+}  // extern "C"
+
+// ============================================================ inference ===
+// Inference-side group batching (App. A.3 "Inference Queue Composition").
+// The collector holds host metadata of queued requests in arrival order and
+// releases the largest FIFO prefix that is compatible at the shared-prefix
+// boundary, bounded by a maximum batch size and a timeout.  The plan makes
+// one physical batch resident: every map and descriptor is uploaded once at
+// creation, and a launch only enqueues kernels (pack, backbone, pool, head
+// forward), which is what a HIP graph can record and replay.
+
+struct jn_collector {
+  struct Item {
+    int64_t id;
+    uint64_t sig;
+    int32_t d, n;
+    int64_t arrival;
+  };
+  int32_t max_batch = 0;
+  int64_t timeout_us = 0;
+  std::deque<Item> q;
+};
+
+struct jn_infer_plan {
+  jn_packed packed{};
+  std::vector<jn_layer> layers;
+  jn_backbone bb{};
+  void* hidden = nullptr;
+  void* bb_ws = nullptr;
+  size_t bb_bytes = 0;
+  float* P = nullptr;
+  const HeadGemm* dd = nullptr;
+  const HeadTile* dt = nullptr;
+  std::vector<std::pair<int32_t, int32_t>> fwd_rng;
+  int32_t max_rows = 0;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+namespace {
+
+// Prefix the collector would release now: count of requests and whether the
+// prefix can no longer grow (size reached, or the next queued request is
+// incompatible or would overflow the batch).
+void collector_prefix(const jn_collector* c, int32_t* count, int64_t* samples, bool* final_) {
+  *count = 0;
+  *samples = 0;
+  *final_ = false;
+  if (c->q.empty()) return;
+  const jn_collector::Item& head = c->q.front();
+  int64_t total = 0;
+  int32_t k = 0;
+  for (const jn_collector::Item& it : c->q) {
+    if (it.sig != head.sig || it.d != head.d) {
+      *final_ = true;
+      break;
+    }
+    if (k > 0 && total + it.n > c->max_batch) {
+      *final_ = true;
+      break;
+    }
+    total += it.n;
+    ++k;
+    if (total >= c->max_batch) {
+      *final_ = true;
+      break;
+    }
+  }
+  *count = k;
+  *samples = total;
+}
+
+// Forward-only head plan inside `w` (fwd tables only): P | Z_k | H_k | descs | tiles.
+struct HeadFwdLayout {
+  int maxL = 0;
+  std::vector<int64_t> width;
+  size_t P = 0, descs = 0, tiles = 0, total = 0;
+  std::vector<size_t> Z, H;
+};
+
+HeadFwdLayout head_fwd_layout(int64_t N, int64_t d, const jn_head* heads, int32_t G) {
+  HeadFwdLayout L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  for (int32_t g = 0; g < G; ++g) L.maxL = std::max(L.maxL, heads[g].n_layers);
+  L.width.assign(L.maxL, 0);
+  for (int32_t g = 0; g < G; ++g)
+    for (int k = 0; k < heads[g].n_layers; ++k) L.width[k] = std::max<int64_t>(L.width[k], heads[g].dims[k + 1]);
+  L.P = take(4 * N * d);
+  L.Z.resize(L.maxL);
+  L.H.resize(L.maxL);
+  for (int k = 0; k < L.maxL; ++k) {
+    L.Z[k] = take(4 * N * L.width[k]);
+    L.H[k] = take(4 * N * L.width[k]);
+  }
+  const int64_t tm_dyn = (N + kHT - 1) / kHT;
+  int64_t ntiles = 0, ndesc = 0;
+  for (int32_t g = 0; g < G; ++g)
+    for (int k = 0; k < heads[g].n_layers; ++k) {
+      ntiles += tm_dyn * ((heads[g].dims[k + 1] + kHT - 1) / kHT);
+      ++ndesc;
+    }
+  L.descs = take(sizeof(HeadGemm) * ndesc);
+  L.tiles = take(sizeof(HeadTile) * ntiles);
+  L.total = o;
+  return L;
+}
+
+// The plan's workspace: maps | tokens | hidden | backbone workspace | heads.
+struct InferLayout {
+  MapLayout m;
+  BbLayout bl;
+  HeadFwdLayout hl;
+  size_t maps = 0, tokens = 0, hidden = 0, bb = 0, heads = 0, total = 0;
+};
+
+jn_status infer_layout(jn_ctx* c, const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                       const jn_pack_opts* o, const jn_backbone* bb, const jn_head* heads, Plan* p,
+                       InferLayout* L) {
+  jn_status st = make_plan(c, req, R, ten, G, o, p);
+  if (st != JN_OK) return st;
+  st = check_backbone(c, bb);
+  if (st != JN_OK) return st;
+  if (bb->d != o->d_model) return fail(c, JN_EINCOMPAT, "pack width %d != backbone width %d", o->d_model, bb->d);
+  if (o->d_model % 8 != 0) return fail(c, JN_EUNSUPPORTED, "d_model %d not a multiple of 8", o->d_model);
+  jn_packed shape{};
+  shape.R = R;
+  shape.G = G;
+  shape.N = p->N;
+  shape.T = p->T;
+  shape.d = o->d_model;
+  if (!heads) return fail(c, JN_EINVAL, "null heads");
+  for (int32_t g = 0; g < G; ++g) {
+    const jn_head& H = heads[g];
+    if (H.n_layers < 1 || !H.dims || !H.W || !H.b) return fail(c, JN_EINVAL, "head %d incomplete", g);
+    if (H.dims[0] != o->d_model) return fail(c, JN_EINCOMPAT, "head %d input %d != feature width %d", g, H.dims[0], o->d_model);
+    for (int k = 0; k <= H.n_layers; ++k)
+      if (H.dims[k] < 1) return fail(c, JN_EINVAL, "head %d dims[%d] < 1", g, k);
+    if ((int64_t)H.action_dim * H.chunk != H.dims[H.n_layers])
+      return fail(c, JN_EINVAL, "head %d output %d != action_dim*chunk", g, H.dims[H.n_layers]);
+    for (int k = 0; k < H.n_layers; ++k)
+      if (!H.W[k] || !H.b[k]) return fail(c, JN_EINVAL, "head %d layer %d null weight", g, k);
+  }
+  L->m = map_layout(p->N, p->T, G, R);
+  L->bl = bb_layout(bb, p->T);
+  L->hl = head_fwd_layout(p->N, o->d_model, heads, G);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  L->maps = take(L->m.total);
+  L->tokens = take((size_t)p->T * o->d_model * 2);
+  L->hidden = take((size_t)p->T * o->d_model * 2);
+  L->bb = take(L->bl.total);
+  L->heads = take(L->hl.total);
+  L->total = off;
+  return JN_OK;
+}
+
+jn_status infer_enqueue(jn_ctx* c, const jn_infer_plan* pl) {
+  const jn_packed& pk = pl->packed;
+  hipStream_t s = c->stream;
+  JN_TRACED(c, JN_OP_PACK, pk.T, pk.d, 0,
+            launch_pack(s, (const ReqEntry*)pk.req_table, pk.sample_request, pk.sample_local, pk.seqlens,
+                        pk.cu_seqlens, pk.N, pk.d, pk.align, pl->max_rows, pk.tokens, pk.token_sample,
+                        pk.token_pos),
+            "pack kernel");
+  jn_status st = jn_backbone_forward(c, &pl->bb, &pk, pl->hidden, pl->bb_ws, pl->bb_bytes);
+  if (st != JN_OK) return st;
+  JN_TRACED(c, JN_OP_POOL, pk.T, pk.d, pk.N,
+            launch_pool(s, pl->hidden, pk.seqlens, pk.cu_seqlens, pk.sample_tenant_rank, pk.N, pk.d, pl->P), "pool");
+  for (auto& r : pl->fwd_rng)
+    if (r.second)
+      JN_TRACED(c, JN_OP_HEAD_FWD, r.second, 0, 0,
+                launch_head_gemm(s, pl->dd, pl->dt + r.first, r.second, pk.tenant_sample_off), "head fwd");
+  return JN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+jn_status jn_collector_create(jn_collector** out, int32_t max_batch_samples, int64_t timeout_us) {
+  if (!out) return JN_EINVAL;
+  *out = nullptr;
+  if (max_batch_samples < 1 || timeout_us < 0) return JN_EINVAL;
+  jn_collector* c = new (std::nothrow) jn_collector();
+  if (!c) return JN_EINVAL;
+  c->max_batch = max_batch_samples;
+  c->timeout_us = timeout_us;
+  *out = c;
+  return JN_OK;
+}
+
+void jn_collector_destroy(jn_collector* c) { delete c; }
+
+jn_status jn_collector_submit(jn_collector* c, int64_t request_id, uint64_t prefix_sig, int32_t d_model,
+                              int32_t n_samples, int64_t arrival_us) {
+  if (!c || n_samples < 1 || d_model < 1) return JN_EINVAL;
+  if (!c->q.empty() && arrival_us < c->q.back().arrival) return JN_EINVAL;  // arrival order
+  c->q.push_back(jn_collector::Item{request_id, prefix_sig, d_model, n_samples, arrival_us});
+  return JN_OK;
+}
+
+jn_status jn_collector_poll(jn_collector* c, int64_t now_us, int64_t* ids, int32_t cap, int32_t* n) {
+  if (!c || !n || (cap > 0 && !ids)) return JN_EINVAL;
+  *n = 0;
+  if (c->q.empty()) return JN_OK;
+  int32_t k;
+  int64_t samples;
+  bool fin;
+  collector_prefix(c, &k, &samples, &fin);
+  const bool expired = now_us - c->q.front().arrival >= c->timeout_us;
+  if (!fin && !expired) return JN_OK;
+  if (cap < k) return JN_ENOSPACE;
+  for (int32_t i = 0; i < k; ++i) {
+    ids[i] = c->q.front().id;
+    c->q.pop_front();
+  }
+  *n = k;
+  return JN_OK;
+}
+
+jn_status jn_collector_status(const jn_collector* c, int32_t* pending, int64_t* deadline_us) {
+  if (!c || !pending || !deadline_us) return JN_EINVAL;
+  *pending = (int32_t)c->q.size();
+  if (c->q.empty()) {
+    *deadline_us = -1;
+    return JN_OK;
+  }
+  int32_t k;
+  int64_t samples;
+  bool fin;
+  collector_prefix(c, &k, &samples, &fin);
+  *deadline_us = fin ? c->q.front().arrival : c->q.front().arrival + c->timeout_us;
+  return JN_OK;
+}
+
+jn_status jn_infer_workspace_size(const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                                  const jn_pack_opts* o, const jn_backbone* bb, const jn_head* heads,
+                                  size_t* bytes) {
+  if (!bytes) return JN_EINVAL;
+  Plan p;
+  InferLayout L;
+  jn_status st = infer_layout(nullptr, req, R, ten, G, o, bb, heads, &p, &L);
+  if (st != JN_OK) return st;
+  *bytes = L.total;
+  return JN_OK;
+}
+
+jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, const jn_tenant* ten, int32_t G,
+                               const jn_pack_opts* o, const jn_backbone* bb, const jn_head* heads,
+                               float* const* actions, void* ws, size_t ws_bytes, jn_infer_plan** out) {
+  if (!c) return JN_EINVAL;
+  if (!out || !actions || !ws) return fail(c, JN_EINVAL, "null output, actions or workspace");
+  *out = nullptr;
+  Plan p;
+  InferLayout L;
+  jn_status st = infer_layout(c, req, R, ten, G, o, bb, heads, &p, &L);
+  if (st != JN_OK) return st;
+  if (ws_bytes < L.total) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, L.total);
+  if (((uintptr_t)ws) % 256 != 0) return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte aligned");
+  for (int32_t r = 0; r < R; ++r)
+    if (((uintptr_t)req[r].embeds) % 16 != 0) return fail(c, JN_EUNSUPPORTED, "request %d embeds not 16-byte aligned", r);
+  for (int32_t g = 0; g < G; ++g)
+    if (!actions[g]) return fail(c, JN_EINVAL, "actions %d is null", g);
+
+  jn_infer_plan* pl = new (std::nothrow) jn_infer_plan();
+  if (!pl) return fail(c, JN_EINVAL, "out of host memory");
+  char* w = (char*)ws;
+  char* maps = w + L.maps;
+  fill_packed(&pl->packed, maps, L.m, p, R, G, o);
+  pl->packed.tokens = w + L.tokens;
+  pl->max_rows = p.max_rows;
+  pl->layers.assign(bb->layers, bb->layers + bb->n_layers);
+  pl->bb = *bb;
+  pl->bb.layers = pl->layers.data();
+  pl->hidden = w + L.hidden;
+  pl->bb_ws = w + L.bb;
+  pl->bb_bytes = L.bl.total;
+
+  // head forward descriptors: one launch per layer index, the last layer of
+  // tenant g writing straight into actions[g] (rows in the tenant's arrival order)
+  const HeadFwdLayout& hl = L.hl;
+  char* hw = w + L.heads;
+  pl->P = (float*)(hw + hl.P);
+  const int64_t N = p.N, d = o->d_model;
+  const int32_t tm_dyn = (int32_t)((N + kHT - 1) / kHT);
+  std::vector<HeadGemm> descs;
+  std::vector<HeadTile> tiles;
+  for (int k = 0; k < hl.maxL; ++k) {
+    int32_t t0 = (int32_t)tiles.size();
+    for (int32_t g = 0; g < G; ++g) {
+      const jn_head& Hh = heads[g];
+      if (k >= Hh.n_layers) continue;
+      const int64_t in = Hh.dims[k], outw = Hh.dims[k + 1];
+      const bool last = k + 1 == Hh.n_layers;
+      HeadGemm D{};
+      D.A = (k == 0) ? pl->P : (const float*)(hw + hl.H[k - 1]);
+      D.sam = (k == 0) ? d : hl.width[k - 1];
+      D.sak = 1;
+      D.B = Hh.W[k];
+      D.sbk = 1;
+      D.sbn = in;
+      D.C = last ? actions[g] : (float*)(hw + hl.Z[k]);
+      D.ldc = last ? outw : hl.width[k];
+      D.bias = Hh.b[k];
+      D.Cact = last ? nullptr : (float*)(hw + hl.H[k]);
+      D.bumpA = D.sam;
+      D.bumpB = 0;
+      D.bumpC = last ? 0 : hl.width[k];
+      D.M = -1;
+      D.N = (int32_t)outw;
+      D.K = (int32_t)in;
+      D.tenant = g;
+      D.tiles_n = (int32_t)((outw + kHT - 1) / kHT);
+      const int32_t di = (int32_t)descs.size();
+      descs.push_back(D);
+      for (int32_t tm = 0; tm < tm_dyn; ++tm)
+        for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
+    }
+    pl->fwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+  }
+  const size_t dbytes = sizeof(HeadGemm) * descs.size(), tbytes = sizeof(HeadTile) * tiles.size();
+  if (hl.descs + dbytes > hl.tiles || hl.tiles + tbytes > hl.total) {
+    delete pl;
+    return fail(c, JN_ENOSPACE, "internal: head table sizing");
+  }
+  pl->dd = (const HeadGemm*)(hw + hl.descs);
+  pl->dt = (const HeadTile*)(hw + hl.tiles);
+
+  // one-time uploads: maps, request table, head tables
+  std::vector<char> img = host_head_image(L.m, p);
+  std::vector<ReqEntry> rt(R);
+  for (int32_t r = 0; r < R; ++r) rt[r] = ReqEntry{req[r].embeds, nullptr, req[r].max_len, req[r].n_samples, p.req_first[r], 0};
+  std::vector<char> himg(hl.total - hl.descs, 0);
+  std::memcpy(himg.data(), descs.data(), dbytes);
+  std::memcpy(himg.data() + (hl.tiles - hl.descs), tiles.data(), tbytes);
+  st = stage_copy(c, maps, img.data(), img.size());
+  if (st == JN_OK) st = stage_copy(c, maps + L.m.reqtab, rt.data(), sizeof(ReqEntry) * R);
+  if (st == JN_OK) st = stage_copy(c, hw + hl.descs, himg.data(), hl.tiles - hl.descs + tbytes);
+  if (st != JN_OK) {
+    delete pl;
+    return st;
+  }
+  *out = pl;
+  return JN_OK;
+}
+
+jn_status jn_infer_plan_packed(const jn_infer_plan* pl, jn_packed* out, void** hidden) {
+  if (!pl || !out) return JN_EINVAL;
+  *out = pl->packed;
+  if (hidden) *hidden = pl->hidden;
+  return JN_OK;
+}
+
+jn_status jn_infer_plan_launch(jn_ctx* c, const jn_infer_plan* pl) {
+  if (!c) return JN_EINVAL;
+  if (!pl) return fail(c, JN_EINVAL, "null plan");
+  return infer_enqueue(c, pl);
+}
+
+jn_status jn_infer_plan_capture(jn_ctx* c, jn_infer_plan* pl) {
+  if (!c) return JN_EINVAL;
+  if (!pl) return fail(c, JN_EINVAL, "null plan");
+  if (!c->stream) return fail(c, JN_EUNSUPPORTED, "graph capture needs a non-null stream");
+  if (c->trace) return fail(c, JN_EUNSUPPORTED, "disable the launch trace before capturing");
+  if (pl->exec) {
+    hipGraphExecDestroy(pl->exec);
+    pl->exec = nullptr;
+  }
+  if (pl->graph) {
+    hipGraphDestroy(pl->graph);
+    pl->graph = nullptr;
+  }
+  JN_HIP(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+  jn_status st = infer_enqueue(c, pl);
+  hipGraph_t graph = nullptr;
+  hipError_t e = hipStreamEndCapture(c->stream, &graph);
+  if (st != JN_OK) {
+    if (graph) hipGraphDestroy(graph);
+    return st;
+  }
+  if (e != hipSuccess || !graph) return hip_fail(c, e != hipSuccess ? e : hipErrorUnknown, "hipStreamEndCapture");
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    hipGraphDestroy(graph);
+    return hip_fail(c, e, "hipGraphInstantiate");
+  }
+  pl->graph = graph;
+  pl->exec = exec;
+  return JN_OK;
+}
+
+jn_status jn_infer_plan_replay(jn_ctx* c, const jn_infer_plan* pl) {
+  if (!c) return JN_EINVAL;
+  if (!pl || !pl->exec) return fail(c, JN_EINVAL, "plan has no captured graph");
+  JN_HIP(c, hipGraphLaunch(pl->exec, c->stream), "hipGraphLaunch");
+  return JN_OK;
+}
+
+void jn_infer_plan_destroy(jn_infer_plan* pl) {
+  if (!pl) return;
+  if (pl->exec) hipGraphExecDestroy(pl->exec);
+  if (pl->graph) hipGraphDestroy(pl->graph);
+  delete pl;
 }
 
 }  // extern "C"

@@ -61,6 +61,8 @@ struct GemmArgs {
   int64_t ldx, ldw, ldc, ldaux;
   int32_t M, N, K;
   int32_t tiles_m, tiles_n, tile_start;  // filled by the launchers
+  int64_t split_c;      // split-K: elements between the fp32 partial outputs of
+                        // consecutive K ranges (blockIdx.y); 0 when unsplit
 };
 
 // Grouped launch over nprob problems sharing one epilogue: the host fills
@@ -75,9 +77,17 @@ hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, i
 // C[M][N] (+)= epi(A[M][K] * B[N][K]^T); A, B bf16 row-major with leading
 // dims lda, ldb (elements); for EPI_GEGLU_BF16, B is w_gate and B2 is w_up,
 // each [N][K], and C has N columns.
+//
+// Launches with few tiles for the GPU and a long K (epilogues EPI_BF16,
+// EPI_RESID_F32, EPI_GELU_BF16) split K into gemm_split() ranges when
+// `split_ws` holds gemm_split_bytes(): each range writes fp32 partials and a
+// reduction adds them in range order, then applies the epilogue.  The split
+// depends only on (epi, M, N, K).
 hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B,
                        const void* B2, int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N,
-                       int32_t K, int tile_hint);
+                       int32_t K, int tile_hint, void* split_ws = nullptr, size_t split_bytes = 0);
+int gemm_split(int epi, int32_t M, int32_t N, int32_t K);
+size_t gemm_split_bytes(int epi, int32_t M, int32_t N, int32_t K);
 
 // Varlen attention over the packed batch (bidirectional inside each sample).
 // qkv: bf16 [T][3d]; out: bf16 [T][d].  Alignment rows of `out` are zeroed.

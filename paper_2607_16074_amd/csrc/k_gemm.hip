@@ -276,10 +276,60 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   }
 }
 
+// Split-K: K range blockIdx.y of a launch whose g.K is the per-range length.
+__device__ __forceinline__ GemmArgs split_range(const GemmArgs& g) {
+  GemmArgs r = g;
+  const int32_t s = blockIdx.y;
+  if (s) {
+    r.X += (int64_t)s * g.K;
+    r.W += (int64_t)s * g.K;
+    r.C = reinterpret_cast<float*>(g.C) + (int64_t)s * g.split_c;
+  }
+  return r;
+}
+
 template <int BN, int BM, int WGN, int WGM, int EPI>
 __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * (BN + BM) * kBK];
-  gemm_tile<BN, BM, WGN, WGM, EPI>(g, blockIdx.x, lds);
+  gemm_tile<BN, BM, WGN, WGM, EPI>(split_range(g), blockIdx.x, lds);
+}
+
+// Sum of the split-K partials in range order, then the epilogue.  Thread =
+// 4 consecutive output columns of one row.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int32_t S,
+                                                            int64_t stride, int32_t M, int32_t N,
+                                                            void* __restrict__ C, int64_t ldc) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int32_t q = N / 4;
+  if (e >= (int64_t)M * q) return;
+  const int32_t m = (int32_t)(e / q), n = (int32_t)(e % q) * 4;
+  float4 acc = *reinterpret_cast<const float4*>(part + (int64_t)m * N + n);
+  for (int32_t s = 1; s < S; ++s) {
+    const float4 v = *reinterpret_cast<const float4*>(part + s * stride + (int64_t)m * N + n);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  if constexpr (EPI == EPI_RESID_F32) {
+    float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
+    float4 o = *p;
+    o.x += acc.x;
+    o.y += acc.y;
+    o.z += acc.z;
+    o.w += acc.w;
+    *p = o;
+  } else {
+    if constexpr (EPI == EPI_GELU_BF16) {
+      acc.x = gelu_fast_f(acc.x);
+      acc.y = gelu_fast_f(acc.y);
+      acc.z = gelu_fast_f(acc.z);
+      acc.w = gelu_fast_f(acc.w);
+    }
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+        make_uint2(pack_bf2(acc.x, acc.y), pack_bf2(acc.z, acc.w));
+  }
 }
 
 // One launch over several independent problems (one per tenant): block b
@@ -457,12 +507,12 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs g) {
 }
 
 template <int BN, int BM, int WGN, int WGM>
-static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g) {
+static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1) {
   const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
   g.tiles_m = (g.M + BM - 1) / BM;
   g.tiles_n = (NL + BN - 1) / BN;
   g.tile_start = 0;
-  dim3 grid(g.tiles_m * g.tiles_n), block(64 * WGN * WGM);
+  dim3 grid(g.tiles_m * g.tiles_n, splits), block(64 * WGN * WGM);
 #define JN_GEMM_CASE(E) \
   case E: gemm_kernel<BN, BM, WGN, WGM, E><<<grid, block, 0, s>>>(g); break;
   switch (epi) {
@@ -519,9 +569,90 @@ int gemm_pick_tile(int epi, int32_t M, int32_t N) {
   return best;
 }
 
+// Split-K: tile shape and K split S chosen together by an estimated time:
+// waves of tiles * S over kSplitCUs, each a tile of 2 * BN * BM * K / S flops
+// (times the shape factor) at the per-CU rate measured for this GEMM, plus
+// the fp32 partials written and read back (2 * 4 * S * M * N bytes) at a
+// sustained HBM rate.  Splits are considered only for launches of at most
+// kSplitCUs / 2 tiles, with ranges of K / S >= 1024 (16 slabs) and S a power
+// of two; S = 1 reproduces gemm_pick_tile's choice.  Fixed constants keep the
+// size query and the launch in agreement on any device.
+constexpr int32_t kSplitCUs = 256;
+constexpr double kCuFlops = 4.3e12;    // ~1.1 PFLOP/s over 256 CUs
+constexpr double kPartialBw = 5.0e12;  // bytes/s for the partial round trip
+
+static void gemm_plan(int epi, int32_t M, int32_t N, int32_t K, int* tile, int* splits) {
+  *tile = gemm_pick_tile(epi, M, N);
+  *splits = 1;
+  if (epi != EPI_BF16 && epi != EPI_RESID_F32 && epi != EPI_GELU_BF16) return;
+  if (M <= 0 || N <= 0 || K <= 0 || N % 4 != 0) return;
+  static const int bn[3] = {256, 256, 128}, bm[3] = {256, 128, 128};
+  static const double eff[3] = {1.0, 1.12, 1.35};
+  double best = 1e300;
+  for (int t = 0; t < 3; ++t) {
+    const int64_t tiles = (int64_t)((M + bm[t] - 1) / bm[t]) * ((N + bn[t] - 1) / bn[t]);
+    for (int S = 1; S <= 64; S *= 2) {
+      if (S > 1 && (tiles * 2 > kSplitCUs || K % (kBK * S) != 0 || K / S < 1024)) break;
+      const double waves = (double)((tiles * S + kSplitCUs - 1) / kSplitCUs);
+      double cost = waves * 2.0 * bn[t] * bm[t] * eff[t] * ((double)K / S) / kCuFlops;
+      if (S > 1) cost += 8.0 * S * (double)M * N / kPartialBw;
+      if (cost < best * 0.999) {
+        best = cost;
+        *tile = t;
+        *splits = S;
+      }
+    }
+  }
+}
+
+int gemm_split(int epi, int32_t M, int32_t N, int32_t K) {
+  int t, S;
+  gemm_plan(epi, M, N, K, &t, &S);
+  return S;
+}
+
+size_t gemm_split_bytes(int epi, int32_t M, int32_t N, int32_t K) {
+  const int S = gemm_split(epi, M, N, K);
+  return S > 1 ? (size_t)S * M * N * sizeof(float) : 0;
+}
+
 hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2, int64_t ldb,
-                       void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int tile_hint) {
+                       void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int tile_hint, void* split_ws,
+                       size_t split_bytes) {
   if (M <= 0 || N <= 0 || K <= 0 || K % kBK != 0 || N % 32 != 0) return hipErrorInvalidValue;
+  int t_split = 0, S = 1;
+  if (tile_hint <= 0) gemm_plan(epi, M, N, K, &t_split, &S);
+  if (S > 1 && split_ws && split_bytes >= (size_t)S * M * N * sizeof(float)) {
+    GemmArgs g{};
+    g.X = reinterpret_cast<const uint16_t*>(A);
+    g.W = reinterpret_cast<const uint16_t*>(B);
+    g.C = split_ws;
+    g.ldx = lda;
+    g.ldw = ldb;
+    g.ldc = N;
+    g.M = M;
+    g.N = N;
+    g.K = K / S;
+    g.split_c = (int64_t)M * N;
+    hipError_t e;
+    switch (t_split) {
+      case 0: e = launch_tile<256, 256, 2, 4>(s, EPI_F32, g, S); break;
+      case 1: e = launch_tile<256, 128, 4, 2>(s, EPI_F32, g, S); break;
+      default: e = launch_tile<128, 128, 2, 2>(s, EPI_F32, g, S); break;
+    }
+    if (e != hipSuccess) return e;
+    const int64_t work = (int64_t)M * (N / 4);
+    const dim3 grid((unsigned)((work + 255) / 256));
+    const float* part = reinterpret_cast<const float*>(split_ws);
+    switch (epi) {
+      case EPI_BF16: splitk_reduce_kernel<EPI_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
+      case EPI_RESID_F32:
+        splitk_reduce_kernel<EPI_RESID_F32><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc);
+        break;
+      default: splitk_reduce_kernel<EPI_GELU_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
+    }
+    return hipGetLastError();
+  }
   GemmArgs g{};
   g.X = reinterpret_cast<const uint16_t*>(A);
   g.W = reinterpret_cast<const uint16_t*>(B);

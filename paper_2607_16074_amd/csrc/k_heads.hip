@@ -14,61 +14,69 @@ namespace jnx {
 
 // ------------------------------------------------------------------ pool ---
 
-template <int CPT>  // column pairs per thread
+// Block = (64-column chunk, sample); 256 threads = 8 column groups (8
+// columns, one 16-byte load each) x 32 row lanes.  Row lane r sums rows
+// r, r+32, r+64, ... of the sample; the 32 lane sums are then combined by a
+// fixed pairwise tree in LDS.  The order depends only on the sample's own
+// length, so a sample pools to the same bits in any batch.
+constexpr int kPoolCols = 64;
+constexpr int kPoolLanes = 32;
+
 __global__ __launch_bounds__(256) void pool_kernel(const uint16_t* __restrict__ hidden,
                                                    const int32_t* __restrict__ seqlens,
                                                    const int32_t* __restrict__ cu_seqlens,
                                                    const int32_t* __restrict__ rank, int32_t d,
                                                    float* __restrict__ pooled) {
-  const int32_t i = blockIdx.x;
+  __shared__ float red[kPoolLanes][kPoolCols + 1];
+  const int32_t chunks = (d + kPoolCols - 1) / kPoolCols;
+  const int32_t i = blockIdx.x / chunks;
+  const int32_t c0 = (blockIdx.x % chunks) * kPoolCols;
   const int32_t L = seqlens[i];
-  const uint32_t* base = reinterpret_cast<const uint32_t*>(hidden + (int64_t)cu_seqlens[i] * d);
-  const int32_t pairs = d / 2;
-  float acc[CPT][2];
+  const int cg = threadIdx.x & 7, r = threadIdx.x >> 3;
+  const int32_t col = c0 + cg * 8;
+  float acc[8];
 #pragma unroll
-  for (int c = 0; c < CPT; ++c) acc[c][0] = acc[c][1] = 0.f;
-  for (int32_t j = 0; j < L; ++j) {
-    const uint32_t* row = base + (int64_t)j * pairs;
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  if (col < d) {
+    const uint16_t* base = hidden + (int64_t)cu_seqlens[i] * d + col;
+    for (int32_t j = r; j < L; j += kPoolLanes) {
+      const uint4 w = *reinterpret_cast<const uint4*>(base + (int64_t)j * d);
+      const uint32_t v[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int32_t p = threadIdx.x + c * 256;
-      if (p < pairs) {
-        uint32_t w = row[p];
-        acc[c][0] += __uint_as_float(w << 16);
-        acc[c][1] += __uint_as_float(w & 0xffff0000u);
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += __uint_as_float(v[e] << 16);
+        acc[2 * e + 1] += __uint_as_float(v[e] & 0xffff0000u);
       }
     }
   }
-  const float inv = 1.0f / (float)L;
-  float* out = pooled + (int64_t)rank[i] * d;
 #pragma unroll
-  for (int c = 0; c < CPT; ++c) {
-    const int32_t p = threadIdx.x + c * 256;
-    if (p < pairs) *reinterpret_cast<float2*>(out + 2 * p) = make_float2(acc[c][0] * inv, acc[c][1] * inv);
+  for (int e = 0; e < 8; ++e) red[r][cg * 8 + e] = acc[e];
+  __syncthreads();
+  for (int w = kPoolLanes / 2; w > 0; w >>= 1) {
+    if (r < w) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[r][cg * 8 + e] += red[r + w][cg * 8 + e];
+    }
+    __syncthreads();
   }
+  if (threadIdx.x < kPoolCols && c0 + (int32_t)threadIdx.x < d)
+    pooled[(int64_t)rank[i] * d + c0 + threadIdx.x] = red[0][threadIdx.x] * (1.0f / (float)L);
 }
 
 hipError_t launch_pool(hipStream_t s, const void* hidden, const int32_t* seqlens, const int32_t* cu_seqlens,
                        const int32_t* rank, int32_t N, int32_t d, float* pooled) {
-  auto H = reinterpret_cast<const uint16_t*>(hidden);
-  const int cpt = (d / 2 + 255) / 256;
-  if (cpt <= 1)
-    pool_kernel<1><<<N, 256, 0, s>>>(H, seqlens, cu_seqlens, rank, d, pooled);
-  else if (cpt <= 2)
-    pool_kernel<2><<<N, 256, 0, s>>>(H, seqlens, cu_seqlens, rank, d, pooled);
-  else if (cpt <= 4)
-    pool_kernel<4><<<N, 256, 0, s>>>(H, seqlens, cu_seqlens, rank, d, pooled);
-  else if (cpt <= 8)
-    pool_kernel<8><<<N, 256, 0, s>>>(H, seqlens, cu_seqlens, rank, d, pooled);
-  else
-    return hipErrorInvalidValue;
+  const int64_t blocks = (int64_t)((d + kPoolCols - 1) / kPoolCols) * N;
+  if (d % 8 != 0 || N < 1 || blocks > 0x7fffffff) return hipErrorInvalidValue;
+  dim3 grid((unsigned)blocks);
+  pool_kernel<<<grid, 256, 0, s>>>(reinterpret_cast<const uint16_t*>(hidden), seqlens, cu_seqlens, rank, d, pooled);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------- head gemm ---
 
 constexpr int HT = 64;   // tile edge
-constexpr int HK = 16;   // k step
+constexpr int HK = 64;   // k step; the next step's operands are loaded into
+                         // registers while the current step is computed
 
 __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restrict__ descs,
                                                         const HeadTile* __restrict__ tiles,
@@ -91,21 +99,33 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
   float acc[4][4] = {};
   const bool a_k_fast = D.sak == 1;
   const bool b_k_fast = D.sbk == 1;
-  for (int32_t k0 = 0; k0 < K; k0 += HK) {
+  constexpr int Q = HT * HK / 256;  // operand elements per thread per step
+  float ra[Q], rb[Q];
+  auto load = [&](int32_t k0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < Q; ++q) {
       const int e = tid + 256 * q;
       int mm, kk;
       if (a_k_fast) { kk = e % HK; mm = e / HK; } else { mm = e % HT; kk = e / HT; }
       const int32_t m = m0 + mm, k = k0 + kk;
-      As[kk][mm] = (m < M && k < K) ? A[(int64_t)m * D.sam + (int64_t)k * D.sak] : 0.f;
+      ra[q] = (m < M && k < K) ? A[(int64_t)m * D.sam + (int64_t)k * D.sak] : 0.f;
       int nn;
       if (b_k_fast) { kk = e % HK; nn = e / HK; } else { nn = e % HT; kk = e / HT; }
       const int32_t n = n0 + nn, k2 = k0 + kk;
-      Bs[kk][nn] = (n < N && k2 < K) ? B[(int64_t)k2 * D.sbk + (int64_t)n * D.sbn] : 0.f;
+      rb[q] = (n < N && k2 < K) ? B[(int64_t)k2 * D.sbk + (int64_t)n * D.sbn] : 0.f;
+    }
+  };
+  load(0);
+  for (int32_t k0 = 0; k0 < K; k0 += HK) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int e = tid + 256 * q;
+      if (a_k_fast) As[e % HK][e / HK] = ra[q]; else As[e / HT][e % HT] = ra[q];
+      if (b_k_fast) Bs[e % HK][e / HK] = rb[q]; else Bs[e / HT][e % HT] = rb[q];
     }
     __syncthreads();
-#pragma unroll
+    if (k0 + HK < K) load(k0 + HK);
+#pragma unroll 8
     for (int kk = 0; kk < HK; ++kk) {
       float a[4], b[4];
 #pragma unroll

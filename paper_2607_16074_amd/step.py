@@ -10,6 +10,9 @@ tenant's head, allocates the buffers a given group of requests needs once
 tenants carry action experts)
 
 on one stream (``run``) with no allocation and no host synchronisation.
+``InferStep`` is the inference-side counterpart: one physical batch made
+resident by ``jn_infer_plan_create`` (pack, shared encode, split, forward-only
+decode), launched eagerly or replayed as a captured HIP graph.
 ``isolated_runs`` builds one such step per tenant over the same device
 weights: the serial-execution comparator of grouped execution, using the
 same kernels and the same tile rule.
@@ -20,8 +23,8 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from . import (EXPERT_LAYER_FIELDS, AdamWTenant, Backbone, Context, Expert, ExpertIO, Head, HeadIO, Request, Tenant,
-               jn_adamw_workspace_size, jn_backbone_forward, jn_backbone_workspace_size, jn_experts_workspace_size,
+from . import (EXPERT_LAYER_FIELDS, AdamWTenant, Backbone, Context, Expert, ExpertIO, Head, HeadIO, InferPlan,
+               Request, Tenant, jn_adamw_workspace_size, jn_infer_workspace_size, jn_backbone_forward, jn_backbone_workspace_size, jn_experts_workspace_size,
                jn_heads_workspace_size, jn_pack_group, jn_pack_plan, jn_pack_tenant_sizes, jn_tenant_adamw_step,
                jn_tenant_experts_fwd_bwd, jn_tenant_heads_fwd_bwd, jn_unpack)
 
@@ -162,6 +165,48 @@ class GroupStep:
         self.backbone()
         self.heads_fwd_bwd()
         self.unpack()
+
+
+class InferStep:
+    """A resident decode-only step over one group of requests on a stream of
+    its own (graph capture needs a non-null stream): ``launch`` enqueues the
+    kernels, ``capture`` records one launch into a HIP graph, ``replay``
+    launches that graph.  ``actions[k]`` is tenant ``tenants[k]``'s output,
+    rows in its arrival order."""
+
+    def __init__(self, model: Model, requests: Sequence[Request], tenants: Sequence[int], align: int = 1,
+                 device="cuda", stream=None):
+        import torch
+        self.model = model
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=device)
+        self.ctx = Context(self.stream)
+        self.tenants = list(tenants)
+        slot = {g: k for k, g in enumerate(self.tenants)}
+        self.requests = [Request(slot[r.tenant], r.embeds, r.lengths, r.max_len) for r in requests]
+        d = model.backbone.d
+        self.table = [Tenant(model.prefix_sig, d) for _ in self.tenants]
+        self.heads = [model.heads[g] for g in self.tenants]
+        if any(h is None for h in self.heads):
+            raise ValueError("InferStep serves MLP-head tenants")
+        self.actions = [torch.empty((int(sum(r.n for r in self.requests if r.tenant == k)), int(h.dims[-1])),
+                                    dtype=torch.float32, device=device) for k, h in enumerate(self.heads)]
+        nbytes = jn_infer_workspace_size(self.requests, self.table, d, align, model.backbone, self.heads)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        torch.cuda.synchronize()
+        self.plan = InferPlan(self.ctx, self.requests, self.table, d, align, model.backbone, self.heads,
+                              self.actions, self.ws)
+
+    def launch(self):
+        self.plan.launch()
+
+    def capture(self):
+        self.plan.capture()
+
+    def replay(self):
+        self.plan.replay()
+
+    def synchronize(self):
+        self.stream.synchronize()
 
 
 class TenantOptimizer:

@@ -261,6 +261,38 @@ def test_config3_sampled_end_to_end(jn):
     _say(f"  hidden {worst:.3e} on {len(keys)} samples, head grads {gw:.3e}")
 
 
+def test_split_k_short_batch_2b(jn):
+    """A one-sample batch on the 2B-shaped backbone: the O projection (K=2048)
+    and the down projection (K=16384) have too few tiles for the GPU and run
+    split over K (2 and 4 ranges, fp32 partials added in range order).  The
+    hidden rows match the oracle's isolated run of that sample, the head
+    stage matches stage-wise, and two runs are bitwise equal."""
+    import oracle
+    from paper_2607_16074_amd import Request
+    from paper_2607_16074_amd import step as jstep
+    import paper_2607_16074_amd._abi as abi  # noqa: F401
+    wl = W.make_workload(3)
+    model, reqs, targets = jstep.from_workload(wl)
+    one = [Request(reqs[0].tenant, reqs[0].embeds[:1], reqs[0].lengths[:1])]
+    g0 = reqs[0].tenant
+    _say(f"split-K: one sample of tenant {g0}, {int(one[0].lengths[0])} rows, 18-layer d2048")
+    st = jstep.GroupStep(model, one, {g0: targets[g0][:1]}, [g0])
+    st.run()
+    torch.cuda.synchronize()
+    h1 = st.hidden.clone()
+    st.run()
+    torch.cuda.synchronize()
+    assert torch.equal(h1, st.hidden)
+    ref = oracle.step.isolated(wl, samples=[(0, 0)], heads=False)
+    z = ref["hidden"][(0, 0)]
+    e = maxrel(bf16_np(st.hidden)[: z.shape[0]], z)
+    _say(f"  hidden max-rel {e:.3e}")
+    assert e < BF16_TOL
+    pooled = st.pooled.cpu().numpy().astype(np.float64)
+    tres = oracle.heads.tenant_step(pooled, wl.heads[g0], np.asarray(targets[g0][:1], np.float64))
+    assert rel_l2(st.ios[0].actions.cpu().numpy(), tres["actions"]) < GRAD_TOL
+
+
 def test_single_sample_of_length_one(jn):
     """The smallest batch: one tenant, one request, one sample of one token,
     padded to a canonical length of 4 (degenerate attention: softmax over one
