@@ -45,7 +45,8 @@ def isolated(wl, samples: Optional[Sequence[Tuple[int, int]]] = None,
     else:
         import workloads
         getw = lambda l: workloads.layer_weights(spec, l)  # noqa: E731
-    zs = bb.backbone_forward(xs, getw, b.layers, b.heads, b.glu, b.eps, wl.gf)
+    zs = bb.backbone_forward(xs, getw, b.layers, b.heads, b.glu, b.eps, wl.gf, b.kv_heads, b.causal,
+                             b.rope_theta)
     hidden = dict(zip(samples, zs))
     pooled = {k: bb.pool(z) for k, z in hidden.items()}
     out = {"hidden": hidden, "pooled": pooled, "tenants": {}}
@@ -88,19 +89,28 @@ def packed_block_diagonal(wl, align: int = 1) -> List[np.ndarray]:
     pos = np.concatenate([np.arange(x.shape[0]) for x in blocks])
     valid_key = pos < np.array(lens)[seg]
     mask = (seg[:, None] == seg[None, :]) & valid_key[None, :]
+    if b.causal:
+        mask &= pos[None, :] <= pos[:, None]
     x = np.concatenate(blocks)
     d, H = b.d, b.heads
     hdim = d // H
+    Hkv = b.kv_heads or H
+    kvw = Hkv * hdim
     for l in range(b.layers):
         lw = bb.LayerF64(wl.layers[l], b.glu)
         h = bb.rms_norm(x, lw.g1, b.eps)
         qkv = h @ lw.wqkv.T
+        q, k, v = qkv[:, :d], qkv[:, d:d + kvw], qkv[:, d + kvw:d + 2 * kvw]
+        if b.rope_theta > 0:  # positions within each sample (the physical row index would be wrong)
+            q = bb.rope(q, H, b.rope_theta, pos)
+            k = bb.rope(k, Hkv, b.rope_theta, pos)
         a = np.empty((x.shape[0], d))
         for hh in range(H):
             sl = slice(hh * hdim, (hh + 1) * hdim)
-            s = (qkv[:, sl] @ qkv[:, d:2 * d][:, sl].T) / np.sqrt(hdim)
+            kl = slice((hh // (H // Hkv)) * hdim, (hh // (H // Hkv) + 1) * hdim)
+            s = (q[:, sl] @ k[:, kl].T) / np.sqrt(hdim)
             s = np.where(mask, s, -np.inf)
-            a[:, sl] = bb.softmax_rows(s) @ qkv[:, 2 * d:][:, sl]
+            a[:, sl] = bb.softmax_rows(s) @ v[:, kl]
         x = x + a @ lw.wo.T
         h = bb.rms_norm(x, lw.g2, b.eps)
         m = bb.gelu(h @ lw.w_up.T) if lw.w_gate is None else bb.gelu(h @ lw.w_gate.T) * (h @ lw.w_up.T)

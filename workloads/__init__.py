@@ -63,10 +63,21 @@ class BackboneSpec:
     ffn: int
     glu: bool          # GeGLU MLP (gate and up projections) instead of GELU MLP
     eps: float = 1e-6  # RMSNorm epsilon
+    kv_heads: int = 0  # key/value heads (0: one per query head; 1: multi-query; else grouped)
+    causal: bool = False      # causal mask inside each sample instead of bidirectional
+    rope_theta: float = 0.0   # > 0: rotary embedding of q and k, positions restart in every sample
 
     @property
     def head_dim(self) -> int:
         return self.d // self.heads
+
+    @property
+    def n_kv(self) -> int:
+        return self.kv_heads or self.heads
+
+    @property
+    def qkv_rows(self) -> int:
+        return (self.heads + 2 * self.n_kv) * self.head_dim
 
 
 @dataclasses.dataclass(frozen=True)
@@ -119,7 +130,7 @@ class Workload:
     spec: WorkloadSpec
     requests: List[Request]
     # backbone weights, bf16 bits, [out][in] layout; per layer a dict
-    #   wqkv [3d, d] (rows: q then k then v, head-major inside each),
+    #   wqkv [(H + 2 Hkv) hd, d] (rows: q then k then v, head-major inside each),
     #   wo [d, d], w_up [f, d], w_gate [f, d] (GeGLU only), w_down [d, f],
     #   g1 [d], g2 [d]; plus final-norm gain gf [d]
     layers: List[dict]
@@ -140,6 +151,13 @@ class Workload:
 _BB_SMALL = BackboneSpec(layers=2, d=128, heads=4, ffn=512, glu=False)
 _BB_BASE = BackboneSpec(layers=12, d=768, heads=12, ffn=3072, glu=False)
 _BB_2B = BackboneSpec(layers=18, d=2048, heads=8, ffn=16384, glu=True)
+# Backbone variants on the 2B shapes: one key/value head and rotary positions
+# over a bidirectional prefix (a Gemma-style prefix encoder), and grouped
+# key/value heads with causal attention and rotary positions (a Qwen-style
+# decoder used as the prefix encoder).
+_BB_2B_MQA = BackboneSpec(layers=18, d=2048, heads=8, ffn=16384, glu=True, kv_heads=1, rope_theta=10000.0)
+_BB_2B_GQA = BackboneSpec(layers=18, d=2048, heads=16, ffn=16384, glu=True, kv_heads=2, causal=True,
+                          rope_theta=1000000.0)
 
 # Config 3's eight tenants cover every action_dim in {7,14,32} and chunk in {1,10,50}.
 _CFG3_SCHEMAS = ((7, 1), (7, 10), (7, 50), (14, 1), (14, 10), (14, 50), (32, 10), (32, 50))
@@ -226,6 +244,11 @@ def config_spec(cfg: int, seed: int = 0) -> WorkloadSpec:
             a, c = _CFG25_SCHEMAS[int(rng.integers(0, 4))]
             t.append(TenantSpec(per_tenant[g], 256 * cams, 16, 64, 256 * cams + 64, (768, 1024, a * c), a, c))
         return WorkloadSpec(5, _BB_BASE, tuple(t), seed, "32 tenants, Zipf(1.2) counts totalling 512")
+    if cfg in (6, 7):
+        t = tuple(TenantSpec(32, 256, 16, 64, 320, (2048, 1024, 1024, a * c), a, c) for a, c in _CFG3_SCHEMAS)
+        if cfg == 6:
+            return WorkloadSpec(6, _BB_2B_MQA, t, seed, "8 tenants x 32, 2B-shaped, 1 KV head, RoPE, bidirectional")
+        return WorkloadSpec(7, _BB_2B_GQA, t, seed, "8 tenants x 32, 2B-shaped, 16 heads / 2 KV heads, causal, RoPE")
     raise ValueError(f"unknown config {cfg}")
 
 
@@ -250,7 +273,7 @@ def layer_weights(spec: WorkloadSpec, layer: int) -> dict:
         return _normal_bf16(_rng(spec.seed, spec.config_id, _S_LAYER + 16 * layer + idx), shape, 0.02)
 
     out = {
-        "wqkv": w(0, (3 * d, d)),
+        "wqkv": w(0, (bb.qkv_rows, d)),
         "wo": w(1, (d, d)),
         "w_up": w(2, (f, d)),
         "w_down": w(4, (d, f)),
