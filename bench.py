@@ -72,7 +72,7 @@ def copy_calibration(mib: int = 512):
 def gemm_flops_per_token(bb) -> dict:
     d, f = bb.d, bb.ffn
     up = 2 * (2 * f if bb.glu else f) * d
-    return {"gemm_qkv": 2 * 3 * d * d, "gemm_o": 2 * d * d, "gemm_up": up, "gemm_down": 2 * f * d}
+    return {"gemm_qkv": 2 * bb.qkv_rows * d, "gemm_o": 2 * d * d, "gemm_up": up, "gemm_down": 2 * f * d}
 
 
 def time_steps(steps, fn, ctx, warmup):
@@ -265,7 +265,7 @@ def main():
         e = by_op.setdefault(op, {"ms": 0.0, "launches": 0})
         e["ms"] += ms
         e["launches"] += 1
-    bb_ms = sum(v["ms"] for k, v in by_op.items() if k in ("rmsnorm", "gemm_qkv", "attention", "gemm_o",
+    bb_ms = sum(v["ms"] for k, v in by_op.items() if k in ("rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o",
                                                           "gemm_up", "gemm_down")) / args.steps
     fpt = gemm_flops_per_token(spec.backbone)
     gemm_stats = {}

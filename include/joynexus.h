@@ -78,7 +78,7 @@ typedef enum jn_op {
   JN_OP_PACK = 1, JN_OP_RMSNORM = 2, JN_OP_GEMM_QKV = 3, JN_OP_ATTENTION = 4, JN_OP_GEMM_O = 5,
   JN_OP_GEMM_UP = 6, JN_OP_GEMM_DOWN = 7, JN_OP_POOL = 8, JN_OP_HEAD_FWD = 9, JN_OP_LOSS = 10,
   JN_OP_HEAD_BWD = 11, JN_OP_UNPACK = 12, JN_OP_EXPERT_GEMM = 13, JN_OP_EXPERT_ATTENTION = 14,
-  JN_OP_EXPERT_OTHER = 15, JN_OP_OPTIMIZER = 16
+  JN_OP_EXPERT_OTHER = 15, JN_OP_OPTIMIZER = 16, JN_OP_ROPE = 17
 } jn_op;
 
 /* One traced kernel launch.  For GEMMs (M, N, K) is the launch shape
@@ -192,8 +192,9 @@ jn_status jn_pack_group(jn_ctx* ctx, const jn_request* req, int32_t R, const jn_
 /* ------------------------------------------------------------ backbone --- */
 
 typedef struct jn_layer {
-  const void* wqkv;        /* bf16 [3d][d]: q rows, then k rows, then v rows;
-                              head h uses rows h*hd .. h*hd+hd-1 of each      */
+  const void* wqkv;        /* bf16 [(H + 2 Hkv) hd][d]: q rows, then k rows,
+                              then v rows (Hkv = H unless grouped); head h
+                              uses rows h*hd .. h*hd+hd-1 of each            */
   const void* wo;          /* bf16 [d][d]                                     */
   const void* w_up;        /* bf16 [f][d]                                     */
   const void* w_gate;      /* bf16 [f][d] for a GeGLU MLP, NULL for GELU MLP  */
@@ -205,16 +206,28 @@ typedef struct jn_layer {
 /* Frozen shared backbone: pre-RMSNorm transformer blocks
  *   h = RMS(x) g1; q,k,v = h Wqkv^T; x += Attn(q,k,v) Wo^T;
  *   h = RMS(x) g2; x += Wdown gelu(Wup h)   or   Wdown (gelu(Wgate h) * Wup h)
- * then z = RMS(x) gf.  Attention is bidirectional within a sample and never
- * crosses samples; RMS(x) = x / sqrt(mean(x^2) + eps); gelu is the tanh form.
+ * then z = RMS(x) gf.  Attention never crosses samples; it is bidirectional
+ * within a sample, or causal (row j sees rows 0..j of its sample) when
+ * `causal` is set.  RMS(x) = x / sqrt(mean(x^2) + eps); gelu is the tanh form.
+ * Variants of the VLM families the paper's tenants build on (Sec. 5.2):
+ *   n_kv_heads    0 (= n_heads) or a divisor of n_heads: query head h reads
+ *                 key/value head h / (n_heads / n_kv_heads); wqkv then has
+ *                 (n_heads + 2 n_kv_heads) * hd rows (q, then k, then v)
+ *   rope_theta    > 0: rotary embedding of q and k after the projection --
+ *                 for i < hd/2 the pair (x_i, x_{i+hd/2}) of a row at
+ *                 position p (its row inside its own sample, from 0) is
+ *                 rotated by p * rope_theta^(-2i/hd); 0: no positions
  * Arithmetic: bf16 GEMM / attention operands with fp32 accumulation, fp32
- * residual stream, fp32 norm / softmax statistics, bf16 stored activations. */
+ * residual stream, fp32 norm / softmax / rotation math, bf16 stored
+ * activations (q and k are stored rotated, rounded once more). */
 typedef struct jn_backbone {
   int32_t n_layers, d, n_heads, ffn;
   float eps;
-  int32_t reserved;
+  int32_t n_kv_heads;      /* 0 = n_heads                               */
   const jn_layer* layers;  /* host array [n_layers] of device pointers */
   const void* gf;          /* bf16 [d] final RMSNorm gain              */
+  int32_t causal;          /* 0 bidirectional, 1 causal                */
+  float rope_theta;        /* 0 = no rotary embedding                  */
 } jn_backbone;
 
 /* Workspace bytes jn_backbone_forward needs for a batch of T rows. */

@@ -202,10 +202,14 @@ def jn_pack_group(ctx: Context, reqs: Sequence[Request], tenants: Sequence[Tenan
 class Backbone:
     """Device weights of the frozen backbone (lists of torch bf16 tensors)."""
 
-    def __init__(self, layers: List[dict], gf, n_heads: int, eps: float):
+    def __init__(self, layers: List[dict], gf, n_heads: int, eps: float, n_kv_heads: int = 0, causal: bool = False,
+                 rope_theta: float = 0.0):
         self.layers = layers
         self.gf = gf
         self.n_heads = int(n_heads)
+        self.n_kv_heads = int(n_kv_heads)
+        self.causal = bool(causal)
+        self.rope_theta = float(rope_theta)
         self.eps = float(eps)
         self.d = int(gf.shape[0])
         self.ffn = int(layers[0]["w_up"].shape[0])
@@ -225,6 +229,9 @@ class Backbone:
         s.n_heads = self.n_heads
         s.ffn = self.ffn
         s.eps = self.eps
+        s.n_kv_heads = self.n_kv_heads
+        s.causal = 1 if self.causal else 0
+        s.rope_theta = self.rope_theta
         s.layers = C.cast(arr, C.POINTER(jn_layer))
         s.gf = _ptr(gf)
         self.struct = s

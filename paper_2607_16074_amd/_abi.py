@@ -35,7 +35,7 @@ EXPORTS = (
 
 OPS = {1: "pack", 2: "rmsnorm", 3: "gemm_qkv", 4: "attention", 5: "gemm_o", 6: "gemm_up", 7: "gemm_down",
        8: "pool", 9: "head_fwd", 10: "loss", 11: "head_bwd", 12: "unpack", 13: "expert_gemm",
-       14: "expert_attention", 15: "expert_other", 16: "optimizer"}
+       14: "expert_attention", 15: "expert_other", 16: "optimizer", 17: "rope"}
 
 
 class jn_trace_entry(C.Structure):
@@ -88,7 +88,8 @@ class jn_layer(C.Structure):
 
 class jn_backbone(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d", C.c_int32), ("n_heads", C.c_int32), ("ffn", C.c_int32),
-                ("eps", C.c_float), ("reserved", C.c_int32), ("layers", C.POINTER(jn_layer)), ("gf", C.c_void_p)]
+                ("eps", C.c_float), ("n_kv_heads", C.c_int32), ("layers", C.POINTER(jn_layer)), ("gf", C.c_void_p),
+                ("causal", C.c_int32), ("rope_theta", C.c_float)]
 
 
 class jn_head(C.Structure):

@@ -461,7 +461,9 @@ BbLayout bb_layout(const jn_backbone* bb, int64_t T) {
   L.mid = take(2 * T * f);
   // fp32 partials of the split-K launches (short batches only)
   const bool glu = bb->layers && bb->layers[0].w_gate != nullptr;
-  size_t sb = std::max(gemm_split_bytes(EPI_BF16, (int32_t)T, (int32_t)(3 * d), (int32_t)d),
+  const int64_t kvh = bb->n_kv_heads ? bb->n_kv_heads : bb->n_heads;
+  const int64_t nqkv = (bb->n_heads + 2 * kvh) * (d / bb->n_heads);
+  size_t sb = std::max(gemm_split_bytes(EPI_BF16, (int32_t)T, (int32_t)nqkv, (int32_t)d),
                        gemm_split_bytes(EPI_RESID_F32, (int32_t)T, (int32_t)d, (int32_t)d));
   sb = std::max(sb, gemm_split_bytes(EPI_RESID_F32, (int32_t)T, (int32_t)d, (int32_t)f));
   if (!glu) sb = std::max(sb, gemm_split_bytes(EPI_GELU_BF16, (int32_t)T, (int32_t)f, (int32_t)d));
@@ -482,6 +484,11 @@ jn_status check_backbone(jn_ctx* c, const jn_backbone* bb) {
   if (bb->d % 128 != 0) return fail(c, JN_EUNSUPPORTED, "d %d not a multiple of 128", bb->d);
   if (bb->ffn % 128 != 0) return fail(c, JN_EUNSUPPORTED, "ffn %d not a multiple of 128", bb->ffn);
   if (!(bb->eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
+  const int kv = bb->n_kv_heads ? bb->n_kv_heads : bb->n_heads;
+  if (kv < 1 || bb->n_heads % kv != 0)
+    return fail(c, JN_EINVAL, "n_kv_heads %d must divide n_heads %d", bb->n_kv_heads, bb->n_heads);
+  if (bb->causal != 0 && bb->causal != 1) return fail(c, JN_EINVAL, "causal must be 0 or 1");
+  if (!(bb->rope_theta >= 0.f) || std::isinf(bb->rope_theta)) return fail(c, JN_EINVAL, "rope_theta must be >= 0");
   bool glu = bb->layers[0].w_gate != nullptr;
   for (int l = 0; l < bb->n_layers; ++l) {
     const jn_layer& L = bb->layers[l];
@@ -526,6 +533,9 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
   void* sp = w + L.split;
   const size_t spb = L.split_bytes;
   const bool glu = bb->layers[0].w_gate != nullptr;
+  const int32_t hd = d / bb->n_heads;
+  const int32_t kvh = bb->n_kv_heads ? bb->n_kv_heads : bb->n_heads;
+  const int32_t nqkv = (bb->n_heads + 2 * kvh) * hd;  // q | k | v columns of the projection
   hipStream_t s = c->stream;
   for (int l = 0; l < bb->n_layers; ++l) {
     const jn_layer& Ly = bb->layers[l];
@@ -533,11 +543,14 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
       JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_bf16in(s, p->tokens, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
     else
       JN_TRACED(c, JN_OP_RMSNORM, T, d, 0, launch_rmsnorm_f32in(s, x, Ly.g1, h, T, d, bb->eps), "rmsnorm");
-    JN_TRACED(c, JN_OP_GEMM_QKV, T, 3 * d, d,
-              launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, 3 * d, T, 3 * d, d, 0, sp, spb), "gemm qkv");
+    JN_TRACED(c, JN_OP_GEMM_QKV, T, nqkv, d,
+              launch_gemm(s, EPI_BF16, h, d, Ly.wqkv, nullptr, d, qkv, nqkv, T, nqkv, d, 0, sp, spb), "gemm qkv");
+    if (bb->rope_theta > 0.f)
+      JN_TRACED(c, JN_OP_ROPE, T, (bb->n_heads + kvh) * hd, 0,
+                launch_rope(s, qkv, nqkv, p->token_pos, T, bb->n_heads + kvh, hd, bb->rope_theta), "rope");
     JN_TRACED(c, JN_OP_ATTENTION, T, d, bb->n_heads,
-              launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, p->max_seqlen,
-                               p->align),
+              launch_attention(s, qkv, att, p->seqlens, p->cu_seqlens, p->N, d, bb->n_heads, kvh, bb->causal != 0,
+                               p->max_seqlen, p->align),
               "attention");
     JN_TRACED(c, JN_OP_GEMM_O, T, d, d, launch_gemm(s, EPI_RESID_F32, att, d, Ly.wo, nullptr, d, x, d, T, d, d, 0, sp, spb),
               "gemm o");

@@ -89,11 +89,18 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
 int gemm_split(int epi, int32_t M, int32_t N, int32_t K);
 size_t gemm_split_bytes(int epi, int32_t M, int32_t N, int32_t K);
 
-// Varlen attention over the packed batch (bidirectional inside each sample).
-// qkv: bf16 [T][3d]; out: bf16 [T][d].  Alignment rows of `out` are zeroed.
+// Varlen attention over the packed batch (bidirectional or causal inside each
+// sample).  qkv: bf16 [T][(H + 2 Hkv) hd] (q | k | v); out: bf16 [T][d],
+// d = H hd.  Query head h reads key/value head h / (H / Hkv).  Alignment rows
+// of `out` are zeroed.
 hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int32_t* seqlens,
-                            const int32_t* cu_seqlens, int32_t N, int32_t d, int32_t n_heads,
-                            int32_t max_seqlen, int32_t align);
+                            const int32_t* cu_seqlens, int32_t N, int32_t d, int32_t n_heads, int32_t n_kv_heads,
+                            bool causal, int32_t max_seqlen, int32_t align);
+// In-place rotary embedding of the first `heads` head slices (hd wide) of
+// every row of qkv [T][ld] whose token_pos >= 0: pair (i, i + hd/2) rotated
+// by token_pos * theta^(-2i/hd).
+hipError_t launch_rope(hipStream_t s, void* qkv, int32_t ld, const int32_t* token_pos, int32_t T, int32_t heads,
+                       int32_t hd, float theta);
 
 // ---- heads ----
 // pooled[sample_tenant_rank[i]][:] = mean over valid rows of hidden for sample i

@@ -1,8 +1,11 @@
-// Segment-masked varlen attention over the packed batch (forward), gfx950.
+// Segment-masked varlen attention over the packed batch (forward), gfx950,
+// and the rotary position embedding applied to q and k before it.
 //
-// Every sample attends bidirectionally over its own valid rows only; nothing
-// crosses a sample (hence a tenant) boundary and alignment rows are neither
-// keys nor queries (their output rows are written as zero).
+// Every sample attends over its own valid rows only -- bidirectionally, or
+// causally (row j sees rows 0..j) -- nothing crosses a sample (hence a
+// tenant) boundary and alignment rows are neither keys nor queries (their
+// output rows are written as zero).  With fewer key/value heads than query
+// heads, query head h reads key/value head h / (H / Hkv).
 //
 // Work item = (sample, head, 128-query tile); a workgroup = 4 wavefronts x 32
 // query rows.  (sample, head) groups are dealt round-robin to the 8 XCDs
@@ -69,11 +72,22 @@ __device__ __forceinline__ void attn_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(N | (7 << 4) | (15 << 8) | (0 << 14));
 }
 
-template <int HD, int KB>
+struct AttnShape {
+  int32_t d;        // output row width = H * hd
+  int32_t ld;       // qkv row width = (H + 2 Hkv) * hd
+  int32_t kv_col;   // first key column (H * hd)
+  int32_t v_col;    // first value column ((H + Hkv) * hd)
+  int32_t n_kv;     // key/value heads
+  int32_t group;    // query heads per key/value head
+  int32_t qtiles;   // 128-query tiles per sample (of the longest sample)
+  int32_t total;    // (sample, key/value head) groups
+  float scale_log2;
+};
+
+template <int HD, int KB, bool CAUSAL>
 __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd_kernel(
     const uint16_t* __restrict__ qkv, uint16_t* __restrict__ out, const int32_t* __restrict__ seqlens,
-    const int32_t* __restrict__ cu_seqlens, int32_t d, int32_t n_heads, int32_t qtiles, int32_t total,
-    float scale_log2) {
+    const int32_t* __restrict__ cu_seqlens, AttnShape sh) {
   constexpr int CPR = HD / 8;            // 16-byte chunks per row
   constexpr int TILE = KB * HD;          // elements of one K (or V) tile
   constexpr int NDMA = 2 * TILE / 512;   // 1 KB DMA instructions per stage (K tile, then V tile)
@@ -86,17 +100,21 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
   static_assert(NDMA % 4 == 0 && KB % 32 == 0, "tile shape");
   __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2 * TILE];
 
-  // XCD-aware work mapping: (sample, head) group g goes to XCD g % 8, and
-  // its query tiles to consecutive slots of that XCD (block b runs on XCD
-  // b % 8, slot b / 8).  Groups interleave across XCDs, so samples of very
-  // different lengths spread evenly, while each group's keys and values are
-  // read by one XCD only.
+  // XCD-aware work mapping: (sample, key/value head) group g goes to XCD
+  // g % 8, and the query tiles of all its query heads to consecutive slots of
+  // that XCD (block b runs on XCD b % 8, slot b / 8).  Groups interleave
+  // across XCDs, so samples of very different lengths spread evenly, while
+  // each group's keys and values are read by one XCD only.
   const int32_t b = blockIdx.x;
   const int32_t slot = b >> 3;
-  const int32_t ih = (slot / qtiles) * 8 + (b & 7);
-  const int32_t qt = slot % qtiles;
-  if (ih >= total) return;
-  const int32_t h = ih % n_heads, i = ih / n_heads;
+  const int32_t units = sh.group * sh.qtiles;
+  const int32_t kg = (slot / units) * 8 + (b & 7);
+  if (kg >= sh.total) return;
+  const int32_t r_in = slot % units;
+  const int32_t qt = r_in % sh.qtiles;
+  const int32_t i = kg / sh.n_kv, kvh = kg % sh.n_kv;
+  const int32_t h = kvh * sh.group + r_in / sh.qtiles;
+  const int32_t d = sh.d;
   const int32_t L = seqlens[i];
   const int32_t base = cu_seqlens[i];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -112,10 +130,11 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
   const int32_t q0 = qt * kQRows;
   if (q0 >= L) return;
 
-  const int64_t ld = 3 * (int64_t)d;
+  const int64_t ld = sh.ld;
+  const float scale_log2 = sh.scale_log2;
   const uint16_t* Qg = qkv + h * HD;
-  const uint16_t* Kg = qkv + d + h * HD;
-  const uint16_t* Vg = qkv + 2 * d + h * HD;
+  const uint16_t* Kg = qkv + sh.kv_col + kvh * HD;
+  const uint16_t* Vg = qkv + sh.v_col + kvh * HD;
 
   // this wave's DMA instructions u = wave*DPW + k fill 1 KB each; lane ->
   // row (v*RPI + lane / CPR) of the K or V tile, physical chunk lane % CPR,
@@ -161,13 +180,16 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
   const int hi4 = half * 4;
 
   issue_stage(0, 0);
-  const int32_t nsteps = (L + KB - 1) / KB;
+  // causal: keys past the tile's last query are never needed
+  const int32_t kend = CAUSAL ? min(L, q0 + kQRows) : L;
+  const int32_t nsteps = (kend + KB - 1) / KB;
   for (int32_t jstep = 0; jstep < nsteps; ++jstep) {
     const int32_t kb = jstep * KB;
     attn_wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();  // step j's tiles landed; step j-1's buffer is free
     if (jstep + 1 < nsteps) issue_stage(kb + KB, (jstep + 1) & 1);
     if (!active) continue;
+    if (CAUSAL && kb > qw + 31) continue;  // every key of the step is later than the wave's queries
     const uint16_t* Ks = &lds[jstep & 1][0];
     const uint16_t* Vs = &lds[jstep & 1][TILE];
 
@@ -190,13 +212,14 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
     // whichever m was used.  Keys past the sample are masked in the last step
     // only (wave-uniform branch).
     float mloc = -INFINITY;
-    if (kb + KB > L) {
+    if (kb + KB > L || (CAUSAL && kb + KB - 1 > qw)) {
+      const int32_t qlane = qw + (lane & 31);
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int32_t key = kb + kt * 32 + (r >> 2) * 8 + hi4 + (r & 3);
-          if (key >= L) s[kt][r] = -INFINITY;
+          if (key >= L || (CAUSAL && key > qlane)) s[kt][r] = -INFINITY;
         }
     }
 #pragma unroll
@@ -266,26 +289,83 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
 }
 
 hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int32_t* seqlens,
-                            const int32_t* cu_seqlens, int32_t N, int32_t d, int32_t n_heads, int32_t max_seqlen,
-                            int32_t align) {
+                            const int32_t* cu_seqlens, int32_t N, int32_t d, int32_t n_heads, int32_t n_kv_heads,
+                            bool causal, int32_t max_seqlen, int32_t align) {
   (void)align;
   const int hd = d / n_heads;
-  const int32_t qtiles = (max_seqlen + kQRows - 1) / kQRows;
-  const int64_t total = (int64_t)N * n_heads;  // (sample, head) groups
-  const int64_t blocks = (total + 7) / 8 * 8 * qtiles;
+  const int32_t kv = n_kv_heads > 0 ? n_kv_heads : n_heads;
+  if (kv < 1 || n_heads % kv != 0) return hipErrorInvalidValue;
+  AttnShape sh;
+  sh.d = d;
+  sh.ld = (n_heads + 2 * kv) * hd;
+  sh.kv_col = n_heads * hd;
+  sh.v_col = (n_heads + kv) * hd;
+  sh.n_kv = kv;
+  sh.group = n_heads / kv;
+  sh.qtiles = (max_seqlen + kQRows - 1) / kQRows;
+  const int64_t total = (int64_t)N * kv;
+  const int64_t blocks = (total + 7) / 8 * 8 * sh.group * sh.qtiles;
   if (total <= 0 || blocks > (1LL << 30)) return hipErrorInvalidValue;
+  sh.total = (int32_t)total;
+  sh.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   const dim3 grid((unsigned)blocks);
-  const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   auto Q = reinterpret_cast<const uint16_t*>(qkv);
   auto O = reinterpret_cast<uint16_t*>(out);
-  const int32_t tot = (int32_t)total;
+#define JN_ATTN(HDV)                                                                        \
+  case HDV:                                                                                 \
+    if (causal)                                                                             \
+      attn_fwd_kernel<HDV, kKeys, true><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, sh);  \
+    else                                                                                    \
+      attn_fwd_kernel<HDV, kKeys, false><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, sh); \
+    break;
   switch (hd) {
-    case 32: attn_fwd_kernel<32, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
-    case 64: attn_fwd_kernel<64, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
-    case 128: attn_fwd_kernel<128, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
-    case 256: attn_fwd_kernel<256, kKeys><<<grid, 256, 0, s>>>(Q, O, seqlens, cu_seqlens, d, n_heads, qtiles, tot, scale_log2); break;
-    default: return hipErrorInvalidValue;
+    JN_ATTN(32)
+    JN_ATTN(64)
+    JN_ATTN(128)
+    JN_ATTN(256)
+    default:
+      return hipErrorInvalidValue;
   }
+#undef JN_ATTN
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ rope ---
+// Rotary embedding in place on the q and k head slices of qkv (bf16).  One
+// block per row; a thread owns two adjacent pairs (2j, 2j+1) of the row's
+// rotation and applies them to a strided subset of its heads, so each sine /
+// cosine is computed once per row.  Angles in fp32: p * theta^(-2i/hd).
+__global__ __launch_bounds__(256) void rope_kernel(uint16_t* __restrict__ qkv, int32_t ld,
+                                                   const int32_t* __restrict__ token_pos, int32_t heads,
+                                                   int32_t hd, float log2_theta) {
+  const int32_t t = blockIdx.x;
+  const int32_t pos = token_pos[t];
+  if (pos < 0) return;  // alignment row
+  const int32_t half = hd >> 1, q4 = hd >> 2;
+  const int32_t j = threadIdx.x % q4, hg = threadIdx.x / q4, hstep = 256 / q4;
+  if (hg >= hstep) return;
+  float c[2], sn[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const float inv_freq = exp2f(-(float)(2 * (2 * j + e)) / (float)hd * log2_theta);
+    sincosf((float)pos * inv_freq, &sn[e], &c[e]);
+  }
+  uint16_t* row = qkv + (int64_t)t * ld;
+  for (int32_t h = hg; h < heads; h += hstep) {
+    uint32_t* pa = reinterpret_cast<uint32_t*>(row + h * hd + 2 * j);
+    uint32_t* pb = reinterpret_cast<uint32_t*>(row + h * hd + half + 2 * j);
+    const uint32_t wa = *pa, wb = *pb;
+    const float a0 = __uint_as_float(wa << 16), a1 = __uint_as_float(wa & 0xffff0000u);
+    const float b0 = __uint_as_float(wb << 16), b1 = __uint_as_float(wb & 0xffff0000u);
+    *pa = pack_bf2(a0 * c[0] - b0 * sn[0], a1 * c[1] - b1 * sn[1]);
+    *pb = pack_bf2(b0 * c[0] + a0 * sn[0], b1 * c[1] + a1 * sn[1]);
+  }
+}
+
+hipError_t launch_rope(hipStream_t s, void* qkv, int32_t ld, const int32_t* token_pos, int32_t T, int32_t heads,
+                       int32_t hd, float theta) {
+  if (T < 1 || heads < 1 || hd % 4 != 0 || hd / 4 > 256 || !(theta > 0.f)) return hipErrorInvalidValue;
+  rope_kernel<<<T, 256, 0, s>>>(reinterpret_cast<uint16_t*>(qkv), ld, token_pos, heads, hd, log2f(theta));
   return hipGetLastError();
 }
 

@@ -54,13 +54,14 @@ class Model:
     @classmethod
     def from_arrays(cls, layers: List[dict], gf: np.ndarray, n_heads: int, eps: float,
                     heads: List[Optional[list]], tenant_meta: List[dict], prefix_sig: int, device="cuda",
-                    experts: Optional[List[Optional[dict]]] = None):
+                    experts: Optional[List[Optional[dict]]] = None, n_kv_heads: int = 0, causal: bool = False,
+                    rope_theta: float = 0.0):
         """``layers``: per layer dict of bf16 bit arrays; ``heads``: per tenant
         list of (W fp32 [out,in], b fp32 [out]) or None; ``experts``: per
         tenant None or a dict of bf16 bit arrays (w_in, w_out, gf, layers)
         with ``tenant_meta[g]["expert_heads"]`` attention heads."""
         dl = [{k: _dev_bf16(v, device) for k, v in L.items()} for L in layers]
-        bb = Backbone(dl, _dev_bf16(gf, device), n_heads, eps)
+        bb = Backbone(dl, _dev_bf16(gf, device), n_heads, eps, n_kv_heads, causal, rope_theta)
         hs, xs = [], []
         for g, layers_g in enumerate(heads):
             if layers_g is None:
@@ -277,8 +278,9 @@ def from_workload(wl, device="cuda", with_noisy: bool = False):
     spec = wl.spec
     meta = [{"action_dim": t.action_dim, "chunk": t.chunk,
              "expert_heads": t.expert[2] if t.expert is not None else 0} for t in spec.tenants]
-    model = Model.from_arrays(wl.layers, wl.gf, spec.backbone.heads, spec.backbone.eps, wl.heads, meta,
-                              spec.tenants[0].schema_sig, device, getattr(wl, "experts", None))
+    b = spec.backbone
+    model = Model.from_arrays(wl.layers, wl.gf, b.heads, b.eps, wl.heads, meta, spec.tenants[0].schema_sig, device,
+                              getattr(wl, "experts", None), b.kv_heads, b.causal, b.rope_theta)
     reqs = [Request(r.tenant, _dev_bf16(r.embeds, device), r.lengths) for r in wl.requests]
     targets, noisy = {}, {}
     for g in range(spec.G):

@@ -1,0 +1,157 @@
+"""GPU parity of the backbone variants against the fp64 oracle: causal masks,
+rotary positions that restart in every sample (read from the pack's
+token_pos map), and grouped / multi-query key-value heads, at every head
+width the attention kernel implements, with lengths spanning several query
+tiles and key steps and a ragged tail.  Bars as for the base backbone:
+hidden rows within 2e-2 max-relative per sample, head stage-wise at 1e-3;
+grouped == isolated bitwise."""
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+GRAD_TOL = 1e-3
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def jn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_16074_amd as lib
+    return lib
+
+
+def maxrel(g, o):
+    return float(np.max(np.abs(np.asarray(g, np.float64) - o)) / max(np.max(np.abs(o)), 1e-30))
+
+
+def rel_l2(g, o):
+    o = np.asarray(o, np.float64)
+    return float(np.linalg.norm(np.asarray(g, np.float64) - o) / max(np.linalg.norm(o), 1e-30))
+
+
+def bf16_np(t):
+    return W.bf16_bits_to_f32(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+
+
+def spec_of(d, heads, kv, causal, theta, ns=(3, 2, 2), lo=1, hi=300, max_len=300, layers=2, glu=False):
+    ten = tuple(W.TenantSpec(n, 0, lo, hi, max_len, (d, 64, 6), 3, 2) for n in ns)
+    bbs = W.BackboneSpec(layers, d, heads, 256, glu, kv_heads=kv, causal=causal, rope_theta=theta)
+    return W.WorkloadSpec(91, bbs, ten, 0, "variant")
+
+
+def run(wl, align=1, tenants=None):
+    from paper_2607_16074_amd import step as jstep
+    model, reqs, targets = jstep.from_workload(wl)
+    st = jstep.GroupStep(model, reqs, targets, list(range(wl.spec.G)) if tenants is None else tenants, align)
+    st.run()
+    torch.cuda.synchronize()
+    return st
+
+
+def check(wl, st, keys=None):
+    import oracle
+    iso = oracle.step.isolated(wl, samples=keys, heads=False)
+    hid = bf16_np(st.hidden)
+    cu = st.packed.map_tensor("cu_seqlens").cpu().numpy()
+    flat = [(r, s) for r, q in enumerate(wl.requests) for s in range(q.n)]
+    worst = 0.0
+    for i, key in enumerate(flat):
+        if key not in iso["hidden"]:
+            continue
+        z = iso["hidden"][key]
+        e = maxrel(hid[cu[i]: cu[i] + z.shape[0]], z)
+        worst = max(worst, e)
+        assert e < BF16_TOL, (key, e)
+        assert not hid[cu[i] + z.shape[0]: cu[i + 1]].any()
+    pooled = st.pooled.cpu().numpy().astype(np.float64)
+    off = 0
+    for k, g in enumerate(st.tenants):
+        n = sum(q.n for q in wl.requests if q.tenant == g)
+        ref = oracle.step.tenant_from_pooled(wl, g, pooled[off: off + n])
+        off += n
+        assert rel_l2(st.ios[k].actions.cpu().numpy(), ref["actions"]) < GRAD_TOL
+        for j, (dW, db) in enumerate(ref["grads"]):
+            assert rel_l2(st.ios[k].dW[j].cpu().numpy(), dW) < GRAD_TOL, (g, j)
+    return worst
+
+
+CASES = [  # d, heads, kv heads, causal, rope theta  ->  head widths 32, 64, 128, 256
+    (128, 4, 4, True, 10000.0),
+    (256, 4, 2, True, 10000.0),
+    (256, 4, 1, False, 500.0),
+    (256, 2, 1, True, 0.0),
+    (512, 2, 1, False, 10000.0),
+    (512, 2, 2, True, 1000000.0),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"d{c[0]}h{c[1]}kv{c[2]}{'c' if c[3] else 'b'}r{int(c[4])}" for c in CASES])
+def test_variant_backbone(jn, case):
+    d, H, kv, causal, theta = case
+    wl = W.make_workload(spec_of(d, H, kv, causal, theta), request_split=(2, 1, 2), request_order=[1, 3, 0, 4, 2])
+    _say(f"variant d={d} heads={H} kv={kv} causal={causal} theta={theta}: "
+         f"lengths {[int(x) for q in wl.requests for x in q.lengths]}")
+    st = run(wl, align=16 if causal else 1)
+    worst = check(wl, st)
+    _say(f"  hidden max-rel {worst:.3e}")
+
+
+def test_variant_grouped_equals_isolated_bitwise(jn):
+    """Rotary positions come from each sample's own rows, so a sample's
+    result does not depend on where the pack put it."""
+    from paper_2607_16074_amd import step as jstep
+    wl = W.make_workload(spec_of(256, 4, 2, True, 10000.0, ns=(4, 3, 2), hi=200, max_len=200))
+    _say("variant grouped == isolated")
+    model, reqs, targets = jstep.from_workload(wl)
+    grouped = jstep.GroupStep(model, reqs, targets, list(range(wl.spec.G)))
+    grouped.run()
+    iso = jstep.isolated_runs(model, reqs, targets, list(range(wl.spec.G)), ctx=grouped.ctx)
+    for s in iso:
+        s.run()
+    torch.cuda.synchronize()
+    off = 0
+    for g, s in enumerate(iso):
+        assert torch.equal(grouped.pooled[off: off + s.N], s.pooled), g
+        assert torch.equal(grouped.ios[g].loss, s.ios[0].loss), g
+        off += s.N
+
+
+@pytest.mark.parametrize("cfg", [6, 7])
+def test_variant_2b_sampled(jn, cfg):
+    """The 2B-shaped variants at full size in the benchmark's launch
+    configuration; the oracle runs the first sample of the first tenant."""
+    wl = W.make_workload(cfg)
+    _say(f"config {cfg}: {wl.spec.name}")
+    st = run(wl)
+    worst = check(wl, st, keys=[(0, 0)])
+    _say(f"  hidden max-rel {worst:.3e}")
+
+
+def test_variant_errors(jn):
+    from paper_2607_16074_amd import step as jstep
+    wl = W.make_workload(spec_of(256, 4, 2, True, 10000.0, ns=(2, 1, 1), hi=40, max_len=40))
+    model, reqs, targets = jstep.from_workload(wl)
+    bb = model.backbone
+    st = jstep.GroupStep(model, reqs, targets, [0, 1, 2])
+    for field, val in (("n_kv_heads", 3), ("causal", 2), ("rope_theta", -1.0)):
+        old = getattr(bb.struct, field)
+        setattr(bb.struct, field, val)
+        st.hidden.fill_(7)
+        torch.cuda.synchronize()
+        with pytest.raises(jn.JNError):
+            st.backbone()
+        torch.cuda.synchronize()
+        assert bool((st.hidden == 7).all())
+        setattr(bb.struct, field, old)
