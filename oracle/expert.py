@@ -21,6 +21,14 @@ fp64.  That is the GPU's precision contract, so parity of gradients can be
 checked at 1e-3 relative L2; with ``rnd=False`` the whole expert is
 plain fp64 (pinned against finite differences).
 
+Flow-matching objective (the GR00T / pi0.5-style training of such experts):
+per sample a flow time tau in (0, 1) and noise eps of the action chunk's
+shape are given; the expert's input is the point x = tau eps + (1 - tau) A
+on the straight path from the clean actions A to the noise, its regression
+target is that path's velocity dx/dtau = eps - A, and every action token's
+embedding receives W_time phi(tau), with phi(tau) the sinusoidal features
+sin(1000 tau w_j), cos(1000 tau w_j), w_j = 10000^(-j / (D/2)), j < D/2.
+
 Implemented with torch float64 CPU tensors and autograd for the chain rule
 (a library primitive; the custom ``Linear`` only decides rounding points).
 """
@@ -103,14 +111,32 @@ def _attn(q, k, v, heads):
     return torch.cat(out, dim=1)
 
 
+def time_features(tau: float, dim: int) -> np.ndarray:
+    """phi(tau) [dim]: sin(1000 tau w_j) for j < dim/2, then cos(1000 tau w_j),
+    w_j = 10000^(-j / (dim/2))."""
+    half = dim // 2
+    w = 10000.0 ** (-np.arange(half, dtype=np.float64) / half)
+    ang = 1000.0 * float(tau) * w
+    return np.concatenate([np.sin(ang), np.cos(ang)])
+
+
+def flow_inputs(tau: float, noise: np.ndarray, actions: np.ndarray):
+    """(x, v): the point tau * noise + (1 - tau) * actions of the straight path
+    and its velocity d x / d tau = noise - actions."""
+    e = np.asarray(noise, np.float64)
+    a = np.asarray(actions, np.float64)
+    return float(tau) * e + (1.0 - float(tau)) * a, e - a
+
+
 def expert_params(w: dict) -> Dict[str, torch.Tensor]:
     """fp64 leaf tensors (requires_grad) from an expert weight dict of bf16
     bit arrays: w_in [d][a], w_out [a][d], gf [d], and per layer
     wqkv_s [3d][d], wo_s [d][d], wq_c [d][d], wkv_c [2d][dp], wo_c [d][d],
     w_up [f][d], w_down [d][f], g1, g2, g3 [d]."""
     P = {}
-    for k in ("w_in", "w_out", "gf"):
-        P[k] = torch.tensor(bf16_to_f64(w[k]), requires_grad=True)
+    for k in ("w_in", "w_out", "gf", "w_time"):
+        if k in w:
+            P[k] = torch.tensor(bf16_to_f64(w[k]), requires_grad=True)
     for l, lw in enumerate(w["layers"]):
         for k, v in lw.items():
             P[f"{l}.{k}"] = torch.tensor(bf16_to_f64(v), requires_grad=True)
@@ -118,14 +144,18 @@ def expert_params(w: dict) -> Dict[str, torch.Tensor]:
 
 
 def expert_forward(P, n_layers: int, heads: int, eps: float, u: Sequence[np.ndarray],
-                   z: Sequence[np.ndarray], rnd: bool) -> List[torch.Tensor]:
-    """Predictions [chunk, a] of every sample.  ``u[i]``: its noisy action
-    tokens [chunk, a] (fp32); ``z[i]``: its valid backbone rows [len_i, dp]
-    (bf16 bits or floats)."""
+                   z: Sequence[np.ndarray], rnd: bool, taus: Sequence[float] = None) -> List[torch.Tensor]:
+    """Predictions [chunk, a] of every sample.  ``u[i]``: its input action
+    tokens [chunk, a]; ``z[i]``: its valid backbone rows [len_i, dp] (bf16 bits
+    or floats); ``taus[i]`` (flow matching): its flow time, whose features
+    phi(tau) projected by ``w_time`` are added to every token's embedding."""
     preds = []
-    for ui, zi in zip(u, z):
+    for i, (ui, zi) in enumerate(zip(u, z)):
         zt = torch.tensor(bf16_to_f64(zi) if zi.dtype == np.uint16 else np.asarray(zi, np.float64))
         x = linear(_q(torch.tensor(np.asarray(ui, np.float64)), rnd), P["w_in"], rnd)
+        if taus is not None:
+            phi = np.tile(time_features(taus[i], P["w_time"].shape[1]), (np.asarray(ui).shape[0], 1))
+            x = x + linear(_q(torch.tensor(phi), rnd), P["w_time"], rnd)
         for l in range(n_layers):
             g = lambda k: P[f"{l}.{k}"]  # noqa: E731
             d = x.shape[1]
@@ -146,14 +176,21 @@ def expert_forward(P, n_layers: int, heads: int, eps: float, u: Sequence[np.ndar
     return preds
 
 
-def expert_step(w: dict, n_layers: int, heads: int, eps: float, u, z, targets, rnd: bool = False) -> Dict:
+def expert_step(w: dict, n_layers: int, heads: int, eps: float, u, z, targets, rnd: bool = False,
+                flow_t=None) -> Dict:
     """Forward, the tenant's MSE loss and the gradient of every parameter.
 
-    ``targets``: [n, chunk, a].  Returns {"pred": [n, chunk, a] fp64,
-    "loss": float, "grads": {name: fp64 array}} with names as in
-    ``expert_params``."""
+    ``targets``: [n, chunk, a].  With ``flow_t`` ([n] flow times), ``u`` is
+    the noise and ``targets`` the clean actions: the expert reads
+    ``flow_inputs`` and regresses the path velocity (flow matching).
+    Returns {"pred": [n, chunk, a] fp64, "loss": float, "grads": {name: fp64
+    array}} with names as in ``expert_params``."""
     P = expert_params(w)
-    preds = expert_forward(P, n_layers, heads, eps, u, z, rnd)
+    if flow_t is not None:
+        pairs = [flow_inputs(flow_t[i], u[i], targets[i]) for i in range(len(u))]
+        u = [x for x, _ in pairs]
+        targets = np.stack([v for _, v in pairs])
+    preds = expert_forward(P, n_layers, heads, eps, u, z, rnd, None if flow_t is None else list(flow_t))
     Y = torch.stack(preds)
     T = torch.tensor(np.asarray(targets, np.float64)).reshape(Y.shape)
     loss = torch.mean((Y - T) ** 2)

@@ -102,6 +102,9 @@ class WorkloadSpec:
     tenants: Tuple[TenantSpec, ...]
     seed: int = 0
     name: str = ""
+    # action-expert tenants trained with the flow-matching objective: width of
+    # the sinusoidal flow-time features (0 = plain regression on the inputs)
+    flow_time_dim: int = 0
 
     @property
     def G(self) -> int:
@@ -142,6 +145,10 @@ class Workload:
     # per tenant (action-expert tenants only, else None): expert weights, noisy actions
     experts: List[Optional[dict]] = dataclasses.field(default_factory=list)
     noisy: List[Optional[np.ndarray]] = dataclasses.field(default_factory=list)
+    # flow matching (flow_time_dim > 0): per tenant flow times [n] fp32; ``noisy``
+    # then holds the noise, ``targets`` the clean actions, and each expert dict
+    # a ``w_time`` [d][flow_time_dim]
+    flow_t: List[Optional[np.ndarray]] = dataclasses.field(default_factory=list)
 
 
 # --------------------------------------------------------------------------
@@ -179,6 +186,8 @@ _S_HEAD = 500_000        # + 16*tenant + layer
 _S_TGT = 600_000         # + tenant
 _S_EXP = 700_000         # + 64*tenant + tensor index
 _S_NOISE = 900_000       # + tenant
+_S_FLOW = 950_000        # + tenant: flow times
+_S_TIME = 970_000        # + tenant: flow-time projection
 
 
 def zipf_counts(total: int, n_ranks: int, s: float) -> List[int]:
@@ -249,6 +258,11 @@ def config_spec(cfg: int, seed: int = 0) -> WorkloadSpec:
         if cfg == 6:
             return WorkloadSpec(6, _BB_2B_MQA, t, seed, "8 tenants x 32, 2B-shaped, 1 KV head, RoPE, bidirectional")
         return WorkloadSpec(7, _BB_2B_GQA, t, seed, "8 tenants x 32, 2B-shaped, 16 heads / 2 KV heads, causal, RoPE")
+    if cfg == 8:
+        # the 16 heterogeneous tenants of config 4 (same draws), their experts
+        # trained with the flow-matching objective
+        return dataclasses.replace(config_spec(4, seed), flow_time_dim=1024,
+                                   name="16 heterogeneous tenants, flow-matching action experts")
     raise ValueError(f"unknown config {cfg}")
 
 
@@ -344,6 +358,19 @@ def draw_noisy_actions(spec: WorkloadSpec, tenant: int) -> np.ndarray:
     return rng.standard_normal((t.n_samples, t.chunk, t.action_dim), dtype=np.float32)
 
 
+def draw_flow_times(spec: WorkloadSpec, tenant: int) -> np.ndarray:
+    """fp32 [n]: flow times 0.001 + 0.999 * Beta(1.5, 1), one per sample."""
+    t = spec.tenants[tenant]
+    rng = _rng(spec.seed, spec.config_id, _S_FLOW + tenant)
+    return (0.001 + 0.999 * rng.beta(1.5, 1.0, size=t.n_samples)).astype(np.float32)
+
+
+def time_weights(spec: WorkloadSpec, tenant: int) -> np.ndarray:
+    """bf16 [d][flow_time_dim] ~N(0, 0.02): the flow-time projection."""
+    d = spec.tenants[tenant].expert[1]
+    return _normal_bf16(_rng(spec.seed, spec.config_id, _S_TIME + tenant), (d, spec.flow_time_dim), 0.02)
+
+
 def draw_targets(spec: WorkloadSpec, tenant: int) -> np.ndarray:
     t = spec.tenants[tenant]
     rng = _rng(spec.seed, spec.config_id, _S_TGT + tenant)
@@ -386,7 +413,13 @@ def make_workload(spec_or_cfg, seed: int = 0, with_weights: bool = True,
     targets = [draw_targets(spec, g) for g in range(G)]
     experts = [expert_weights(spec, g) if spec.tenants[g].expert is not None else None for g in range(G)]
     noisy = [draw_noisy_actions(spec, g) if spec.tenants[g].expert is not None else None for g in range(G)]
-    return Workload(spec, requests, layers, gf, heads, targets, experts, noisy)
+    flow = spec.flow_time_dim > 0
+    flow_t = [draw_flow_times(spec, g) if flow and spec.tenants[g].expert is not None else None for g in range(G)]
+    if flow:
+        for g in range(G):
+            if experts[g] is not None:
+                experts[g]["w_time"] = time_weights(spec, g)
+    return Workload(spec, requests, layers, gf, heads, targets, experts, noisy, flow_t)
 
 
 def tenant_rows(wl: Workload, tenant: int) -> List[Tuple[int, int]]:
