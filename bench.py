@@ -117,8 +117,9 @@ def cpu_oracle_baseline(wl, budget_s=25.0):
         from oracle import expert as oexpert
         L_e, _, H_e, _ = ten.expert
         z = res["hidden"][key]
+        ft = wl.flow_t[req.tenant] if getattr(wl, "flow_t", None) else None
         oexpert.expert_step(wl.experts[req.tenant], L_e, H_e, wl.spec.backbone.eps, [wl.noisy[req.tenant][0]], [z],
-                            wl.targets[req.tenant][:1])
+                            wl.targets[req.tenant][:1], flow_t=None if ft is None else ft[:1])
         what = "its tenant's action-expert fwd/loss/grad for that sample"
     dt = time.perf_counter() - t0
     L = int(req.lengths[0])
@@ -251,7 +252,8 @@ def main():
         return
     G = spec.G
     experts = spec.tenants[0].expert is not None
-    grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align, noisy=noisy)
+    flow = jstep.flow_times(wl)
+    grouped = jstep.GroupStep(model, reqs, targets, list(range(G)), args.align, noisy=noisy, flow_t=flow)
     torch.cuda.synchronize()
     N, valid = grouped.N, grouped.valid_tokens
     log(f"N={N} samples, {valid} valid tokens, T={grouped.T} packed rows")
@@ -289,7 +291,8 @@ def main():
 
     iso_ms = None
     if not args.no_isolated:
-        iso = jstep.isolated_runs(model, reqs, targets, list(range(G)), args.align, ctx=grouped.ctx, noisy=noisy)
+        iso = jstep.isolated_runs(model, reqs, targets, list(range(G)), args.align, ctx=grouped.ctx, noisy=noisy,
+                                  flow_t=flow)
         torch.cuda.synchronize()
 
         def run_iso():

@@ -307,6 +307,16 @@ typedef struct jn_expert {
   const void* w_out;    /* [action_dim][d] */
   const void* gf;       /* [d]             */
   const jn_expert_layer* layers;  /* host [n_layers] */
+  /* Flow matching (the GR00T / pi0.5-style objective of such experts): with
+   * w_time set, the expert reads the point x = t*noise + (1-t)*actions of the
+   * straight path from the clean actions to the noise, every action token's
+   * embedding receives w_time phi(t), phi(t) = [sin(1000 t w_j) | cos(1000 t
+   * w_j)], w_j = 10000^(-j/(d_time/2)), j < d_time/2, and the regression
+   * target is the path's velocity noise - actions.  NULL: plain regression
+   * of `targets` from `noisy`. */
+  const void* w_time;   /* [d][d_time] or NULL                     */
+  int32_t d_time;       /* even, a multiple of 64, when w_time set */
+  int32_t reserved;
 } jn_expert;
 
 /* fp32 gradient outputs, same shapes as the weights they belong to. */
@@ -326,6 +336,11 @@ typedef struct jn_expert_io {
   float* dw_out;          /* out: fp32 [action_dim][d]                     */
   float* dgf;             /* out: fp32 [d]                                 */
   const jn_expert_layer_grads* layers;  /* host [n_layers] of device outputs */
+  /* flow matching (expert w_time set): `noisy` holds the noise, `targets` the
+   * clean actions, flow_t the per-sample flow times; dw_time receives the
+   * gradient of w_time.  Both NULL otherwise. */
+  const float* flow_t;    /* device fp32 [n], tenant arrival order         */
+  float* dw_time;         /* out: fp32 [d][d_time]                         */
 } jn_expert_io;
 
 jn_status jn_experts_workspace_size(const jn_packed* p, const jn_expert* ex, const jn_expert_io* io, int32_t G,

@@ -324,8 +324,9 @@ class Expert:
     """A tenant's action expert: device bf16 tensors w_in [d, a], w_out [a, d],
     gf [d] and per layer a dict with the keys of ``EXPERT_LAYER_FIELDS``."""
 
-    def __init__(self, w_in, w_out, gf, layers: List[dict], n_heads: int, chunk: int, d_prefix: int, eps: float):
-        self.w_in, self.w_out, self.gf, self.layers = w_in, w_out, gf, layers
+    def __init__(self, w_in, w_out, gf, layers: List[dict], n_heads: int, chunk: int, d_prefix: int, eps: float,
+                 w_time=None):
+        self.w_in, self.w_out, self.gf, self.layers, self.w_time = w_in, w_out, gf, layers, w_time
         s = jn_expert()
         s.n_layers = len(layers)
         s.d = int(w_in.shape[0])
@@ -336,6 +337,9 @@ class Expert:
         s.d_prefix = int(d_prefix)
         s.eps = float(eps)
         s.w_in, s.w_out, s.gf = _ptr(w_in), _ptr(w_out), _ptr(gf)
+        if w_time is not None:  # flow matching: [d, d_time] flow-time projection
+            s.w_time = _ptr(w_time)
+            s.d_time = int(w_time.shape[1])
         self._layers = (jn_expert_layer * len(layers))(
             *[jn_expert_layer(*[_ptr(lw[k]) for k in EXPERT_LAYER_FIELDS]) for lw in layers])
         s.layers = C.cast(self._layers, C.POINTER(jn_expert_layer))
@@ -348,14 +352,16 @@ class ExpertIO:
     a dict of gradients keyed as ``EXPERT_LAYER_FIELDS``."""
 
     def __init__(self, n_samples: int, prefix_rows: int, noisy, targets, pred, loss, dw_in, dw_out, dgf,
-                 layers: List[dict]):
+                 layers: List[dict], flow_t=None, dw_time=None):
         self.noisy, self.targets, self.pred, self.loss = noisy, targets, pred, loss
         self.dw_in, self.dw_out, self.dgf, self.layers = dw_in, dw_out, dgf, layers
+        self.flow_t, self.dw_time = flow_t, dw_time
         s = jn_expert_io()
         s.n_samples = int(n_samples)
         s.prefix_rows = int(prefix_rows)
         s.noisy, s.targets, s.pred, s.loss = _ptr(noisy), _ptr(targets), _ptr(pred), _ptr(loss)
         s.dw_in, s.dw_out, s.dgf = _ptr(dw_in), _ptr(dw_out), _ptr(dgf)
+        s.flow_t, s.dw_time = _ptr(flow_t), _ptr(dw_time)
         self._layers = (jn_expert_layer_grads * len(layers))(
             *[jn_expert_layer_grads(*[_ptr(lg[k]) for k in EXPERT_LAYER_FIELDS]) for lg in layers])
         s.layers = C.cast(self._layers, C.POINTER(jn_expert_layer_grads))

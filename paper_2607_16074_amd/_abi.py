@@ -113,7 +113,8 @@ class jn_expert(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d", C.c_int32), ("n_heads", C.c_int32), ("ffn", C.c_int32),
                 ("action_dim", C.c_int32), ("chunk", C.c_int32), ("d_prefix", C.c_int32), ("eps", C.c_float),
                 ("w_in", C.c_void_p), ("w_out", C.c_void_p), ("gf", C.c_void_p),
-                ("layers", C.POINTER(jn_expert_layer))]
+                ("layers", C.POINTER(jn_expert_layer)), ("w_time", C.c_void_p), ("d_time", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class jn_expert_layer_grads(C.Structure):
@@ -124,7 +125,7 @@ class jn_expert_io(C.Structure):
     _fields_ = [("n_samples", C.c_int32), ("reserved", C.c_int32), ("prefix_rows", C.c_int64),
                 ("noisy", C.c_void_p), ("targets", C.c_void_p), ("pred", C.c_void_p), ("loss", C.c_void_p),
                 ("dw_in", C.c_void_p), ("dw_out", C.c_void_p), ("dgf", C.c_void_p),
-                ("layers", C.POINTER(jn_expert_layer_grads))]
+                ("layers", C.POINTER(jn_expert_layer_grads)), ("flow_t", C.c_void_p), ("dw_time", C.c_void_p)]
 
 
 class jn_adamw_tenant(C.Structure):

@@ -876,6 +876,8 @@ constexpr int kKP = 64;
 struct ExpShape {
   int32_t L, d, H, f, chunk, dp;
   float eps;
+  int32_t dt = 0;     // flow-time feature width (0: plain regression)
+  int32_t ki = kAP;   // staged input width: padded actions, then flow-time features
 };
 
 // Host view of one expert call: per-tenant rows and padded contraction sizes.
@@ -890,8 +892,8 @@ struct ExpPlan {
 // Workspace regions (byte offsets); per-layer saves are arrays of offsets.
 struct ExpLayout {
   size_t arena = 0, arena_bytes = 0;
-  size_t x, xf, yb, ub, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, part, TA, TB,
-      WT, dwinp, dwoutp;
+  size_t x, xf, yb, ub, vel, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, part,
+      TA, TB, WT, dwinp, dwoutp;
   std::vector<size_t> x1, x2, x3, h1, h2, h3, qkv, os, osb, lses, qc, kv, oc, ocb, lsec, pre, mb;
   size_t total = 0;
 };
@@ -910,6 +912,12 @@ jn_status exp_plan(jn_ctx* c, const jn_packed* p, const jn_expert* ex, const jn_
   if (sh.f % 64 != 0 || sh.dp % 64 != 0) return fail(c, JN_EUNSUPPORTED, "ffn and d_prefix must be multiples of 64");
   if (sh.dp != p->d) return fail(c, JN_EINCOMPAT, "expert reads width %d, backbone has %d", sh.dp, p->d);
   if (!(sh.eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
+  if (e0.w_time) {
+    if (e0.d_time < 64 || e0.d_time % 64 != 0 || e0.d_time > 4096)
+      return fail(c, JN_EUNSUPPORTED, "d_time %d must be a multiple of 64 in [64, 4096]", e0.d_time);
+    sh.dt = e0.d_time;
+    sh.ki = kAP + e0.d_time;
+  }
   P->sh = sh;
   P->G = G;
   P->N = p->N;
@@ -931,6 +939,12 @@ jn_status exp_plan(jn_ctx* c, const jn_packed* p, const jn_expert* ex, const jn_
     if (I.n_samples < 1 || I.prefix_rows < I.n_samples) return fail(c, JN_ESHAPE, "io %d sizes", g);
     if (!I.noisy || !I.targets || !I.pred || !I.loss || !I.dw_in || !I.dw_out || !I.dgf || !I.layers)
       return fail(c, JN_EINVAL, "io %d incomplete", g);
+    if ((e.w_time != nullptr) != (sh.dt > 0) || (sh.dt > 0 && e.d_time != sh.dt))
+      return fail(c, JN_EUNSUPPORTED, "expert %d differs from expert 0 in its flow-time projection", g);
+    if (sh.dt > 0 && (!I.flow_t || !I.dw_time || ((uintptr_t)I.dw_time) % 16 != 0))
+      return fail(c, JN_EINVAL, "io %d: flow matching needs flow_t and an aligned dw_time", g);
+    if (sh.dt == 0 && (I.flow_t || I.dw_time))
+      return fail(c, JN_EINVAL, "io %d: flow_t / dw_time given but expert %d has no w_time", g, g);
     for (int l = 0; l < sh.L; ++l) {
       const jn_expert_layer_grads& Gr = I.layers[l];
       float* ps[] = {Gr.wqkv_s, Gr.wo_s, Gr.wq_c, Gr.wkv_c, Gr.wo_c, Gr.w_up, Gr.w_down, Gr.g1, Gr.g2, Gr.g3};
@@ -983,13 +997,15 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.x = take(4 * Na * d);
   Ly.xf = take(4 * Na * d);
   Ly.yb = take(2 * Na * d);
-  Ly.ub = take(2 * Na * kAP);
+  const int64_t KI = s.ki;
+  Ly.ub = take(2 * Na * KI);
+  Ly.vel = take(s.dt > 0 ? 4 * Na * 32 : 0);
   Ly.predp = take(4 * Na * kAP);
   Ly.dpred = take(4 * Na * kAP);
   Ly.dpredb = take(2 * Na * kAP);
   Ly.z = take(2 * Pz * s.dp);
   Ly.zoff = take(4 * (P.N + 1));
-  Ly.winp = take(2 * G * d * kAP);
+  Ly.winp = take(2 * G * d * KI);
   Ly.woutp = take(2 * G * kAP * d);
   Ly.woutpT = take(2 * G * d * kAP);
   Ly.dx = take(4 * Na * d);
@@ -1002,9 +1018,9 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.gx = take(4 * Na * d);
   Ly.part = take(4 * G * 16 * d);
   Ly.TA = take(2 * std::max<int64_t>(wmax * P.KaT, 2 * d * P.KzT));
-  Ly.TB = take(2 * std::max<int64_t>(wmax * P.KaT, (int64_t)s.dp * P.KzT));
+  Ly.TB = take(2 * std::max<int64_t>(std::max<int64_t>(wmax, KI) * P.KaT, (int64_t)s.dp * P.KzT));
   Ly.WT = take(2 * G * std::max<int64_t>(f * d, 3 * d * d) + 2 * G * 2 * d * s.dp);
-  Ly.dwinp = take(4 * G * d * kAP);
+  Ly.dwinp = take(4 * G * d * KI);
   Ly.dwoutp = take(4 * G * kAP * d);
   for (int l = 0; l < s.L; ++l) {
     Ly.x1.push_back(take(4 * Na * d));
@@ -1097,6 +1113,8 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
   char* const darena = w + Ly.arena;
   const ExpShape& S = P.sh;
   const int64_t d = S.d, f = S.f, dp = S.dp, H = S.H;
+  const bool flow = S.dt > 0;
+  const int64_t KI = S.ki;  // staged input width
   auto F = [&](size_t off) { return (float*)(w + off); };
   auto B = [&](size_t off) { return (uint16_t*)(w + off); };
   Recorder rec;
@@ -1262,14 +1280,33 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     std::vector<CopyDesc> v;
     for (int32_t g = 0; g < G; ++g) {
       const int32_t a = ex[g].action_dim;
-      CopyDesc u{io[g].noisy, B(Ly.ub) + (int64_t)P.roff[g] * kAP, a, kAP, P.rows[g], kAP, P.rows[g], a, 0, 1, 0, 0};
-      CopyDesc wi{ex[g].w_in, B(Ly.winp) + (int64_t)g * d * kAP, a, kAP, (int32_t)d, kAP, (int32_t)d, a, 1, 1, 0, 0};
+      if (!flow) {
+        CopyDesc u{io[g].noisy, B(Ly.ub) + (int64_t)P.roff[g] * KI, a, KI, P.rows[g], kAP, P.rows[g], a, 0, 1, 0, 0};
+        v.push_back(u);
+      }
+      CopyDesc wi{ex[g].w_in, B(Ly.winp) + (int64_t)g * d * KI, a, KI, (int32_t)d, kAP, (int32_t)d, a, 1, 1, 0, 0};
       CopyDesc wo{ex[g].w_out, B(Ly.woutp) + (int64_t)g * kAP * d, d, d, kAP, (int32_t)d, a, (int32_t)d, 1, 1, 0, 0};
-      v.push_back(u);
       v.push_back(wi);
       v.push_back(wo);
+      if (flow)  // the flow-time projection occupies input columns kAP .. kAP + d_time
+        v.push_back(CopyDesc{ex[g].w_time, B(Ly.winp) + (int64_t)g * d * KI + kAP, S.dt, KI, (int32_t)d, S.dt,
+                             (int32_t)d, S.dt, 1, 1, 0, 0});
     }
     copy(v);
+    if (flow) {
+      std::vector<FlowDesc> fv(G);
+      for (int32_t g = 0; g < G; ++g)
+        fv[g] = FlowDesc{io[g].flow_t, io[g].noisy, io[g].targets, F(Ly.vel) + (int64_t)P.roff[g] * 32,
+                         (int64_t)P.roff[g], P.rows[g], ex[g].action_dim};
+      const size_t at = rec.add(fv.data(), sizeof(FlowDesc) * G);
+      const int64_t na = P.Na;
+      const int32_t ch = S.chunk, dt = S.dt;
+      uint16_t* const ubp = B(Ly.ub);
+      rec.ops.push_back([=](char* ar) {
+        return launch_flow_prep(s, (const FlowDesc*)(ar + at), G, na, ch, kAP, dt, ubp, (int32_t)KI);
+      });
+      rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+    }
     std::vector<TransDesc> t;
     for (int32_t g = 0; g < G; ++g)
       t.push_back(TransDesc{B(Ly.woutp) + (int64_t)g * kAP * d, B(Ly.woutpT) + (int64_t)g * d * kAP, d, kAP, kAP,
@@ -1281,7 +1318,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
                            (int32_t*)(w + Ly.zoff), w + Ly.z);
     });
     rec.opcode.push_back(JN_OP_EXPERT_OTHER);
-    rows_gemm(EPI_F32, B(Ly.ub), kAP, [&](int32_t g) { return B(Ly.winp) + (int64_t)g * d * kAP; }, d, F(Ly.x), d, true);
+    rows_gemm(EPI_F32, B(Ly.ub), KI, [&](int32_t g) { return B(Ly.winp) + (int64_t)g * d * KI; }, d, F(Ly.x), d, true);
   }
   const float scale = 1.0f / sqrtf((float)(d / H));
   for (int l = 0; l < S.L; ++l) {
@@ -1366,7 +1403,9 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
             kAP, true);
   {
     std::vector<XLossDesc> v(G);
-    for (int32_t g = 0; g < G; ++g) v[g] = XLossDesc{io[g].targets, io[g].pred, io[g].loss, ex[g].action_dim, 0};
+    for (int32_t g = 0; g < G; ++g)
+      v[g] = XLossDesc{flow ? F(Ly.vel) + (int64_t)P.roff[g] * 32 : io[g].targets, io[g].pred, io[g].loss,
+                       ex[g].action_dim, 0};
     const size_t at = rec.add(v.data(), sizeof(XLossDesc) * G);
     rec.ops.push_back([=](char* a) {
       return launch_xloss(s, (const XLossDesc*)(a + at), (const int32_t*)(a + roff_at), G, F(Ly.predp), kAP,
@@ -1495,14 +1534,17 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
   // input projection and the padded output-projection gradient
   rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
   trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-  trans_rows(B(Ly.ub), kAP, B(Ly.TB), false);
-  wgrad(d, kAP, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * kAP; }, false);
+  trans_rows(B(Ly.ub), KI, B(Ly.TB), false);
+  wgrad(d, KI, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * KI; }, false);
   {
     std::vector<CopyDesc> v;
     for (int32_t g = 0; g < G; ++g) {
       const int32_t a = ex[g].action_dim;
-      v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * kAP, io[g].dw_in, kAP, a, (int32_t)d, a, (int32_t)d, a, 0, 0, 0,
+      v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * KI, io[g].dw_in, KI, a, (int32_t)d, a, (int32_t)d, a, 0, 0, 0,
                            0});
+      if (flow)
+        v.push_back(CopyDesc{F(Ly.dwinp) + (int64_t)g * d * KI + kAP, io[g].dw_time, KI, S.dt, (int32_t)d, S.dt,
+                             (int32_t)d, S.dt, 0, 0, 0, 0});
       v.push_back(CopyDesc{F(Ly.dwoutp) + (int64_t)g * kAP * d, io[g].dw_out, d, d, a, (int32_t)d, a, (int32_t)d, 0, 0, 0,
                            0});
     }

@@ -216,6 +216,21 @@ struct AttnArgs {
 };
 hipError_t launch_xattn(hipStream_t s, const AttnArgs& A, int32_t nsamples, bool backward);
 
+// Flow-matching inputs of one tenant's expert rows (rows = n * chunk, tenant
+// arrival order): input row [x | 0 | phi(t)] (bf16, ld columns: x = t*noise +
+// (1-t)*act in the first a, zeros up to kap, the d_time flow-time features
+// after) and vel = noise - act (fp32 [rows][a]).
+struct FlowDesc {
+  const float* t;       // [n]
+  const float* noise;   // [rows][a]
+  const float* act;     // [rows][a]
+  float* vel;           // [rows][a]
+  int64_t roff;         // first row of the tenant in the expert's row space
+  int32_t rows, a;
+};
+hipError_t launch_flow_prep(hipStream_t s, const FlowDesc* d, int32_t G, int64_t total_rows, int32_t chunk,
+                            int32_t kap, int32_t d_time, uint16_t* in_rows, int32_t ld);
+
 struct XLossDesc {
   const float* target;  // [rows_t][a]
   float* pred;          // [rows_t][a]

@@ -830,4 +830,46 @@ hipError_t launch_xloss(hipStream_t s, const XLossDesc* d, const int32_t* roff, 
   return hipGetLastError();
 }
 
+
+// ------------------------------------------------------------- flow prep ---
+// One block per expert row: the tenant is found from the descriptors' row
+// ranges, the sample from row / chunk.  Columns [0, a): bf16(t e + (1-t) A)
+// and vel = e - A; [a, kap): 0; [kap, kap + d_time): bf16 of sin / cos of
+// 1000 t w_j with w_j = 10000^(-j / (d_time/2)) (fp32 math).
+__global__ __launch_bounds__(256) void flow_prep_kernel(const FlowDesc* __restrict__ d, int32_t G, int32_t chunk,
+                                                        int32_t kap, int32_t d_time, uint16_t* __restrict__ in_rows,
+                                                        int32_t ld) {
+  const int64_t row = blockIdx.x;
+  int32_t g = 0;
+  while (g + 1 < G && row >= d[g + 1].roff) ++g;
+  const FlowDesc D = d[g];
+  const int64_t r = row - D.roff;
+  if (r < 0 || r >= D.rows) return;
+  const float tau = D.t[r / chunk];
+  uint16_t* out = in_rows + row * ld;
+  const int32_t half = d_time >> 1;
+  const float l2 = 13.287712379549449f;  // log2(10000)
+  for (int32_t c = threadIdx.x; c < kap + d_time; c += 256) {
+    float v = 0.f;
+    if (c < D.a) {
+      const float e = D.noise[r * D.a + c], A = D.act[r * D.a + c];
+      v = tau * e + (1.0f - tau) * A;
+      D.vel[r * D.a + c] = e - A;
+    } else if (c >= kap) {
+      const int32_t j = c - kap;
+      const int32_t jj = j < half ? j : j - half;
+      const float ang = 1000.0f * tau * exp2f(-(float)jj / (float)half * l2);
+      v = j < half ? sinf(ang) : cosf(ang);
+    }
+    out[c] = f2bf(v);
+  }
+}
+
+hipError_t launch_flow_prep(hipStream_t s, const FlowDesc* d, int32_t G, int64_t total_rows, int32_t chunk,
+                            int32_t kap, int32_t d_time, uint16_t* in_rows, int32_t ld) {
+  if (G < 1 || total_rows < 1 || total_rows > 0x7fffffff || chunk < 1 || ld < kap + d_time) return hipErrorInvalidValue;
+  flow_prep_kernel<<<(unsigned)total_rows, 256, 0, s>>>(d, G, chunk, kap, d_time, in_rows, ld);
+  return hipGetLastError();
+}
+
 }  // namespace jnx

@@ -77,7 +77,8 @@ class Model:
                 xl = [{k: _dev_bf16(v, device) for k, v in L.items()} for L in e["layers"]]
                 xs.append(Expert(_dev_bf16(e["w_in"], device), _dev_bf16(e["w_out"], device),
                                  _dev_bf16(e["gf"], device), xl, tenant_meta[g]["expert_heads"],
-                                 tenant_meta[g]["chunk"], bb.d, eps))
+                                 tenant_meta[g]["chunk"], bb.d, eps,
+                                 _dev_bf16(e["w_time"], device) if "w_time" in e else None))
         return cls(bb, hs, tenant_meta, prefix_sig, xs)
 
 
@@ -86,7 +87,7 @@ class GroupStep:
 
     def __init__(self, model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
                  tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda",
-                 noisy: Optional[Dict[int, np.ndarray]] = None):
+                 noisy: Optional[Dict[int, np.ndarray]] = None, flow_t: Optional[Dict[int, np.ndarray]] = None):
         import torch
         self.model = model
         self.ctx = ctx or Context()
@@ -125,7 +126,9 @@ class GroupStep:
                                          torch.empty(shape, dtype=torch.float32, device=device),
                                          torch.empty(1, dtype=torch.float32, device=device),
                                          f32(w_in), f32(w_out), f32(gf),
-                                         [{k2: f32(L[k2]) for k2 in EXPERT_LAYER_FIELDS} for L in xl]))
+                                         [{k2: f32(L[k2]) for k2 in EXPERT_LAYER_FIELDS} for L in xl],
+                                         _dev_f32(flow_t[g], device) if e.w_time is not None else None,
+                                         f32(e.w_time) if e.w_time is not None else None))
             self.hd_ws = torch.empty(jn_experts_workspace_size(self.packed, self.experts, self.ios), dtype=torch.uint8,
                                      device=device)
         else:
@@ -229,6 +232,8 @@ class TenantOptimizer:
             if group.use_experts:
                 e, io = group.experts[k], group.ios[k]
                 pairs = [(e.w_in, io.dw_in), (e.w_out, io.dw_out), (e.gf, io.dgf)]
+                if e.w_time is not None:
+                    pairs.append((e.w_time, io.dw_time))
                 for L, Lg in zip(e.layers, io.layers):
                     pairs += [(L[n], Lg[n]) for n in EXPERT_LAYER_FIELDS]
                 masters = [w.float().contiguous() for w, _ in pairs]
@@ -256,13 +261,13 @@ class TenantOptimizer:
 
 def isolated_runs(model: Model, requests: Sequence[Request], targets: Dict[int, np.ndarray],
                   tenants: Sequence[int], align: int = 1, ctx: Optional[Context] = None, device="cuda",
-                  noisy: Optional[Dict[int, np.ndarray]] = None):
+                  noisy: Optional[Dict[int, np.ndarray]] = None, flow_t: Optional[Dict[int, np.ndarray]] = None):
     """One ``GroupStep`` per tenant (its own requests only), sharing the weights."""
     ctx = ctx or Context()
     out = []
     for g in tenants:
         reqs = [r for r in requests if r.tenant == g]
-        out.append(GroupStep(model, reqs, targets, [g], align, ctx, device, noisy))
+        out.append(GroupStep(model, reqs, targets, [g], align, ctx, device, noisy, flow_t))
     return out
 
 
@@ -295,3 +300,17 @@ def from_workload(wl, device="cuda", with_noisy: bool = False):
     if with_noisy:
         return model, reqs, targets, noisy
     return model, reqs, targets
+
+
+def flow_times(wl) -> Optional[Dict[int, np.ndarray]]:
+    """Flow times of every flow-matching expert tenant in arrival order, or
+    None when the workload trains its experts by plain regression."""
+    ft = getattr(wl, "flow_t", None)
+    if not ft or all(x is None for x in ft):
+        return None
+    out = {}
+    for g, x in enumerate(ft):
+        if x is not None:
+            idx = [i for r in wl.requests if r.tenant == g for i in range(r.first, r.first + r.n)]
+            out[g] = np.asarray(x, np.float32)[np.array(idx, dtype=np.int64)]
+    return out

@@ -47,18 +47,20 @@ def rel_l2(g, o):
     return float(np.linalg.norm(np.asarray(g, np.float64) - o) / max(np.linalg.norm(o), 1e-30))
 
 
-def expert_spec(expert, chunk, schemas, d=128, lo=4, hi=40, img=16, max_len=64, layers=1):
-    """Backbone of width d; tenants (n_samples, action_dim) with one expert shape."""
+def expert_spec(expert, chunk, schemas, d=128, lo=4, hi=40, img=16, max_len=64, layers=1, flow=0):
+    """Backbone of width d; tenants (n_samples, action_dim) with one expert shape;
+    ``flow`` > 0: flow-matching objective with that many flow-time features."""
     ten = tuple(W.TenantSpec(n, img, lo, hi, max_len, (d, 64, a * chunk), a, chunk, expert=expert)
                 for n, a in schemas)
-    return W.WorkloadSpec(91, W.BackboneSpec(layers, d, 4, 256, False), ten, 0, "expert")
+    return W.WorkloadSpec(91, W.BackboneSpec(layers, d, 4, 256, False), ten, 0, "expert", flow)
 
 
 def run_experts(wl, align=1, tenants=None):
     from paper_2607_16074_amd import step as jstep
     model, reqs, targets, noisy = jstep.from_workload(wl, with_noisy=True)
     G = wl.spec.G
-    st = jstep.GroupStep(model, reqs, targets, list(range(G)) if tenants is None else tenants, align, noisy=noisy)
+    st = jstep.GroupStep(model, reqs, targets, list(range(G)) if tenants is None else tenants, align, noisy=noisy,
+                         flow_t=jstep.flow_times(wl))
     st.run()
     torch.cuda.synchronize()
     return st, targets, noisy
@@ -78,7 +80,10 @@ def check_stagewise(wl, st, targets, noisy, only=None):
             continue
         L, _, H, _ = wl.spec.tenants[g].expert
         z = [hidden[cu[i]: cu[i] + sl[i]] for i in perm[tso[k]: tso[k + 1]]]
-        ref = oexpert.expert_step(wl.experts[g], L, H, eps, list(noisy[g]), z, targets[g], rnd=True)
+        from paper_2607_16074_amd import step as jstep
+        ft = jstep.flow_times(wl)
+        ref = oexpert.expert_step(wl.experts[g], L, H, eps, list(noisy[g]), z, targets[g], rnd=True,
+                                  flow_t=None if ft is None else ft[g])
         io = st.ios[k]
         # a gradient that vanishes analytically (e.g. the queries of a one-key
         # attention) is compared against the tenant's gradient scale instead
@@ -92,6 +97,8 @@ def check_stagewise(wl, st, targets, noisy, only=None):
                 "w_in": grel(io.dw_in.cpu().numpy(), ref["grads"]["w_in"]),
                 "w_out": grel(io.dw_out.cpu().numpy(), ref["grads"]["w_out"]),
                 "gf": grel(io.dgf.cpu().numpy(), ref["grads"]["gf"])}
+        if io.dw_time is not None:
+            errs["w_time"] = grel(io.dw_time.cpu().numpy(), ref["grads"]["w_time"])
         for l, lg in enumerate(io.layers):
             for name, t in lg.items():
                 errs[f"{l}.{name}"] = grel(t.cpu().numpy(), ref["grads"][f"{l}.{name}"])
@@ -131,21 +138,48 @@ def test_expert_degenerate_single_token(jn):
     check_stagewise(wl, st, targets, noisy)
 
 
-def test_expert_grouped_equals_isolated_bitwise(jn):
+def test_expert_flow_matching_small(jn):
+    """Flow-matching objective (path point in, velocity target, 64 flow-time
+    features projected into every action token): three ragged tenants, the
+    time projection's gradient included."""
+    spec = expert_spec((2, 256, 4, 512), 10, [(3, 7), (5, 14), (2, 32)], flow=64)
+    wl = W.make_workload(spec, request_split=(1, 2, 1), request_order=[2, 0, 3, 1])
+    _say("expert flow matching small")
+    st, targets, noisy = run_experts(wl, align=16)
+    check_stagewise(wl, st, targets, noisy)
+
+
+def test_expert_flow_matching_config8_sampled(jn):
+    """The flow-matching preset's shapes (6-layer d1024 experts, 1024 flow-time
+    features, 12-layer d768 backbone): the three tenants with the fewest
+    samples as one group, all three stage-wise."""
+    full = W.config_spec(8, 0)
+    order = sorted(range(full.G), key=lambda g: (full.tenants[g].n_samples, g))[:3]
+    spec = dataclasses.replace(full, tenants=tuple(full.tenants[g] for g in order))
+    _say(f"config-8 tenants {order}")
+    wl = W.make_workload(spec)
+    st, targets, noisy = run_experts(wl)
+    check_stagewise(wl, st, targets, noisy)
+
+
+@pytest.mark.parametrize("flow", [0, 64])
+def test_expert_grouped_equals_isolated_bitwise(jn, flow):
     from paper_2607_16074_amd import step as jstep
-    spec = expert_spec((2, 256, 4, 512), 10, [(3, 7), (5, 14), (2, 32)])
+    spec = expert_spec((2, 256, 4, 512), 10, [(3, 7), (5, 14), (2, 32)], flow=flow)
     wl = W.make_workload(spec)
     _say("expert grouped vs isolated")
     st, targets, noisy = run_experts(wl)
     model, reqs = st.model, st.requests
     for k, g in enumerate(st.tenants):
         reqs_g = [r for r in jstep.from_workload(wl)[1] if r.tenant == g]
-        iso = jstep.GroupStep(model, reqs_g, targets, [g], 1, noisy=noisy)
+        iso = jstep.GroupStep(model, reqs_g, targets, [g], 1, noisy=noisy, flow_t=jstep.flow_times(wl))
         iso.run()
         torch.cuda.synchronize()
         a, b = st.ios[k], iso.ios[0]
         assert torch.equal(a.pred, b.pred) and torch.equal(a.loss, b.loss), g
         assert torch.equal(a.dw_in, b.dw_in) and torch.equal(a.dw_out, b.dw_out) and torch.equal(a.dgf, b.dgf), g
+        if a.dw_time is not None:
+            assert torch.equal(a.dw_time, b.dw_time), g
         for la, lb in zip(a.layers, b.layers):
             for name in la:
                 assert torch.equal(la[name], lb[name]), (g, name)
@@ -166,6 +200,19 @@ def test_expert_errors_enqueue_nothing(jn):
             assert e.value.status == status, (field, e.value)
         finally:
             setattr(x0, field, saved)
+    # flow-time data without a flow-time projection, and the reverse
+    io0 = st.ios[0].struct
+    io0.flow_t = st.ios[0].loss.data_ptr()
+    with pytest.raises(jn.JNError) as e:
+        jn.jn_tenant_experts_fwd_bwd(st.ctx, st.packed, st.hidden, st.experts, st.ios, st.hd_ws)
+    assert e.value.status == 1
+    io0.flow_t = None
+    x0.w_time = st.experts[0].w_in.data_ptr()
+    x0.d_time = 64
+    with pytest.raises(jn.JNError):
+        jn.jn_tenant_experts_fwd_bwd(st.ctx, st.packed, st.hidden, st.experts, st.ios, st.hd_ws)
+    x0.w_time = None
+    x0.d_time = 0
     small = st.hd_ws[:1024]
     with pytest.raises(jn.JNError) as e:
         jn.jn_tenant_experts_fwd_bwd(st.ctx, st.packed, st.hidden, st.experts, st.ios, small)
