@@ -75,6 +75,38 @@ def gemm_flops_per_token(bb) -> dict:
     return {"gemm_qkv": 2 * bb.qkv_rows * d, "gemm_o": 2 * d * d, "gemm_up": up, "gemm_down": 2 * f * d}
 
 
+def kernel_rates(by_op, steps, spec, reqs, T, valid, N):
+    """Attention against the bf16 MFMA peak and the HBM-bound kernels against
+    8 TB/s, from their per-step event times and algorithmic work (valid rows
+    only; bytes each kernel must move)."""
+    bb = spec.backbone
+    d, H, hd = bb.d, bb.heads, bb.d // bb.heads
+    lens = np.concatenate([np.asarray(r.lengths, np.int64) for r in reqs])
+    if bb.causal:
+        att_flops = bb.layers * float(np.sum(2 * lens * (lens + 1) * d))   # keys <= query only
+    else:
+        att_flops = bb.layers * float(np.sum(4 * lens * lens * d))
+    out = {}
+    if "attention" in by_op:
+        ms = by_op["attention"]["ms"] / steps
+        out["attention"] = {"ms_per_step": ms, "tflops": att_flops / (ms * 1e-3) / 1e12,
+                            "frac_of_bf16_peak": att_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+    # bytes per step: pack / unpack read and write every valid row once; the
+    # first RMSNorm reads bf16 and writes the fp32 residual and the bf16 output,
+    # the other 2L of them read fp32 and write bf16; pool reads every valid row
+    # and writes N fp32 rows; the rotation reads and writes q and k
+    kvh = bb.kv_heads or H
+    nbytes = {"pack": 4.0 * valid * d, "unpack": 4.0 * valid * d,
+              "rmsnorm": (8.0 + 6.0 * 2 * bb.layers) * T * d, "pool": 2.0 * valid * d + 4.0 * N * d,
+              "rope": bb.layers * 4.0 * T * (H + kvh) * hd}
+    for op, b in nbytes.items():
+        if op in by_op:
+            ms = by_op[op]["ms"] / steps
+            out[op] = {"ms_per_step": ms, "GB_per_s": b / (ms * 1e-3) / 1e9,
+                       "frac_of_hbm": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    return out
+
+
 def time_steps(steps, fn, ctx, warmup):
     import torch
     for _ in range(warmup):
@@ -364,6 +396,7 @@ def main():
                      "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(args.config),
                      "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},
         "gemm_by_op": gemm_stats,
+        "kernels": kernel_rates(by_op, args.steps, spec, reqs, grouped.T, valid, N),
         "tenant_optimizer": opt_stats,
         "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample")},
     }
