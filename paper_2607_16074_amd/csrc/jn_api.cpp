@@ -524,6 +524,19 @@ jn_status jn_backbone_forward(jn_ctx* c, const jn_backbone* bb, const jn_packed*
     return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte and hidden 16-byte aligned");
 
   const int32_t T = p->T, d = bb->d, f = bb->ffn;
+  {
+    // launch-size limits, checked before anything is enqueued: a dispatch
+    // holds at most 2^32 - 1 work-items (GEMM: <= 512 threads per 128x128-or-
+    // larger tile), and the attention grid at most 2^30 workgroups
+    const int64_t kv = bb->n_kv_heads ? bb->n_kv_heads : bb->n_heads;
+    const int64_t nmax = std::max<int64_t>((bb->n_heads + 2 * kv) * (d / bb->n_heads),
+                                           (bb->layers[0].w_gate ? 2 : 1) * (int64_t)f);
+    const int64_t gemm_items = ((int64_t)T + 127) / 128 * ((nmax + 127) / 128) * 512;
+    const int64_t qtiles = ((int64_t)p->max_seqlen + 127) / 128;
+    const int64_t attn_blocks = ((int64_t)p->N * kv + 7) / 8 * 8 * (bb->n_heads / kv) * qtiles;
+    if (gemm_items >= (1ll << 32) || attn_blocks > (1ll << 30))
+      return fail(c, JN_ESHAPE, "batch of %d rows / %d samples exceeds one launch's grid", T, p->N);
+  }
   char* w = (char*)ws;
   float* x = (float*)(w + L.x);
   void* h = w + L.h;
@@ -671,6 +684,7 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hid
   if (!hidden || !io || !ws) return fail(c, JN_EINVAL, "null hidden, io or workspace");
   if (((uintptr_t)hidden) % 16 != 0 || p->d % 8 != 0)
     return fail(c, JN_EUNSUPPORTED, "hidden must be 16-byte aligned and d a multiple of 8");
+  if ((int64_t)p->N * ((p->d + 63) / 64) > 0x7fffffff) return fail(c, JN_ESHAPE, "too many samples for the pool grid");
   jn_status st = check_heads(c, p, heads, G);
   if (st != JN_OK) return st;
   for (int32_t g = 0; g < G; ++g) {
@@ -1919,6 +1933,7 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
   if (st != JN_OK) return st;
   if (ws_bytes < L.total) return fail(c, JN_ENOSPACE, "workspace %zu B < %zu B", ws_bytes, L.total);
   if (((uintptr_t)ws) % 256 != 0) return fail(c, JN_EUNSUPPORTED, "workspace must be 256-byte aligned");
+  if ((int64_t)p.N * ((o->d_model + 63) / 64) > 0x7fffffff) return fail(c, JN_ESHAPE, "too many samples for the pool grid");
   for (int32_t r = 0; r < R; ++r)
     if (((uintptr_t)req[r].embeds) % 16 != 0) return fail(c, JN_EUNSUPPORTED, "request %d embeds not 16-byte aligned", r);
   for (int32_t g = 0; g < G; ++g)
