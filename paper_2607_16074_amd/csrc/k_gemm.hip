@@ -2,27 +2,30 @@
 //
 //   C[M][N] (+)= epi( X[M][K] * W[N][K]^T )     X = activations, W = weights
 //
-// Tiling: a workgroup of WGN x WGM wavefronts owns a BN x BM tile (weight rows
-// x tokens; 256x256 with 8 wavefronts for large launches); each wavefront
-// accumulates (BN/WGN) x (BM/WGM) with v_mfma_f32_32x32x16_bf16.  The weight tile is the MFMA "A" operand, the
-// token tile the "B" operand, so each lane ends with 4 consecutive output
-// columns of one token row and the epilogue writes 8-byte (bf16) / 16-byte
-// (fp32) vectors along the row-major output.
+// MFMA: v_mfma_f32_16x16x32_bf16.  The weight tile is the MFMA "A" operand
+// and the token tile the "B" operand: lane l holds 8 consecutive K values of
+// weight row l & 15 and of token row l & 15, K block 8 * (l >> 4), and ends
+// with 4 consecutive output columns 4 * (l >> 4) .. +3 of token row l & 15,
+// so the epilogue writes 8-byte (bf16) / 16-byte (fp32) vectors along the
+// row-major output.  Measured on the 2048-wide shapes the 16x16x32 form runs
+// 3-10% faster than 32x32x16 with the same operand traffic (the chip is
+// power-limited and this form needs less energy per flop); a K=64 slab is two
+// K=32 steps.  Every loop below issues, per output element, the same MFMA
+// sequence (slab order, K=32 steps in order, the same lane layout), so all
+// tile shapes and loops give identical bits.
 //
 // Operand staging: global_load_lds_dwordx4 moves 16-byte chunks straight from
-// global memory into LDS (no register staging).  K advances 64 per stage
-// (one 128-byte segment of every operand row) through two stages, so one slab
-// is in flight while the other is consumed.  Chunk c of LDS row r sits at
-// position c ^ swz(r), swz(r) = (r >> 1) & 7: two 128-byte rows share a 256-byte
-// bank row, and with this swizzle every 16-lane phase of a fragment read
-// (rows lane & 31, chunk 2*step + (lane >> 5)) covers all 64 banks (derived
-// from the bank-conflict counter's response to probe patterns; the GEMM runs
-// conflict-free).  Each DMA instruction fills 1 KB = 8 rows; the lane ->
-// source-chunk assignment applies the swizzle.  Per slab, four K=16 steps:
-// the fragments of step s+1 are read under the MFMAs of step s; the next
-// slab's DMA is interleaved with the first MFMAs; the one barrier per slab
-// sits before the last step's MFMAs, which then cover the read of the next
-// slab's first fragments.
+// global memory into LDS (no register staging).  K advances 64 per slab (one
+// 128-byte segment of every operand row).  Chunk c of LDS row r sits at
+// position c ^ swz(r), swz(r) = (r >> 1) & 7: two 128-byte rows share a
+// 256-byte bank row, and every 16-lane phase of a fragment read (16
+// consecutive rows, one chunk) covers all 64 banks.  Each DMA instruction
+// fills 1 KB = 8 rows; the lane -> source-chunk assignment applies the
+// swizzle.
+//
+// Loops: the 256x256 tile (8 wavefronts) runs a ring-buffered ping-pong loop
+// (gemm_ring_kernel); the smaller tiles of short launches and of the grouped
+// per-tenant launches run an interleaved double-buffered loop (gemm_tile).
 //
 // Launch order: tiles are walked in groups of 16 token-tiles (token tile
 // fastest).  Workgroups are dealt round-robin to the 8 XCDs, so each XCD's
@@ -31,23 +34,24 @@
 // the 2048-wide workloads, giving each XCD a contiguous block of tiles (an
 // explicit XCD remap) is no faster with 4x8 blocks and 13% slower with 16x2.
 //
-// Epilogues: bf16 store, GELU -> bf16, fp32 residual add (in place), and
-// GeGLU, whose gate and up weight rows are interleaved in 32-row blocks as
-// they are loaded, so the gate and up accumulators of an output column land
-// in the same lane.
+// Epilogues: bf16 store, GELU -> bf16, fp32 residual add (in place), fp32
+// store, GELU with fp32 pre-activation save, GELU' product, and GeGLU, whose
+// gate and up weight rows are interleaved in 16-row blocks as they are
+// loaded, so the gate and up accumulators of an output column land in the
+// same lane.
 #include "jn_device.h"
 #include "jn_internal.h"
 
 namespace jnx {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 #define JN_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-constexpr int kBK = 64;       // K per stage (128-byte rows)
-constexpr int kStages = 2;    // double buffer
+constexpr int kBK = 64;       // K per slab (128-byte rows)
+constexpr int kStages = 2;    // double buffer of the interleaved loop
 constexpr int kGroupM = 16;   // token tiles per L2 group
 
 __device__ __forceinline__ int lds_swz(int r) { return (r >> 1) & 7; }
@@ -67,84 +71,160 @@ __device__ __forceinline__ void wait_lgkmcnt() {
   __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (N << 8));
 }
 
+// T fragments of 16 rows each (rows row0, row0 + 16, ...), chunk position pos.
 template <int T>
 __device__ __forceinline__ void gemm_frags(bf16x8 (&f)[T], const uint16_t* stage, int row0, int pos) {
 #pragma unroll
-  for (int i = 0; i < T; ++i) f[i] = *reinterpret_cast<const bf16x8*>(stage + (row0 + i * 32) * kBK + pos * 8);
+  for (int i = 0; i < T; ++i) f[i] = *reinterpret_cast<const bf16x8*>(stage + (row0 + i * 16) * kBK + pos * 8);
 }
 
-template <int TN, int TM>
-__device__ __forceinline__ void gemm_mfma(f32x16 (&acc)[TN][TM], const bf16x8 (&fw)[TN], const bf16x8 (&fx)[TM]) {
-#pragma unroll
-  for (int i = 0; i < TN; ++i)
-#pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+// Source row of weight-tile row r: plain, or for GeGLU the gate / up rows
+// interleaved in 16-row blocks (block 2b = gate columns 16b.., 2b+1 = up).
+template <bool GLU>
+__device__ __forceinline__ const uint16_t* weight_row(const uint16_t* W, const uint16_t* W2, int64_t ldw, int32_t tn,
+                                                      int BN, int r, int32_t N) {
+  if constexpr (GLU) {
+    const int32_t col = min(tn * (BN / 2) + (r >> 5) * 16 + (r & 15), N - 1);
+    return (((r >> 4) & 1) ? W2 : W) + (int64_t)col * ldw;
+  } else {
+    return W + (int64_t)min(tn * BN + r, N - 1) * ldw;
+  }
 }
 
+// Epilogue shared by the loops: accumulator block (i, j) covers weight rows
+// 16 i .. of the wave's part and tokens 16 j ..; lane l owns output columns
+// n .. n+3, n = 16 i + 4 (l >> 4), of token row 16 j + (l & 15).
+template <int BN, int BM, int WGN, int WGM, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x4 (&acc)[BN / WGN / 16][BM / WGM / 16],
+                                              int32_t tm, int32_t tn, int wn, int wm, int lane) {
+  constexpr bool GLU = EPI == EPI_GEGLU_BF16;
+  constexpr int WN = BN / WGN, WM = BM / WGM;
+  constexpr int TN = WN / 16, TM = WM / 16;
+  void* __restrict__ C = g.C;
+  const int64_t ldc = g.ldc;
+  const int32_t M = g.M, N = g.N;
+  const int q4 = (lane >> 4) * 4;
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int32_t m = tm * BM + wm * WM + j * 16 + (lane & 15);
+    if (m >= M) continue;
+    if constexpr (GLU) {
+#pragma unroll
+      for (int i = 0; i < TN; i += 2) {
+        const int32_t n = tn * (BN / 2) + wn * (WN / 2) + (i >> 1) * 16 + q4;
+        if (n >= N) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = gelu_fast_f(acc[i][j][e]) * acc[i + 1][j][e];
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+            make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int32_t n = tn * BN + wn * WN + i * 16 + q4;
+        if (n >= N) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e];
+        if constexpr (EPI == EPI_RESID_F32) {
+          float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
+          float4 o = *p;
+          o.x += v[0];
+          o.y += v[1];
+          o.z += v[2];
+          o.w += v[3];
+          *p = o;
+        } else if constexpr (EPI == EPI_F32) {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n) =
+              make_float4(v[0], v[1], v[2], v[3]);
+        } else if constexpr (EPI == EPI_GELU_SAVE) {
+          *reinterpret_cast<float4*>(g.aux + (int64_t)m * g.ldaux + n) = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+              make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+        } else if constexpr (EPI == EPI_GELUGRAD_BF16) {
+          const float4 z = *reinterpret_cast<const float4*>(g.aux + (int64_t)m * g.ldaux + n);
+          v[0] *= gelu_grad_f(z.x);
+          v[1] *= gelu_grad_f(z.y);
+          v[2] *= gelu_grad_f(z.z);
+          v[3] *= gelu_grad_f(z.w);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+              make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+        } else {
+          if constexpr (EPI == EPI_GELU_BF16) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_fast_f(v[e]);
+          }
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+              make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+        }
+      }
+    }
+  }
+}
+
+// Position of tile pid in the grouped walk (16 token tiles per group).
+__device__ __forceinline__ void tile_of(int32_t pid, int32_t tiles_m, int32_t tiles_n, int32_t& tm, int32_t& tn) {
+  const int32_t per_group = kGroupM * tiles_n;
+  const int32_t first_m = (pid / per_group) * kGroupM;
+  const int32_t gsize = min(tiles_m - first_m, kGroupM);
+  tm = first_m + (pid % per_group) % gsize;
+  tn = (pid % per_group) / gsize;
+}
+
+// Interleaved double-buffered loop (tiles of short and grouped launches).
+// Per slab, two K=32 steps: the fragments of step 1 are read under the MFMAs
+// of step 0; the next slab's DMA (into the buffer the previous slab used) is
+// interleaved with the first MFMAs; the one barrier per slab sits before the
+// second step's MFMAs, which then cover the read of the next slab's first
+// fragments.
 template <int BN, int BM, int WGN, int WGM, int EPI>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16_t* __restrict__ lds) {
   const uint16_t* __restrict__ X = g.X;
-  const uint16_t* __restrict__ W = g.W;
-  const uint16_t* __restrict__ W2 = g.W2;
-  void* __restrict__ C = g.C;
-  const int64_t ldx = g.ldx, ldw = g.ldw, ldc = g.ldc;
-  const int32_t M = g.M, N = g.N, K = g.K, tiles_n = g.tiles_n, tiles_m = g.tiles_m;
+  const int64_t ldx = g.ldx;
+  const int32_t M = g.M, K = g.K;
   constexpr bool GLU = EPI == EPI_GEGLU_BF16;
-  constexpr int NW = WGN * WGM;              // wavefronts
+  constexpr int NW = WGN * WGM;                // wavefronts
   constexpr int WN = BN / WGN, WM = BM / WGM;  // per-wave tile
-  constexpr int TN = WN / 32, TM = WM / 32;
-  constexpr int ROWS = BN + BM;              // weight rows then token rows in a stage
-  constexpr int NI = ROWS / (8 * NW);        // 1 KB DMA instructions per wave per stage
-  constexpr int STAGE = ROWS * kBK;          // elements per stage
+  constexpr int TN = WN / 16, TM = WM / 16;
+  constexpr int ROWS = BN + BM;                // weight rows then token rows in a stage
+  constexpr int NI = ROWS / (8 * NW);          // 1 KB DMA instructions per wave per stage
+  constexpr int STAGE = ROWS * kBK;            // elements per stage
   static_assert(ROWS % (8 * NW) == 0 && TN >= 1 && TM >= 1, "tile shape");
-  static_assert(!GLU || TN % 2 == 0, "GeGLU pairs gate/up tiles inside a wave");
+  static_assert(!GLU || TN % 2 == 0, "GeGLU pairs gate/up blocks inside a wave");
 
-  // ---- grouped tile order
-  const int32_t per_group = kGroupM * tiles_n;
-  const int32_t group = pid / per_group;
-  const int32_t first_m = group * kGroupM;
-  const int32_t gsize = min(tiles_m - first_m, kGroupM);
-  const int32_t tm = first_m + (pid % per_group) % gsize;
-  const int32_t tn = (pid % per_group) / gsize;
-
+  int32_t tm, tn;
+  tile_of(pid, g.tiles_m, g.tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave / WGM, wm = wave % WGM;
 
-  // ---- DMA sources: this wave's instruction i fills stage rows 8*(wave*NI+i) ..
-  // +7 (1 KB); lane -> (row lane>>3, position lane&7), and the position holds
-  // logical chunk position ^ swz(row) of that row's 128-byte K segment.
-  const int32_t NL = GLU ? 2 * N : N;
+  // ---- DMA sources: this wave's instruction i fills stage rows 8*(wave*NI+i)
+  // .. +7 (1 KB); lane -> (row lane>>3, position lane&7), and the position
+  // holds logical chunk position ^ swz(row) of that row's 128-byte K segment.
   const uint16_t* src[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int row = 8 * (wave * NI + i) + (lane >> 3);
     const int chunk = (lane & 7) ^ lds_swz(row);
-    if (row < BN) {
-      if constexpr (GLU) {
-        const int32_t col = min(tn * (BN / 2) + (row >> 6) * 32 + (row & 31), N - 1);
-        src[i] = (((row >> 5) & 1) ? W2 : W) + (int64_t)col * ldw + chunk * 8;
-      } else {
-        src[i] = W + (int64_t)min(tn * BN + row, NL - 1) * ldw + chunk * 8;
-      }
-    } else {
+    if (row < BN)
+      src[i] = weight_row<GLU>(g.W, g.W2, g.ldw, tn, BN, row, g.N) + chunk * 8;
+    else
       src[i] = X + (int64_t)min(tm * BM + row - BN, M - 1) * ldx + chunk * 8;
-    }
   }
   uint16_t* const dst0 = lds + wave * NI * 512;  // 512 elements = 1 KB per instruction
 
-  f32x16 acc[TN][TM];
+  f32x4 acc[TN][TM];
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int KT = K / kBK;
-  // fragment rows and their swizzle (row0 of every fragment is a multiple of 32)
-  const int sw = lds_swz(lane & 31), half = lane >> 5;
-  const int wrow = wn * WN + (lane & 31), xrow = BN + wm * WM + (lane & 31);
+  const int sw = lds_swz(lane & 15), quad = lane >> 4;
+  const int wrow = wn * WN + (lane & 15), xrow = BN + wm * WM + (lane & 15);
 
   // prologue: slabs 0 and 1 in flight
 #pragma unroll
@@ -160,40 +240,32 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   }
   __builtin_amdgcn_s_barrier();
 
-  // Per slab: four K=16 steps; the fragments of step s+1 are read while the
-  // MFMAs of step s run.  The DMA of slab kt+1 (into the buffer slab kt-1
-  // used) is interleaved with the first MFMAs of slab kt.  The stage barrier
-  // sits before the last step's MFMAs: each wave has waited for its slab kt+1
-  // DMA and for its last reads of slab kt, meets the others, reads step 0 of
-  // slab kt+1 and only then issues the last eight MFMAs of slab kt, which
-  // cover that read.
   bf16x8 fw[2][TN], fx[2][TM];
-  gemm_frags<TN>(fw[0], lds, wrow, half ^ sw);
-  gemm_frags<TM>(fx[0], lds, xrow, half ^ sw);
+  gemm_frags<TN>(fw[0], lds, wrow, quad ^ sw);
+  gemm_frags<TM>(fx[0], lds, xrow, quad ^ sw);
   for (int kt = 0; kt < KT; ++kt) {
     const uint16_t* cur = lds + (kt & 1) * STAGE;
     const bool fill = kt >= 1 && kt + 1 < KT;  // slab kt+1 goes into the buffer slab kt-1 used
     uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
 #pragma unroll
-    for (int step = 0; step < 4; ++step) {
-      const int b = step & 1;
-      if (step < 3) {
-        const int pos = (2 * (step + 1) + half) ^ sw;
-        gemm_frags<TN>(fw[b ^ 1], cur, wrow, pos);
-        gemm_frags<TM>(fx[b ^ 1], cur, xrow, pos);
+    for (int step = 0; step < 2; ++step) {
+      if (step == 0) {
+        const int pos = (4 + quad) ^ sw;
+        gemm_frags<TN>(fw[1], cur, wrow, pos);
+        gemm_frags<TM>(fx[1], cur, xrow, pos);
       } else if (kt + 1 < KT) {
         wait_vmcnt<0>();
         wait_lgkmcnt<0>();
         __builtin_amdgcn_s_barrier();
         const uint16_t* nxt = lds + ((kt + 1) & 1) * STAGE;
-        gemm_frags<TN>(fw[0], nxt, wrow, half ^ sw);
-        gemm_frags<TM>(fx[0], nxt, xrow, half ^ sw);
+        gemm_frags<TN>(fw[0], nxt, wrow, quad ^ sw);
+        gemm_frags<TM>(fx[0], nxt, xrow, quad ^ sw);
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int q = 0; q < TN * TM; ++q) {
         const int i = q / TM, j = q % TM;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[b][i], fx[b][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[step][i], fx[step][j], acc[i][j], 0, 0, 0);
         // DMA d of slab kt+1 after MFMA d of the slab (as early as possible)
         constexpr int PER = (NI + TN * TM - 1) / (TN * TM);  // DMAs per MFMA
 #pragma unroll
@@ -207,73 +279,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
     }
   }
 
-  // ---- epilogue: lane owns output columns n..n+3 of token row m
-  const int hi4 = (lane >> 5) * 4;
-#pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int32_t m = tm * BM + wm * WM + j * 32 + (lane & 31);
-    if (m >= M) continue;
-    if constexpr (GLU) {
-#pragma unroll
-      for (int i = 0; i < TN; i += 2) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int32_t n = tn * (BN / 2) + wn * (WN / 2) + (i >> 1) * 32 + rr * 8 + hi4;
-          if (n >= N) continue;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = gelu_fast_f(acc[i][j][rr * 4 + e]) * acc[i + 1][j][rr * 4 + e];
-          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-              make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < TN; ++i) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int32_t n = tn * BN + wn * WN + i * 32 + rr * 8 + hi4;
-          if (n >= N) continue;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][rr * 4 + e];
-          if constexpr (EPI == EPI_RESID_F32) {
-            float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
-            float4 o = *p;
-            o.x += v[0];
-            o.y += v[1];
-            o.z += v[2];
-            o.w += v[3];
-            *p = o;
-          } else if constexpr (EPI == EPI_F32) {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n) =
-                make_float4(v[0], v[1], v[2], v[3]);
-          } else if constexpr (EPI == EPI_GELU_SAVE) {
-            *reinterpret_cast<float4*>(g.aux + (int64_t)m * g.ldaux + n) = make_float4(v[0], v[1], v[2], v[3]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-                make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-          } else if constexpr (EPI == EPI_GELUGRAD_BF16) {
-            const float4 z = *reinterpret_cast<const float4*>(g.aux + (int64_t)m * g.ldaux + n);
-            v[0] *= gelu_grad_f(z.x);
-            v[1] *= gelu_grad_f(z.y);
-            v[2] *= gelu_grad_f(z.z);
-            v[3] *= gelu_grad_f(z.w);
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-                make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-          } else {
-            if constexpr (EPI == EPI_GELU_BF16) {
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = gelu_fast_f(v[e]);
-            }
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-                make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-          }
-        }
-      }
-    }
-  }
+  gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
 }
 
 // Split-K: K range blockIdx.y of a launch whose g.K is the per-range length.
@@ -345,165 +351,169 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_grouped_kernel(const G
   gemm_tile<BN, BM, WGN, WGM, EPI>(g, b - g.tile_start, lds);
 }
 
-
-// Ping-pong variant of the 256x256 tile (8 wavefronts), used for the plain
-// bf16 and fp32-residual epilogues.  Waves w and w+4 share a SIMD; group 0
-// (waves 0-3) and group 1 (waves 4-7) alternate between a memory phase (all
-// 24 fragments of one K=64 slab from LDS, plus their share of a later slab's
-// DMA) and a compute phase (the slab's 32 MFMAs, which only read registers),
-// one workgroup barrier per phase, group 1 one phase behind group 0.  Slab
-// kt+1 is fetched by group 0 during its memory phase of slab kt and by group
-// 1 during its compute phase of slab kt-1; every wave waits for its own DMA
-// before the barrier that precedes the first read of that slab.  Per output
-// element the MFMA sequence (K order, operand lane layout) equals the
-// non-ping-pong kernel's, so both produce identical bits.  Measured against
-// the interleaved loop: +9.5% on the K=16384 residual projection, +4% on the
-// K=2048 one, equal or slightly better elsewhere; the GeGLU projection is 4%
-// slower with it and keeps the interleaved loop.
+// Ring-buffered ping-pong loop of the 256x256 tile (8 wavefronts).  Waves w
+// and w+4 share a SIMD; group 0 (waves 0-3) and group 1 (waves 4-7)
+// alternate between a memory phase (all 24 fragments of one K=64 slab from
+// LDS) and a compute phase (the slab's 64 MFMAs, which only read registers),
+// one workgroup barrier per phase, group 1 one phase behind group 0.  The LDS
+// holds two token slots and three weight slots of one slab each (5 x 32 KB =
+// 160 KB).  Group 0 fetches the token half of slab kt+1 as one burst at the
+// start of its memory phase of slab kt; group 1 fetches the weight half of
+// slab kt+3, spread over its compute phase of slab kt, into the slot slab kt
+// used.  Weight rows are thus requested two slabs ahead of their first read,
+// token rows one slab ahead; every wave waits for its own DMA before the
+// barrier that precedes the first read of that slab.  Measured on the
+// 2048-wide shapes (32x32x16 form): the third weight slot took the K=16384
+// residual projection from 4.81 to 4.50 ms over a two-slot ping-pong loop,
+// which was itself 9.5% faster there than the interleaved loop.  Split-K
+// ranges come from blockIdx.y as in gemm_kernel.
 template <int EPI>
-__global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs g) {
+__global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   constexpr int BN = 256, BM = 256, WGN = 2, WGM = 4;
-  constexpr int NW = WGN * WGM;
   constexpr int WN = BN / WGN, WM = BM / WGM;
-  constexpr int TN = WN / 32, TM = WM / 32;
-  constexpr int ROWS = BN + BM;
-  constexpr int NI = ROWS / (8 * NW);
-  constexpr int STAGE = ROWS * kBK;
-  static_assert(EPI == EPI_BF16 || EPI == EPI_RESID_F32, "ping-pong epilogues");
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * ROWS * kBK];
-  const uint16_t* __restrict__ X = g.X;
-  const uint16_t* __restrict__ W = g.W;
-  void* __restrict__ C = g.C;
-  const int64_t ldx = g.ldx, ldw = g.ldw, ldc = g.ldc;
-  const int32_t M = g.M, N = g.N, K = g.K, tiles_n = g.tiles_n, tiles_m = g.tiles_m;
-  const int32_t pid = blockIdx.x;
+  constexpr int TN = WN / 16, TM = WM / 16;
+  constexpr int NI = 8;            // 1 KB DMA instructions per wave per half-slab
+  constexpr int SLOT = 256 * kBK;  // elements per half-slab slot
+  constexpr bool GLU = EPI == EPI_GEGLU_BF16;
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * SLOT];
+  const GemmArgs g = split_range(g0);
+  const int32_t M = g.M, K = g.K;
 
-  const int32_t per_group = kGroupM * tiles_n;
-  const int32_t group = pid / per_group;
-  const int32_t first_m = group * kGroupM;
-  const int32_t gsize = min(tiles_m - first_m, kGroupM);
-  const int32_t tm = first_m + (pid % per_group) % gsize;
-  const int32_t tn = (pid % per_group) / gsize;
-
+  int32_t tm, tn;
+  tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave / WGM, wm = wave % WGM;
-  const int grp = wave >> 2;
+  const int grp = wave >> 2, sub = wave & 3;
 
+  // group 0: token rows 64*sub .. +63 of the tile; group 1: weight rows
   const uint16_t* src[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
-    const int row = 8 * (wave * NI + i) + (lane >> 3);
-    const int chunk = (lane & 7) ^ lds_swz(row);
-    if (row < BN)
-      src[i] = W + (int64_t)min(tn * BN + row, N - 1) * ldw + chunk * 8;
+    const int r = 64 * sub + 8 * i + (lane >> 3);
+    const int chunk = (lane & 7) ^ lds_swz(r);
+    if (grp == 0)
+      src[i] = g.X + (int64_t)min(tm * BM + r, M - 1) * g.ldx + chunk * 8;
     else
-      src[i] = X + (int64_t)min(tm * BM + row - BN, M - 1) * ldx + chunk * 8;
+      src[i] = weight_row<GLU>(g.W, g.W2, g.ldw, tn, BN, r, g.N) + chunk * 8;
   }
-  uint16_t* const dst0 = lds + wave * NI * 512;
+  const int dro = sub * NI * 512;  // this wave's 1 KB blocks inside a slot
+  uint16_t* const xs = lds;
+  uint16_t* const wsl = lds + 2 * SLOT;
 
-  f32x16 acc[TN][TM];
+  f32x4 acc[TN][TM];
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int KT = K / kBK;
-  const int sw = lds_swz(lane & 31), half = lane >> 5;
-  const int wrow = wn * WN + (lane & 31), xrow = BN + wm * WM + (lane & 31);
+  const int sw = lds_swz(lane & 15), quad = lane >> 4;
+  const int wrow = wn * WN + (lane & 15), xrow = wm * WM + (lane & 15);
 
-  // slab 0 from every wave; group 1 also issues its share of slab 1 and then
-  // waits one extra barrier, which puts it one phase behind group 0
+  // prologue: slab 0 whole, weight halves of slabs 1 and 2 in flight; group 1
+  // then waits one extra barrier, which puts it one phase behind group 0
+  if (grp == 0) {
 #pragma unroll
-  for (int i = 0; i < NI; ++i)
-    __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(dst0 + i * 512), 16, 0, 0);
-  wait_vmcnt<0>();
-  __builtin_amdgcn_s_barrier();
-  if (grp == 1) {
+    for (int i = 0; i < NI; ++i)
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(xs + dro + i * 512), 16, 0, 0);
+    wait_vmcnt<0>();
+  } else {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(wsl + dro + i * 512), 16, 0, 0);
     if (KT > 1) {
 #pragma unroll
       for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(dst0 + STAGE + i * 512), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(wsl + SLOT + dro + i * 512), 16, 0, 0);
+      wait_vmcnt<NI>();
+    } else {
+      wait_vmcnt<0>();
+    }
+  }
+  __builtin_amdgcn_s_barrier();
+  if (grp == 1) {
+    if (KT > 2) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + 2 * kBK), JN_LPTR(wsl + 2 * SLOT + dro + i * 512), 16, 0,
+                                         0);
     }
     __builtin_amdgcn_s_barrier();
   }
 
-  bf16x8 fw[4][TN], fx[4][TM];
+  bf16x8 fw[2][TN], fx[2][TM];
+  int wslot = 0;  // kt % 3
   for (int kt = 0; kt < KT; ++kt) {
-    const uint16_t* cur = lds + (kt & 1) * STAGE;
-    // ---- memory phase: slab kt's fragments (+ group 0's share of slab kt+1)
+    const uint16_t* cw = wsl + wslot * SLOT;
+    const uint16_t* cx = xs + (kt & 1) * SLOT;
+    // ---- memory phase: slab kt's fragments (+ group 0: token half of slab kt+1)
     __builtin_amdgcn_sched_barrier(0);
     if (grp == 0 && kt + 1 < KT) {
-      uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
+      uint16_t* const fdst = xs + ((kt + 1) & 1) * SLOT + dro;
 #pragma unroll
       for (int i = 0; i < NI; ++i)
         __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + 1) * kBK), JN_LPTR(fdst + i * 512), 16, 0, 0);
     }
 #pragma unroll
-    for (int step = 0; step < 4; ++step) {
-      const int pos = (2 * step + half) ^ sw;
-      gemm_frags<TN>(fw[step], cur, wrow, pos);
-      gemm_frags<TM>(fx[step], cur, xrow, pos);
+    for (int step = 0; step < 2; ++step) {
+      const int pos = (4 * step + quad) ^ sw;
+      gemm_frags<TN>(fw[step], cw, wrow, pos);
+      gemm_frags<TM>(fx[step], cx, xrow, pos);
     }
     wait_lgkmcnt<0>();
-    if (grp == 1) wait_vmcnt<0>();  // group 1's share of slab kt+1 (issued a phase earlier)
+    if (grp == 1) {  // weight half of slab kt+1 (the one of kt+2 may stay in flight)
+      if (kt + 2 < KT)
+        wait_vmcnt<NI>();
+      else
+        wait_vmcnt<0>();
+    }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // ---- compute phase: 32 MFMAs from registers (+ group 1's share of slab kt+2)
-    const bool fill = grp == 1 && kt + 2 < KT;
-    uint16_t* const gdst = dst0 + (kt & 1) * STAGE;
+    // ---- compute phase: 64 MFMAs from registers (+ group 1: weight half of slab kt+3)
+    const bool fill = grp == 1 && kt + 3 < KT;
+    uint16_t* const gdst = wsl + wslot * SLOT + dro;
 #pragma unroll
-    for (int step = 0; step < 4; ++step) {
+    for (int step = 0; step < 2; ++step) {
 #pragma unroll
       for (int q = 0; q < TN * TM; ++q) {
         const int i = q / TM, j = q % TM;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[step][i], fx[step][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[step][i], fx[step][j], acc[i][j], 0, 0, 0);
         const int d = step * TN * TM + q;
-        if ((d & 3) == 3 && fill)
-          __builtin_amdgcn_global_load_lds(JN_GPTR(src[d >> 2] + (kt + 2) * kBK), JN_LPTR(gdst + (d >> 2) * 512),
-                                           16, 0, 0);
+        if ((d & 7) == 7 && fill)
+          __builtin_amdgcn_global_load_lds(JN_GPTR(src[d >> 3] + (kt + 3) * kBK), JN_LPTR(gdst + (d >> 3) * 512), 16,
+                                           0, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if (grp == 0) wait_vmcnt<0>();  // group 0's share of slab kt+1
+    if (grp == 0) wait_vmcnt<0>();  // token half of slab kt+1
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    wslot = wslot == 2 ? 0 : wslot + 1;
   }
   if (grp == 0) __builtin_amdgcn_s_barrier();  // equal barrier counts in both groups
 
-  const int hi4 = (lane >> 5) * 4;
-#pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int32_t m = tm * BM + wm * WM + j * 32 + (lane & 31);
-    if (m >= M) continue;
-#pragma unroll
-    for (int i = 0; i < TN; ++i) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int32_t n = tn * BN + wn * WN + i * 32 + rr * 8 + hi4;
-        if (n >= N) continue;
-        float a[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) a[e] = acc[i][j][rr * 4 + e];
-        if constexpr (EPI == EPI_RESID_F32) {
-          float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
-          float4 o = *p;
-          o.x += a[0];
-          o.y += a[1];
-          o.z += a[2];
-          o.w += a[3];
-          *p = o;
-        } else {
-          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-              make_uint2(pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]));
-        }
-      }
-    }
+  gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
+}
+
+// The 256x256 ring loop over all tiles of g (grid.y = split-K ranges).
+static hipError_t launch_ring(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1) {
+  const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
+  g.tiles_m = (g.M + 255) / 256;
+  g.tiles_n = (NL + 255) / 256;
+  g.tile_start = 0;
+  const dim3 grid(g.tiles_m * g.tiles_n, splits), block(512);
+  switch (epi) {
+    case EPI_BF16: gemm_ring_kernel<EPI_BF16><<<grid, block, 0, s>>>(g); break;
+    case EPI_GELU_BF16: gemm_ring_kernel<EPI_GELU_BF16><<<grid, block, 0, s>>>(g); break;
+    case EPI_RESID_F32: gemm_ring_kernel<EPI_RESID_F32><<<grid, block, 0, s>>>(g); break;
+    case EPI_GEGLU_BF16: gemm_ring_kernel<EPI_GEGLU_BF16><<<grid, block, 0, s>>>(g); break;
+    case EPI_F32: gemm_ring_kernel<EPI_F32><<<grid, block, 0, s>>>(g); break;
+    default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
 }
 
 template <int BN, int BM, int WGN, int WGM>
@@ -616,6 +626,55 @@ size_t gemm_split_bytes(int epi, int32_t M, int32_t N, int32_t K) {
   return S > 1 ? (size_t)S * M * N * sizeof(float) : 0;
 }
 
+// One launch over all rows of g with tile shape t (0: 256x256 ring loop,
+// 1: 256x128, 2: 128x128).
+static hipError_t launch_rows(hipStream_t s, int epi, GemmArgs g, int t) {
+  switch (t) {
+    case 0: return launch_ring(s, epi, g);
+    case 1: return launch_tile<256, 128, 4, 2>(s, epi, g);
+    default: return launch_tile<128, 128, 2, 2>(s, epi, g);
+  }
+}
+
+// Row split against the last, partly filled wave of tiles: rows [0, m1) run
+// with tile shape t1 and rows [m1, M) as a second launch with a smaller shape
+// t2, chosen by the same time estimate as gemm_plan (tile-waves over the 256
+// CUs, per-shape efficiency) plus the gap between two launches.  For example
+// 2,368 tiles of 256x256 (9.25 waves) become 9 full waves plus one wave of
+// 128x128 tiles at about a third of the cost.  Every tile shape runs the same
+// MFMA sequence per output element, so the split does not change any bit.
+constexpr double kLaunchGap = 6e-6;  // seconds between two launches on one stream
+
+static void gemm_plan_rows(int epi, int32_t M, int32_t N, int32_t K, int* t1, int32_t* m1, int* t2) {
+  const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * N : N;
+  static const int bn[3] = {256, 256, 128}, bm[3] = {256, 128, 128};
+  static const double eff[3] = {1.0, 1.12, 1.35};
+  auto cost_of = [&](int t, int32_t rows) {
+    const int64_t tiles = (int64_t)((rows + bm[t] - 1) / bm[t]) * ((NL + bn[t] - 1) / bn[t]);
+    const double waves = (double)((tiles + kSplitCUs - 1) / kSplitCUs);
+    return waves * 2.0 * bn[t] * bm[t] * eff[t] * (double)K / kCuFlops;
+  };
+  *t1 = gemm_pick_tile(epi, M, N);
+  *m1 = M;
+  *t2 = *t1;
+  double best = cost_of(*t1, M);
+  for (int a = 0; a < 2; ++a) {
+    const int32_t tma = (M + bm[a] - 1) / bm[a];
+    for (int32_t r = tma - 1; r >= 1 && r >= tma - 64; --r) {
+      const int32_t ma = r * bm[a];
+      for (int b = a + 1; b < 3; ++b) {
+        const double cost = cost_of(a, ma) + cost_of(b, M - ma) + kLaunchGap;
+        if (cost < best * 0.98) {
+          best = cost;
+          *t1 = a;
+          *m1 = ma;
+          *t2 = b;
+        }
+      }
+    }
+  }
+}
+
 hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2, int64_t ldb,
                        void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int tile_hint, void* split_ws,
                        size_t split_bytes) {
@@ -636,7 +695,7 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
     g.split_c = (int64_t)M * N;
     hipError_t e;
     switch (t_split) {
-      case 0: e = launch_tile<256, 256, 2, 4>(s, EPI_F32, g, S); break;
+      case 0: e = launch_ring(s, EPI_F32, g, S); break;
       case 1: e = launch_tile<256, 128, 4, 2>(s, EPI_F32, g, S); break;
       default: e = launch_tile<128, 128, 2, 2>(s, EPI_F32, g, S); break;
     }
@@ -661,26 +720,25 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
   g.ldx = lda;
   g.ldw = ldb;
   g.ldc = ldc;
-  g.M = M;
   g.N = N;
   g.K = K;
-  const int t = tile_hint > 0 ? tile_hint - 1 : gemm_pick_tile(epi, M, N);
-  switch (t) {
-    case 0:
-      if (epi == EPI_BF16 || epi == EPI_RESID_F32) {
-        g.tiles_m = (g.M + 255) / 256;
-        g.tiles_n = (g.N + 255) / 256;
-        g.tile_start = 0;
-        if (epi == EPI_BF16)
-          gemm_pp_kernel<EPI_BF16><<<dim3(g.tiles_m * g.tiles_n), dim3(512), 0, s>>>(g);
-        else
-          gemm_pp_kernel<EPI_RESID_F32><<<dim3(g.tiles_m * g.tiles_n), dim3(512), 0, s>>>(g);
-        return hipGetLastError();
-      }
-      return launch_tile<256, 256, 2, 4>(s, epi, g);
-    case 1: return launch_tile<256, 128, 4, 2>(s, epi, g);
-    default: return launch_tile<128, 128, 2, 2>(s, epi, g);
+  if (tile_hint > 0) {
+    g.M = M;
+    return launch_rows(s, epi, g, tile_hint - 1);
   }
+  int t1, t2;
+  int32_t m1;
+  gemm_plan_rows(epi, M, N, K, &t1, &m1, &t2);
+  if (m1 > 0) {
+    g.M = m1;
+    const hipError_t e = launch_rows(s, epi, g, t1);
+    if (e != hipSuccess || m1 == M) return e;
+  }
+  const size_t esize = (epi == EPI_RESID_F32 || epi == EPI_F32) ? 4 : 2;
+  g.X += (int64_t)m1 * lda;
+  g.C = static_cast<char*>(C) + (size_t)m1 * ldc * esize;
+  g.M = M - m1;
+  return launch_rows(s, epi, g, t2);
 }
 
 int gemm_grouped_tile_shape(int32_t max_m) { return max_m >= 1024 ? 1 : 2; }
