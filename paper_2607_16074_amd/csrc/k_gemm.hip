@@ -351,6 +351,98 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_grouped_kernel(const G
   gemm_tile<BN, BM, WGN, WGM, EPI>(g, b - g.tile_start, lds);
 }
 
+// Epilogues of the 256x256 ring loop that stage the tile through the (then
+// free) LDS so that global memory sees whole rows: 16-byte lanes, each wave
+// instruction covering complete 128-byte lines.  Written directly from the
+// MFMA layout, each lane would touch 8 or 16 bytes of 16 different rows per
+// instruction.  Measured on the 2048-wide shapes: QKV (bf16) 1.70-1.78 ->
+// 1.61 ms, O (fp32 residual, K=2048) 0.716 -> 0.690 ms; the GeGLU tile (half
+// as many columns, GELU-bound) gains nothing and keeps the direct path.
+// The caller has passed a barrier after the last fragment read.
+//
+// bf16 / GELU-bf16: the whole 256 x 256 tile (row stride padded by 16 bytes,
+// 132 KB), then 32 rows per wave, 2 rows per instruction.
+template <int EPI>
+__device__ __forceinline__ void ring_epilogue_bf16(const GemmArgs& g, const f32x4 (&acc)[8][4], uint16_t* lds,
+                                                   int32_t tm, int32_t tn, int wn, int wm, int wave, int lane) {
+  constexpr int OS = 256 + 8;  // LDS row stride (elements)
+  const int q4 = (lane >> 4) * 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = wm * 64 + j * 16 + (lane & 15);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = EPI == EPI_GELU_BF16 ? gelu_fast_f(acc[i][j][e]) : acc[i][j][e];
+      *reinterpret_cast<uint2*>(lds + row * OS + wn * 128 + i * 16 + q4) =
+          make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+    }
+  }
+  wait_lgkmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  const int c = lane & 31, rr = lane >> 5;  // 32 chunks of 16 bytes per row
+  const int32_t n = tn * 256 + c * 8;
+#pragma unroll
+  for (int it = 0; it < 16; ++it) {
+    const int row = wave * 32 + it * 2 + rr;
+    const int32_t m = tm * 256 + row;
+    const uint4 v = *reinterpret_cast<const uint4*>(lds + row * OS + c * 8);
+    if (m < g.M && n < g.N) *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(g.C) + (int64_t)m * g.ldc + n) = v;
+  }
+}
+
+// fp32 residual add: two halves of 128 token rows (row stride padded by 16
+// bytes, 130 KB each); in each half the waves holding those rows write them,
+// then every wave adds 16 whole 1 KB rows into C.
+__device__ __forceinline__ void ring_epilogue_resid(const GemmArgs& g, const f32x4 (&acc)[8][4], uint16_t* lds,
+                                                    int32_t tm, int32_t tn, int wn, int wm, int wave, int lane) {
+  constexpr int OS = 256 + 4;  // LDS row stride (floats)
+  float* const ot = reinterpret_cast<float*>(lds);
+  const int q4 = (lane >> 4) * 4;
+  const int32_t n = tn * 256 + lane * 4;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    if ((wm >> 1) == half) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = (wm & 1) * 64 + j * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          *reinterpret_cast<float4*>(ot + row * OS + wn * 128 + i * 16 + q4) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+    wait_lgkmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    float4 cv[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int32_t m = tm * 256 + half * 128 + wave * 16 + it;
+      if (m < g.M && n < g.N)
+        cv[it] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g.C) + (int64_t)m * g.ldc + n);
+    }
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int row = wave * 16 + it;
+      const int32_t m = tm * 256 + half * 128 + row;
+      if (m < g.M && n < g.N) {
+        const float4 a = *reinterpret_cast<const float4*>(ot + row * OS + lane * 4);
+        float4 o = cv[it];
+        o.x += a.x;
+        o.y += a.y;
+        o.z += a.z;
+        o.w += a.w;
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.C) + (int64_t)m * g.ldc + n) = o;
+      }
+    }
+    if (half == 0) {  // the second half's writes reuse the buffer
+      wait_lgkmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    }
+  }
+}
+
 // Ring-buffered ping-pong loop of the 256x256 tile (8 wavefronts).  Waves w
 // and w+4 share a SIMD; group 0 (waves 0-3) and group 1 (waves 4-7)
 // alternate between a memory phase (all 24 fragments of one K=64 slab from
@@ -495,7 +587,12 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   }
   if (grp == 0) __builtin_amdgcn_s_barrier();  // equal barrier counts in both groups
 
-  gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_GELU_BF16)
+    ring_epilogue_bf16<EPI>(g, acc, lds, tm, tn, wn, wm, wave, lane);
+  else if constexpr (EPI == EPI_RESID_F32)
+    ring_epilogue_resid(g, acc, lds, tm, tn, wn, wm, wave, lane);
+  else
+    gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
 }
 
 // The 256x256 ring loop over all tiles of g (grid.y = split-K ranges).
