@@ -391,7 +391,7 @@ def main():
         "speedup_vs_isolated": (iso_ms / (t_step * 1e3)) if iso_ms else None,
         "backbone_gemm_tflops": gemm_tflops,
         "backbone_gemm_frac_of_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS,
-        "roofline": {"bound": "mfma", "kernel": f"gemm_kernel ({dom}, {spec.backbone.d}-wide)",
+        "roofline": {"bound": "mfma", "kernel": f"{dom} projection GEMM ({spec.backbone.d}-wide; gemm_ring_kernel tiles)",
                      "achieved": gs["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(args.config),
                      "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},

@@ -36,12 +36,13 @@ __device__ __forceinline__ float gelu_f(float u) {
   return 0.5f * u * (1.0f + tanhf(c * (u + 0.044715f * u * u * u)));
 }
 
-// The same tanh-form GELU written as u * sigmoid(2 sqrt(2/pi) (u + 0.044715 u^3))
-// with the hardware exp2 / reciprocal (relative error ~1e-6, far below the
-// bf16 rounding of the values it produces).  Used in GEMM epilogues.
+// The same tanh-form GELU written as u / (1 + 2^(y)), y = -log2(e) * 2 sqrt(2/pi)
+// * (u + 0.044715 u^3), with the log2(e) factor folded into the polynomial and
+// the hardware exp2 / reciprocal (relative error ~1e-6, far below the bf16
+// rounding of the values it produces).  Used in GEMM epilogues.
 __device__ __forceinline__ float gelu_fast_f(float u) {
-  const float z = u * (1.5957691216057308f + 0.07135481627260025f * u * u);
-  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+  const float y = u * (-2.302208198144325f - 0.1029432395800235f * u * u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(y));
 }
 
 __device__ __forceinline__ float gelu_grad_f(float u) {
