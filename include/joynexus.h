@@ -219,7 +219,10 @@ typedef struct jn_layer {
  *                 rotated by p * rope_theta^(-2i/hd); 0: no positions
  * Arithmetic: bf16 GEMM / attention operands with fp32 accumulation, fp32
  * residual stream, fp32 norm / softmax / rotation math, bf16 stored
- * activations (q and k are stored rotated, rounded once more). */
+ * activations (q and k are stored rotated, rounded once more).
+ * Supported sizes: d a multiple of 128 in [128, 4096], ffn a multiple of 128,
+ * head dim d / n_heads in {32, 64, 128, 256}; other sizes fail with
+ * JN_EUNSUPPORTED before anything is enqueued. */
 typedef struct jn_backbone {
   int32_t n_layers, d, n_heads, ffn;
   float eps;

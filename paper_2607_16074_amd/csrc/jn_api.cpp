@@ -481,7 +481,8 @@ jn_status check_backbone(jn_ctx* c, const jn_backbone* bb) {
   int hd = bb->d / bb->n_heads;
   if (hd != 32 && hd != 64 && hd != 128 && hd != 256)
     return fail(c, JN_EUNSUPPORTED, "head dim %d not in {32,64,128,256}", hd);
-  if (bb->d % 128 != 0) return fail(c, JN_EUNSUPPORTED, "d %d not a multiple of 128", bb->d);
+  if (bb->d % 128 != 0 || bb->d > 4096)
+    return fail(c, JN_EUNSUPPORTED, "d %d not a multiple of 128 in [128, 4096]", bb->d);
   if (bb->ffn % 128 != 0) return fail(c, JN_EUNSUPPORTED, "ffn %d not a multiple of 128", bb->ffn);
   if (!(bb->eps > 0.f)) return fail(c, JN_EINVAL, "eps must be > 0");
   const int kv = bb->n_kv_heads ? bb->n_kv_heads : bb->n_heads;

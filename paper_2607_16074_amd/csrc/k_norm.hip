@@ -119,7 +119,7 @@ static hipError_t launch_rms(hipStream_t s, const void* x, float* x_out, const v
   JN_RMS(8, 8)   // 4096
   // any other multiple of 128 up to 4096: two elements per lane per chunk
 #define JN_RMS2(NC) JN_RMS(2, NC)
-  JN_RMS2(5) JN_RMS2(7) JN_RMS2(9) JN_RMS2(10) JN_RMS2(11) JN_RMS2(13) JN_RMS2(14) JN_RMS2(15)
+  JN_RMS2(3) JN_RMS2(5) JN_RMS2(7) JN_RMS2(9) JN_RMS2(10) JN_RMS2(11) JN_RMS2(13) JN_RMS2(14) JN_RMS2(15)
   JN_RMS2(17) JN_RMS2(18) JN_RMS2(19) JN_RMS2(20) JN_RMS2(21) JN_RMS2(22) JN_RMS2(23) JN_RMS2(25)
   JN_RMS2(26) JN_RMS2(27) JN_RMS2(28) JN_RMS2(29) JN_RMS2(30) JN_RMS2(31)
 #undef JN_RMS2

@@ -293,6 +293,24 @@ def test_split_k_short_batch_2b(jn):
     assert rel_l2(st.ios[0].actions.cpu().numpy(), tres["actions"]) < GRAD_TOL
 
 
+def test_ragged_weight_widths_on_the_large_tile(jn):
+    """The 256x256 GEMM tile with weight widths that are not multiples of 256
+    (QKV 1152, O and down 384, so their last column tile is half outside):
+    ~77K tokens make the tile planner choose that tile for these projections,
+    so its load clamps and the staged epilogues' column bounds run on partial
+    tiles.  Oracle on the first, a middle and the last sample."""
+    ten = tuple(W.TenantSpec(130, 256, 16, 64, 320, (384, 64, 6), 3, 2) for _ in range(2))
+    spec = W.WorkloadSpec(94, W.BackboneSpec(2, 384, 6, 1408, True), ten, 0, "ragged widths")
+    wl = W.make_workload(spec)
+    T = int(sum(int(q.lengths.sum()) for q in wl.requests))
+    _say(f"ragged widths: d=384 ffn=1408 GeGLU, {T} tokens")
+    st = run_group(wl)
+    last = len(wl.requests) - 1
+    keys = [(0, 0), (0, wl.requests[0].n // 2), (last, wl.requests[last].n - 1)]
+    worst = _check_backbone(wl, st, keys)
+    _say(f"  worst hidden max-rel {worst:.3e}")
+
+
 def test_single_sample_of_length_one(jn):
     """The smallest batch: one tenant, one request, one sample of one token,
     padded to a canonical length of 4 (degenerate attention: softmax over one
@@ -312,8 +330,24 @@ def test_single_sample_of_length_one(jn):
 
 def test_grouped_equals_isolated_bitwise(jn):
     """The defining invariant (Sec. 5.2): grouping changes no tenant's result."""
+    _grouped_equals_isolated(W.make_workload(2))
+
+
+def test_grouped_equals_isolated_bitwise_geglu(jn):
+    """The same invariant across GEMM loops and tile shapes: a GeGLU backbone
+    where the 2-sample tenant's rows (first in the packed batch) go through
+    the 256x256 ring loop in the grouped run (~18K tokens) and through 128x128
+    tiles of the interleaved loop in its own run (~600 tokens).  ffn = 1920
+    keeps every launch of both runs unsplit over K (a K split adds fp32
+    partials in another order, the one documented exception)."""
+    ten = (W.TenantSpec(2, 256, 16, 64, 320, (512, 64, 6), 3, 2), W.TenantSpec(60, 256, 16, 64, 320, (512, 64, 6), 3, 2))
+    spec = W.WorkloadSpec(95, W.BackboneSpec(2, 512, 4, 1920, True), ten, 0, "geglu bitwise")
+    _say("grouped == isolated, GeGLU backbone, 2 + 60 samples")
+    _grouped_equals_isolated(W.make_workload(spec))
+
+
+def _grouped_equals_isolated(wl):
     from paper_2607_16074_amd import step as jstep
-    wl = W.make_workload(2)
     model, reqs, targets = jstep.from_workload(wl)
     grouped = jstep.GroupStep(model, reqs, targets, list(range(wl.spec.G)))
     grouped.run()
@@ -385,5 +419,12 @@ def test_errors_enqueue_nothing(jn):
     with pytest.raises(jn.JNError) as e:
         jn.jn_tenant_heads_fwd_bwd(st.ctx, st.packed, st.hidden, st.heads[:1], st.ios[:1], st.hd_ws)
     assert e.value.status == jn._abi.JN_EINVAL
+
+    class _Wide:  # the same layers described with a width beyond the kernels' range
+        struct = jn._abi.jn_backbone.from_buffer_copy(st.model.backbone.struct)
+    _Wide.struct.d, _Wide.struct.n_heads = 4224, 33
+    with pytest.raises(jn.JNError) as e:
+        jn.jn_backbone_forward(st.ctx, _Wide, st.packed, st.hidden, small)
+    assert e.value.status == jn._abi.JN_EUNSUPPORTED
     torch.cuda.synchronize()
     assert torch.equal(before, st.hidden)
