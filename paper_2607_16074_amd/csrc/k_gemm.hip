@@ -27,12 +27,14 @@
 // (gemm_ring_kernel); the smaller tiles of short launches and of the grouped
 // per-tenant launches run an interleaved double-buffered loop (gemm_tile).
 //
-// Launch order: tiles are walked in groups of 16 token-tiles (token tile
-// fastest).  Workgroups are dealt round-robin to the 8 XCDs, so each XCD's
-// resident tiles share a token tile and walk the weight tiles, and every
-// weight slab is requested by all XCDs at about the same time.  Measured on
-// the 2048-wide workloads, giving each XCD a contiguous block of tiles (an
-// explicit XCD remap) is no faster with 4x8 blocks and 13% slower with 16x2.
+// Launch order: tiles are walked in groups of 32 token-tiles (token tile
+// fastest).  Workgroups are dealt round-robin to the 8 XCDs, so the 32 tiles
+// an XCD holds at a time form a block of 4 token tiles x 8 weight tiles, and
+// every weight slab is requested by all XCDs at about the same time.
+// Measured in the step on the 2048-wide workload: groups of 32 give 290.1 ms
+// per step against 292.9 (16), 298.7 (8), 292.0 (64) and 300.6 (128); an
+// explicit XCD remap giving each XCD a contiguous block of tiles was no
+// faster with 4x8 blocks and 13% slower with 16x2 (32x32x16 loop).
 //
 // Epilogues: bf16 store, GELU -> bf16, fp32 residual add (in place), fp32
 // store, GELU with fp32 pre-activation save, GELU' product, and GeGLU, whose
@@ -52,7 +54,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 64;       // K per slab (128-byte rows)
 constexpr int kStages = 2;    // double buffer of the interleaved loop
-constexpr int kGroupM = 16;   // token tiles per L2 group
+constexpr int kGroupM = 32;   // token tiles per L2 group
 
 __device__ __forceinline__ int lds_swz(int r) { return (r >> 1) & 7; }
 
@@ -165,7 +167,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x4 (&a
   }
 }
 
-// Position of tile pid in the grouped walk (16 token tiles per group).
+// Position of tile pid in the grouped walk (kGroupM token tiles per group).
 __device__ __forceinline__ void tile_of(int32_t pid, int32_t tiles_m, int32_t tiles_n, int32_t& tm, int32_t& tn) {
   const int32_t per_group = kGroupM * tiles_n;
   const int32_t first_m = (pid / per_group) * kGroupM;
