@@ -158,7 +158,19 @@ def cpu_oracle_baseline(wl, budget_s=25.0):
     return {"value": 1.0 / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"1 of {sum(q.n for q in wl.requests)} samples ({L} tokens): full backbone forward in fp64 "
                       f"+ {what}; {dt:.1f} s on the host",
-            "seconds": dt, "host_cpus": os.cpu_count()}
+            "seconds": dt, "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or "" where unavailable."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 def local_batch_sweep(model, reqs, targets, steps, warmup, tenants_list=(2, 4, 6, 8), batches=(1, 2, 4, 8)):
@@ -398,7 +410,8 @@ def main():
         "gemm_by_op": gemm_stats,
         "kernels": kernel_rates(by_op, args.steps, spec, reqs, grouped.T, valid, N),
         "tenant_optimizer": opt_stats,
-        "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample")},
+        "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample",
+                                                                      "host_cpus", "cpu_model")},
     }
     print(json.dumps(result), flush=True)
 
