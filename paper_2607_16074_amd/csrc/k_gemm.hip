@@ -450,17 +450,22 @@ __device__ __forceinline__ void ring_epilogue_resid(const GemmArgs& g, const f32
 // alternate between a memory phase (all 24 fragments of one K=64 slab from
 // LDS) and a compute phase (the slab's 64 MFMAs, which only read registers),
 // one workgroup barrier per phase, group 1 one phase behind group 0.  The LDS
-// holds two token slots and three weight slots of one slab each (5 x 32 KB =
-// 160 KB).  Group 0 fetches the token half of slab kt+1 as one burst at the
-// start of its memory phase of slab kt; group 1 fetches the weight half of
+// holds two weight slots and three token slots of one slab each (5 x 32 KB =
+// 160 KB).  Group 0 fetches the weight half of slab kt+1 as one burst at the
+// start of its memory phase of slab kt; group 1 fetches the token half of
 // slab kt+3, spread over its compute phase of slab kt, into the slot slab kt
-// used.  Weight rows are thus requested two slabs ahead of their first read,
-// token rows one slab ahead; every wave waits for its own DMA before the
+// used.  Token rows are thus requested two slabs ahead of their first read,
+// weight rows one slab ahead; every wave waits for its own DMA before the
 // barrier that precedes the first read of that slab.  Measured on the
-// 2048-wide shapes (32x32x16 form): the third weight slot took the K=16384
-// residual projection from 4.81 to 4.50 ms over a two-slot ping-pong loop,
-// which was itself 9.5% faster there than the interleaved loop.  Split-K
-// ranges come from blockIdx.y as in gemm_kernel.
+// 2048-wide shapes: a third slot took the K=16384 residual projection from
+// 4.81 to 4.50 ms over a two-slot ping-pong loop (32x32x16 form), which was
+// itself 9.5% faster there than the interleaved loop; giving the third slot
+// to the token operand instead of the weights made the 2B-shaped step
+// 0.8-2.6% faster (the weight slabs, read by every XCD at about the same
+// time, arrive sooner than the token slabs).  Issuing the token DMA in the
+// first half of the compute phase instead of spreading it over the whole
+// phase made the step 3% slower.  Split-K ranges come from blockIdx.y as in
+// gemm_kernel.
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   constexpr int BN = 256, BM = 256, WGN = 2, WGM = 4;
@@ -480,20 +485,20 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   const int wn = wave / WGM, wm = wave % WGM;
   const int grp = wave >> 2, sub = wave & 3;
 
-  // group 0: token rows 64*sub .. +63 of the tile; group 1: weight rows
+  // group 0: weight rows 64*sub .. +63 of the tile; group 1: token rows
   const uint16_t* src[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int r = 64 * sub + 8 * i + (lane >> 3);
     const int chunk = (lane & 7) ^ lds_swz(r);
-    if (grp == 0)
+    if (grp == 1)
       src[i] = g.X + (int64_t)min(tm * BM + r, M - 1) * g.ldx + chunk * 8;
     else
       src[i] = weight_row<GLU>(g.W, g.W2, g.ldw, tn, BN, r, g.N) + chunk * 8;
   }
   const int dro = sub * NI * 512;  // this wave's 1 KB blocks inside a slot
-  uint16_t* const xs = lds;
-  uint16_t* const wsl = lds + 2 * SLOT;
+  uint16_t* const ring2 = lds;             // weight slabs, slot kt % 2
+  uint16_t* const ring3 = lds + 2 * SLOT;  // token slabs, slot kt % 3
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -505,21 +510,21 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = wm * WM + (lane & 15);
 
-  // prologue: slab 0 whole, weight halves of slabs 1 and 2 in flight; group 1
+  // prologue: slab 0 whole, token halves of slabs 1 and 2 in flight; group 1
   // then waits one extra barrier, which puts it one phase behind group 0
   if (grp == 0) {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(xs + dro + i * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(ring2 + dro + i * 512), 16, 0, 0);
     wait_vmcnt<0>();
   } else {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(wsl + dro + i * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(ring3 + dro + i * 512), 16, 0, 0);
     if (KT > 1) {
 #pragma unroll
       for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(wsl + SLOT + dro + i * 512), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(ring3 + SLOT + dro + i * 512), 16, 0, 0);
       wait_vmcnt<NI>();
     } else {
       wait_vmcnt<0>();
@@ -530,21 +535,21 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
     if (KT > 2) {
 #pragma unroll
       for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + 2 * kBK), JN_LPTR(wsl + 2 * SLOT + dro + i * 512), 16, 0,
+        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + 2 * kBK), JN_LPTR(ring3 + 2 * SLOT + dro + i * 512), 16, 0,
                                          0);
     }
     __builtin_amdgcn_s_barrier();
   }
 
   bf16x8 fw[2][TN], fx[2][TM];
-  int wslot = 0;  // kt % 3
+  int slot3 = 0;  // kt % 3
   for (int kt = 0; kt < KT; ++kt) {
-    const uint16_t* cw = wsl + wslot * SLOT;
-    const uint16_t* cx = xs + (kt & 1) * SLOT;
-    // ---- memory phase: slab kt's fragments (+ group 0: token half of slab kt+1)
+    const uint16_t* cw = ring2 + (kt & 1) * SLOT;
+    const uint16_t* cx = ring3 + slot3 * SLOT;
+    // ---- memory phase: slab kt's fragments (+ group 0: weight half of slab kt+1)
     __builtin_amdgcn_sched_barrier(0);
     if (grp == 0 && kt + 1 < KT) {
-      uint16_t* const fdst = xs + ((kt + 1) & 1) * SLOT + dro;
+      uint16_t* const fdst = ring2 + ((kt + 1) & 1) * SLOT + dro;
 #pragma unroll
       for (int i = 0; i < NI; ++i)
         __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + 1) * kBK), JN_LPTR(fdst + i * 512), 16, 0, 0);
@@ -556,7 +561,7 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
       gemm_frags<TM>(fx[step], cx, xrow, pos);
     }
     wait_lgkmcnt<0>();
-    if (grp == 1) {  // weight half of slab kt+1 (the one of kt+2 may stay in flight)
+    if (grp == 1) {  // token half of slab kt+1 (the one of kt+2 may stay in flight)
       if (kt + 2 < KT)
         wait_vmcnt<NI>();
       else
@@ -565,9 +570,9 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // ---- compute phase: 64 MFMAs from registers (+ group 1: weight half of slab kt+3)
+    // ---- compute phase: 64 MFMAs from registers (+ group 1: token half of slab kt+3)
     const bool fill = grp == 1 && kt + 3 < KT;
-    uint16_t* const gdst = wsl + wslot * SLOT + dro;
+    uint16_t* const gdst = ring3 + slot3 * SLOT + dro;
 #pragma unroll
     for (int step = 0; step < 2; ++step) {
 #pragma unroll
@@ -581,11 +586,11 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if (grp == 0) wait_vmcnt<0>();  // token half of slab kt+1
+    if (grp == 0) wait_vmcnt<0>();  // weight half of slab kt+1
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    wslot = wslot == 2 ? 0 : wslot + 1;
+    slot3 = slot3 == 2 ? 0 : slot3 + 1;
   }
   if (grp == 0) __builtin_amdgcn_s_barrier();  // equal barrier counts in both groups
 
