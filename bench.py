@@ -69,6 +69,28 @@ def copy_calibration(mib: int = 512):
     del a, b
 
 
+def copy_reference(mib: int = 1024, reps: int = 20) -> dict:
+    """The practical rate of a stream that reads and writes HBM once: a plain
+    device-to-device copy (torch copy_), timed with events after warm-up."""
+    import torch
+    a = torch.empty(mib << 18, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    gbs = 2.0 * (mib << 20) / (ms * 1e-3) / 1e9
+    return {"what": f"{mib} MiB device-to-device copy (torch copy_), read + write", "ms": ms, "GB_per_s": gbs,
+            "frac_of_hbm": gbs / PEAK_HBM_GBS}
+
+
 def gemm_flops_per_token(bb) -> dict:
     d, f = bb.d, bb.ffn
     up = 2 * (2 * f if bb.glu else f) * d
@@ -376,6 +398,15 @@ def main():
         log(f"cpu oracle: {cpu['value']:.4f} samples/s on {cpu['cores']} threads")
 
     gs = gemm_stats[dom]
+    # reference rate for the HBM-bound kernels, measured after the timed steps
+    copy_ref = copy_reference()
+    kernels = kernel_rates(by_op, args.steps, spec, reqs, grouped.T, valid, N)
+    for v in kernels.values():
+        if "GB_per_s" in v:
+            v["frac_of_copy"] = v["GB_per_s"] / copy_ref["GB_per_s"]
+    if opt_stats is not None:
+        opt_stats["frac_of_copy"] = opt_stats["GB_per_s"] / copy_ref["GB_per_s"]
+    log(f"copy reference: {copy_ref['GB_per_s']:.0f} GB/s")
     result = {
         "metric": METRIC,
         "value": N / t_step,
@@ -408,7 +439,8 @@ def main():
                      "frac": gs["tflops"] / PEAK_BF16_TFLOPS, "traffic": measured_traffic(args.config),
                      "avg_launch_ms": gs["avg_ms"], "flops_per_launch": fpt[dom] * valid},
         "gemm_by_op": gemm_stats,
-        "kernels": kernel_rates(by_op, args.steps, spec, reqs, grouped.T, valid, N),
+        "kernels": kernels,
+        "copy_reference": copy_ref,
         "tenant_optimizer": opt_stats,
         "cpu_baseline": None if cpu is None else {k: cpu[k] for k in ("value", "unit", "cores", "kind", "sample",
                                                                       "host_cpus", "cpu_model")},

@@ -14,53 +14,58 @@ namespace jnx {
 
 // ------------------------------------------------------------------ pool ---
 
-// Block = (64-column chunk, sample); 256 threads = 8 column groups (8
-// columns, one 16-byte load each) x 32 row lanes.  Row lane r sums rows
-// r, r+32, r+64, ... of the sample; the 32 lane sums are then combined by a
-// fixed pairwise tree in LDS.  The order depends only on the sample's own
-// length, so a sample pools to the same bits in any batch.
-constexpr int kPoolCols = 64;
-constexpr int kPoolLanes = 32;
+// Block = (sample, 512-column chunk); 256 threads = 4 wavefronts, lane l
+// owning columns 8 l .. 8 l + 7 (one 16-byte load covers 1 KB of a row per
+// wave).  Wave w sums rows w, w+4, w+8, ... of the sample in that order, four
+// loads in flight per lane; the four wave sums are combined as
+// (s0 + s1) + (s2 + s3).  The order depends only on the sample's own length,
+// so a sample pools to the same bits in any batch.
+constexpr int kPoolCols = 512;
+constexpr int kPoolWaves = 4;
 
 __global__ __launch_bounds__(256) void pool_kernel(const uint16_t* __restrict__ hidden,
                                                    const int32_t* __restrict__ seqlens,
                                                    const int32_t* __restrict__ cu_seqlens,
                                                    const int32_t* __restrict__ rank, int32_t d,
                                                    float* __restrict__ pooled) {
-  __shared__ float red[kPoolLanes][kPoolCols + 1];
+  __shared__ float red[kPoolWaves][kPoolCols];
   const int32_t chunks = (d + kPoolCols - 1) / kPoolCols;
   const int32_t i = blockIdx.x / chunks;
   const int32_t c0 = (blockIdx.x % chunks) * kPoolCols;
   const int32_t L = seqlens[i];
-  const int cg = threadIdx.x & 7, r = threadIdx.x >> 3;
-  const int32_t col = c0 + cg * 8;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int32_t col = c0 + lane * 8;
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
   if (col < d) {
     const uint16_t* base = hidden + (int64_t)cu_seqlens[i] * d + col;
-    for (int32_t j = r; j < L; j += kPoolLanes) {
-      const uint4 w = *reinterpret_cast<const uint4*>(base + (int64_t)j * d);
-      const uint32_t v[4] = {w.x, w.y, w.z, w.w};
+    auto add = [&](const uint4& q) {
+      const uint32_t v[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         acc[2 * e] += __uint_as_float(v[e] << 16);
         acc[2 * e + 1] += __uint_as_float(v[e] & 0xffff0000u);
       }
+    };
+    int32_t j = w;
+    for (; j + 3 * kPoolWaves < L; j += 4 * kPoolWaves) {
+      uint4 q[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) q[k] = *reinterpret_cast<const uint4*>(base + (int64_t)(j + k * kPoolWaves) * d);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) add(q[k]);
     }
+    for (; j < L; j += kPoolWaves) add(*reinterpret_cast<const uint4*>(base + (int64_t)j * d));
   }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) red[r][cg * 8 + e] = acc[e];
+  for (int e = 0; e < 8; ++e) red[w][lane * 8 + e] = acc[e];
   __syncthreads();
-  for (int w = kPoolLanes / 2; w > 0; w >>= 1) {
-    if (r < w) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) red[r][cg * 8 + e] += red[r + w][cg * 8 + e];
-    }
-    __syncthreads();
+  const float inv = 1.0f / (float)L;
+  for (int t = threadIdx.x; t < kPoolCols; t += 256) {
+    if (c0 + t < d)
+      pooled[(int64_t)rank[i] * d + c0 + t] = ((red[0][t] + red[1][t]) + (red[2][t] + red[3][t])) * inv;
   }
-  if (threadIdx.x < kPoolCols && c0 + (int32_t)threadIdx.x < d)
-    pooled[(int64_t)rank[i] * d + c0 + threadIdx.x] = red[0][threadIdx.x] * (1.0f / (float)L);
 }
 
 hipError_t launch_pool(hipStream_t s, const void* hidden, const int32_t* seqlens, const int32_t* cu_seqlens,
