@@ -18,6 +18,40 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
   return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
 }
 
+// v together with the value lane l ^ 16 (v_permlane16_swap) or l ^ 32
+// (v_permlane32_swap) holds, without an LDS round trip.  The two come back
+// in an order that differs between the lanes of a pair, so only commutative
+// combinations (max, sum) of .x and .y are the same in both lanes.
+__device__ __forceinline__ float2 lane_pair16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float2 lane_pair32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float max_xor16(float v) {
+  const float2 p = lane_pair16(v);
+  return fmaxf(p.x, p.y);
+}
+
+__device__ __forceinline__ float max_xor32(float v) {
+  const float2 p = lane_pair32(v);
+  return fmaxf(p.x, p.y);
+}
+
+__device__ __forceinline__ float sum_xor16(float v) {
+  const float2 p = lane_pair16(v);
+  return p.x + p.y;
+}
+
+__device__ __forceinline__ float sum_xor32(float v) {
+  const float2 p = lane_pair32(v);
+  return p.x + p.y;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[kt][r]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
+    mloc = max_xor32(mloc) * scale_log2;
     if (__any(mloc > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mloc);
       if (__all(m_run == -INFINITY)) {
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
         s[kt][r] = p;
         lsum += p;
       }
-    lsum += __shfl_xor(lsum, 32, 64);
+    lsum = sum_xor32(lsum);
     l_run += lsum;
 
     // P^T operands: 16-key chunk kc holds registers 8*(kc&1) .. +7 of tile kc>>1,
@@ -414,16 +414,29 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
     const uint16_t* Ks = &lds[jstep & 1][0];
     const uint16_t* Vs = &lds[jstep & 1][TILE];
 
+    // scores: dim chunk c outer, so the four 16-key blocks' accumulators
+    // alternate; the K fragments of chunk c+1 are read before the MFMAs of
+    // chunk c (each accumulator still sums c = 0..NQC-1 in order)
     f32x4 s[4];
+    bf16x8 kf[2][4];
 #pragma unroll
     for (int kb16 = 0; kb16 < 4; ++kb16) {
       s[kb16] = f32x4{0.f, 0.f, 0.f, 0.f};
+      kf[0][kb16] = *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + ((quad ^ kswz) * 8));
+    }
 #pragma unroll
-      for (int c = 0; c < NQC; ++c) {
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + (((4 * c + quad) ^ kswz) * 8));
-        s[kb16] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], s[kb16], 0, 0, 0);
+    for (int c = 0; c < NQC; ++c) {
+      if (c + 1 < NQC) {
+#pragma unroll
+        for (int kb16 = 0; kb16 < 4; ++kb16)
+          kf[(c + 1) & 1][kb16] =
+              *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + (((4 * (c + 1) + quad) ^ kswz) * 8));
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kb16 = 0; kb16 < 4; ++kb16)
+        s[kb16] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c & 1][kb16], qf[c], s[kb16], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // online softmax (see attn_fwd_kernel); the four lanes of a query are
     // lane ^ 16 and lane ^ 32 apart
@@ -442,8 +455,7 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
     for (int kb16 = 0; kb16 < 4; ++kb16)
 #pragma unroll
       for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, s[kb16][e]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
+    mloc = max_xor32(max_xor16(mloc)) * scale_log2;
     if (__any(mloc > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mloc);
       if (__all(m_run == -INFINITY)) {
@@ -465,8 +477,7 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
         s[kb16][e] = p;
         lsum += p;
       }
-    lsum += __shfl_xor(lsum, 16, 64);
-    lsum += __shfl_xor(lsum, 32, 64);
+    lsum = sum_xor32(sum_xor16(lsum));
     l_run += lsum;
 
     bf16x8 pf[2];
@@ -477,8 +488,9 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
         pf[c][e] = (__bf16)s[2 * c][e];
         pf[c][4 + e] = (__bf16)s[2 * c + 1][e];
       }
-#pragma unroll
-    for (int t = 0; t < NOT; ++t) {
+    // P.V: the V^T fragments of head-dim block t+2 are read before the
+    // MFMAs of block t
+    auto read_v = [&](int t, bf16x8 (&vf)[2]) {
       const int col = t * 16 + 4 * (j16 & 3);
       const int pos = (((col >> 3) ^ vswz) * 8) + (col & 7);
 #pragma unroll
@@ -488,9 +500,18 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
             (__attribute__((address_space(3))) bf16x4*)(Vs + r0 * HD + pos));
         const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (__attribute__((address_space(3))) bf16x4*)(Vs + (r0 + 16) * HD + pos));
-        const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[c], o[t], 0, 0, 0);
+        vf[c] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
+    };
+    bf16x8 vb[2][2];
+    read_v(0, vb[0]);
+#pragma unroll
+    for (int t = 0; t < NOT; ++t) {
+      if (t + 1 < NOT) read_v(t + 1, vb[(t + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[t & 1][c], pf[c], o[t], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
