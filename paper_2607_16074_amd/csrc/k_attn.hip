@@ -196,17 +196,30 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
     const uint16_t* Ks = &lds[jstep & 1][0];
     const uint16_t* Vs = &lds[jstep & 1][TILE];
 
-    // S^T for NKT 32-key tiles
+    // S^T for NKT 32-key tiles: dim chunk c outer, so the tiles' accumulators
+    // alternate, with the K fragments of chunk c+1 read before the MFMAs of
+    // chunk c (each accumulator still sums c = 0..NQC-1 in order)
     f32x16 s[NKT];
+    bf16x8 kf[2][NKT];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[kt][e] = 0.f;
+      kf[0][kt] = *reinterpret_cast<const bf16x8*>(Ks + (kt * 32 + krow) * HD + ((half ^ kswz) * 8));
+    }
 #pragma unroll
-      for (int c = 0; c < NQC; ++c) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + (kt * 32 + krow) * HD + (((2 * c + half) ^ kswz) * 8));
-        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], s[kt], 0, 0, 0);
+    for (int c = 0; c < NQC; ++c) {
+      if (c + 1 < NQC) {
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+          kf[(c + 1) & 1][kt] =
+              *reinterpret_cast<const bf16x8*>(Ks + (kt * 32 + krow) * HD + (((2 * (c + 1) + half) ^ kswz) * 8));
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c & 1][kt], qf[c], s[kt], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // Online softmax in the log2 domain (scores scaled by log2(e)/sqrt(hd)).
     // The running max m only moves when some query of the wave gains more
@@ -266,19 +279,30 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
     for (int kc = 0; kc < NKC; ++kc)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[kc][e] = (__bf16)s[kc >> 1][(kc & 1) * 8 + e];
+    // O^T += V^T P^T: key chunk kc outer, so the head-dim blocks'
+    // accumulators alternate, with the V^T fragments of chunk kc+1 read
+    // before the MFMAs of chunk kc (each o[t] still sums kc = 0..NKC-1 in order)
+    auto read_v = [&](int kc, bf16x8 (&vf)[NOT]) {
+      const int r0 = kc * 16 + vrow0;
 #pragma unroll
-    for (int t = 0; t < NOT; ++t) {
-      const int col = t * 32 + vcol;
-#pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) {
-        const int r0 = kc * 16 + vrow0;
+      for (int t = 0; t < NOT; ++t) {
+        const int col = t * 32 + vcol;
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (__attribute__((address_space(3))) bf16x4*)(Vs + r0 * HD + (((col >> 3) ^ vswz0) * 8) + (col & 7)));
         const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (__attribute__((address_space(3))) bf16x4*)(Vs + (r0 + 8) * HD + (((col >> 3) ^ vswz1) * 8) + (col & 7)));
-        const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kc], o[t], 0, 0, 0);
+        vf[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
+    };
+    bf16x8 vb[2][NOT];
+    read_v(0, vb[0]);
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      if (kc + 1 < NKC) read_v(kc + 1, vb[(kc + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < NOT; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vb[kc & 1][t], pf[kc], o[t], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
