@@ -23,7 +23,10 @@
 // Scores: S^T = K Q^T with v_mfma_f32_32x32x16_bf16, K the "A" operand
 // (16-byte LDS reads), Q held in registers as "B", so each lane owns one
 // query row's scores for 16 of every 32 keys and the online-softmax row
-// max / sum need only its registers plus one exchange with lane ^ 32.  The
+// max / sum need only its registers plus one exchange with lane ^ 32
+// (v_permlane32_swap, no LDS round trip).  Both products run their
+// contraction chunks outermost, so independent accumulators alternate, and
+// read the next chunk's fragments before the current chunk's MFMAs.  The
 // probabilities then sit in the operand layout of O^T += V^T P^T (keys
 // contracted in the permuted order the score layout gives), so P stays in
 // registers.  The V^T operand is read from the row-major V tile with
