@@ -108,6 +108,30 @@ def test_variant_backbone(jn, case):
     _say(f"  hidden max-rel {worst:.3e}")
 
 
+WIDE_AND_LONG = [  # d, heads, kv heads, causal, rope theta, samples per tenant, text lengths
+    (4096, 16, 16, False, 10000.0, (2, 1), (16, 96)),  # widest supported row, head width 256
+    (4096, 32, 8, True, 0.0, (1, 2), (16, 96)),  # widest row, head width 128, grouped KV heads
+    (512, 2, 2, False, 0.0, (1, 1), (2000, 3000)),  # long samples: 32-47 key steps per query tile
+    (512, 8, 8, True, 10000.0, (1, 1), (2000, 3000)),  # long causal samples, head width 64
+]
+
+
+@pytest.mark.parametrize("case", WIDE_AND_LONG,
+                         ids=[f"d{c[0]}h{c[1]}kv{c[2]}{'c' if c[3] else 'b'}L{c[6][1]}" for c in WIDE_AND_LONG])
+def test_variant_wide_and_long(jn, case):
+    """The widest backbone row the library supports (d = 4096: eight 8-wide
+    chunks per lane in RMSNorm, a 12,288-wide QKV projection, GeGLU) and
+    samples of 2000-3000 tokens (many key steps, lazy rescaling across them,
+    up to 47 query tiles per head), hidden rows against the oracle."""
+    d, H, kv, causal, theta, ns, (lo, hi) = case
+    wl = W.make_workload(spec_of(d, H, kv, causal, theta, ns=ns, lo=lo, hi=hi, max_len=hi, layers=1, glu=True))
+    _say(f"wide/long d={d} heads={H} kv={kv} causal={causal}: "
+         f"lengths {[int(x) for q in wl.requests for x in q.lengths]}")
+    st = run(wl, align=16 if causal else 1)
+    worst = check(wl, st)
+    _say(f"  hidden max-rel {worst:.3e}")
+
+
 def test_variant_grouped_equals_isolated_bitwise(jn):
     """Rotary positions come from each sample's own rows, so a sample's
     result does not depend on where the pack put it."""
