@@ -151,7 +151,9 @@ typedef struct jn_pack_sizes {
  *   token_sample[T]       sample of packed row t, -1 for an alignment row
  *   token_pos[T]          row of that sample, -1 for an alignment row      */
 typedef struct jn_packed {
-  int32_t R, G, N, T, d, max_seqlen, align, reserved;
+  int32_t R, G, N, T, d, max_seqlen, align;
+  int32_t req_sig;         /* signature of the requests' (n_samples, max_len)
+                              list, checked by jn_unpack                     */
   void* tokens;            /* device bf16 [T][d]; alignment rows are zero */
   int32_t* seqlens;
   int32_t* cu_seqlens;
@@ -399,7 +401,10 @@ jn_status jn_tenant_adamw_step(jn_ctx* ctx, const jn_adamw_tenant* t, int32_t G,
 /* Scatter packed rows back to the requests: for sample i of request r and
  * j < max_len_r, out[r][s][j] = rows[cu_seqlens[i] + j] if j < seqlens[i],
  * else zero.  `rows`: device [T][row_bytes]; `req_out`: host array [R] of
- * device buffers [n_r][max_len_r][row_bytes]; row_bytes a multiple of 4. */
+ * device buffers [n_r][max_len_r][row_bytes]; row_bytes a multiple of 4.
+ * `req` must list the requests the batch was packed from, in the same order:
+ * requests whose sample counts or max_len differ (even with the same total)
+ * are JN_ESHAPE, and nothing is enqueued. */
 jn_status jn_unpack(jn_ctx* ctx, const jn_packed* p, const jn_request* req, int32_t R,
                     const void* rows, size_t row_bytes, void* const* req_out);
 

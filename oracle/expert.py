@@ -17,9 +17,15 @@ The backbone is frozen: nothing flows back into the shared features.
 ``rnd=True`` rounds to bf16 exactly where the GPU stores a GEMM
 operand in bf16 (forward: every GEMM input activation; backward: every
 incoming gradient before it meets a GEMM), computing everything else in
-fp64.  That is the GPU's precision contract, so parity of gradients can be
-checked at 1e-3 relative L2; with ``rnd=False`` the whole expert is
-plain fp64 (pinned against finite differences).
+fp64.  That is the GPU's precision contract.  It does not make the two
+agree to fp32 rounding: a value that lands near a bf16 rounding boundary
+can round the other way on the GPU, which moves it by one bf16 step, and
+the change propagates.  fp32-sized perturbations before every rounding point
+move this mode's predictions and gradients by 1e-3 (2 layers) to 5e-3
+(6 layers) relative L2, so the stage-wise bar against this mode is 1e-2
+relative L2 (about twice that floor).  With ``rnd=False`` the whole expert
+is plain fp64 (pinned against finite differences); the GPU is compared with
+that mode too, at a bar derived from the distance between the two modes.
 
 Flow-matching objective (the GR00T / pi0.5-style training of such experts):
 per sample a flow time tau in (0, 1) and noise eps of the action chunk's

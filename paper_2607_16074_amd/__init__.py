@@ -159,7 +159,7 @@ def jn_pack_maps_host(reqs: Sequence[Request], tenants: Sequence[Tenant], d: int
     _check(_lib.jn_pack_maps_host(ra, len(reqs), ta, len(tenants), C.byref(o),
                                   buf.ctypes.data_as(C.c_void_p), buf.nbytes, C.byref(out)), what="jn_pack_maps_host")
     base = buf.ctypes.data
-    res = {"N": out.N, "T": out.T, "max_seqlen": out.max_seqlen}
+    res = {"N": out.N, "T": out.T, "max_seqlen": out.max_seqlen, "req_sig": out.req_sig}
     for name in jn_packed.MAP_FIELDS:
         off = C.cast(getattr(out, name), C.c_void_p).value - base
         res[name] = buf[off: off + 4 * out.map_len(name)].view(np.int32).copy()

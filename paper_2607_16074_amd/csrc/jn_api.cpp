@@ -279,6 +279,26 @@ std::vector<char> host_head_image(const MapLayout& m, const Plan& p) {
   return img;
 }
 
+// Signature of the request shapes a physical batch was planned from: FNV-1a
+// over R and every request's (n_samples, max_len).  jn_unpack compares it
+// with the requests it is given, because the unpack kernel indexes each
+// request's buffer with the pack-time sample positions.
+int32_t request_signature(const jn_request* req, int32_t R) {
+  uint32_t h = 2166136261u;
+  auto mix = [&](uint32_t v) {
+    for (int b = 0; b < 4; ++b) {
+      h ^= (v >> (8 * b)) & 0xffu;
+      h *= 16777619u;
+    }
+  };
+  mix((uint32_t)R);
+  for (int32_t r = 0; r < R; ++r) {
+    mix((uint32_t)req[r].n_samples);
+    mix((uint32_t)req[r].max_len);
+  }
+  return (int32_t)h;
+}
+
 bool valid_packed(const jn_packed* p) {
   return p && p->N > 0 && p->T > 0 && p->G > 0 && p->R > 0 && p->d > 0 && p->seqlens && p->cu_seqlens &&
          p->sample_request && p->sample_local && p->tenant_sample_off && p->sample_tenant_rank &&
@@ -397,6 +417,7 @@ jn_status jn_pack_maps_host(const jn_request* req, int32_t R, const jn_tenant* t
   ReqEntry* rt = (ReqEntry*)(base + m.reqtab);
   for (int32_t r = 0; r < R; ++r) rt[r] = ReqEntry{req[r].embeds, nullptr, req[r].max_len, req[r].n_samples, p.req_first[r], 0};
   fill_packed(out, base, m, p, R, G, o);
+  out->req_sig = request_signature(req, R);
   return JN_OK;
 }
 
@@ -427,6 +448,7 @@ jn_status jn_pack_group(jn_ctx* c, const jn_request* req, int32_t R, const jn_te
   if (st != JN_OK) return st;
   jn_packed tmp;
   fill_packed(&tmp, base, m, p, R, G, o);
+  tmp.req_sig = request_signature(req, R);
   tmp.tokens = tokens;
   JN_TRACED(c, JN_OP_PACK, p.T, o->d_model, 0,
             launch_pack(c->stream, (const ReqEntry*)tmp.req_table, tmp.sample_request, tmp.sample_local,
@@ -869,6 +891,8 @@ jn_status jn_unpack(jn_ctx* c, const jn_packed* p, const jn_request* req, int32_
     mreq = std::max(mreq, req[r].max_len);
   }
   if (n != p->N) return fail(c, JN_ESHAPE, "requests hold %lld samples, packed batch %d", (long long)n, p->N);
+  if (request_signature(req, R) != p->req_sig)
+    return fail(c, JN_ESHAPE, "requests differ from those the batch was packed from (sample counts or max_len)");
   jn_status st = stage_copy(c, p->req_table, rt.data(), sizeof(ReqEntry) * R);
   if (st != JN_OK) return st;
   JN_TRACED(c, JN_OP_UNPACK, p->T, (int64_t)row_bytes, 0, launch_unpack(c->stream, (const ReqEntry*)p->req_table, p->sample_request, p->sample_local,
@@ -1945,6 +1969,7 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
   char* w = (char*)ws;
   char* maps = w + L.maps;
   fill_packed(&pl->packed, maps, L.m, p, R, G, o);
+  pl->packed.req_sig = request_signature(req, R);
   pl->packed.tokens = w + L.tokens;
   pl->max_rows = p.max_rows;
   pl->layers.assign(bb->layers, bb->layers + bb->n_layers);

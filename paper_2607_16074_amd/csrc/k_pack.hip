@@ -50,10 +50,12 @@ __global__ __launch_bounds__(256) void unpack_kernel(const ReqEntry* __restrict_
   const int32_t i = blockIdx.x;
   const ReqEntry e = req_table[sample_request[i]];
   const int32_t j0 = blockIdx.y * kRowsPerBlock;
-  if (j0 >= e.max_len) return;
+  const int32_t s = sample_local[i];
+  // the host checks that the requests match the packed batch; a sample
+  // beyond its request's buffer is still never written
+  if (j0 >= e.max_len || s >= e.n) return;
   const int32_t nr = min(kRowsPerBlock, e.max_len - j0);
   const int32_t L = seqlens[i];
-  const int32_t s = sample_local[i];
   V* dst = reinterpret_cast<V*>(e.out) + ((int64_t)s * e.max_len + j0) * row_vecs;
   const V* src = rows + (int64_t)(cu_seqlens[i] + j0) * row_vecs;
   for (int64_t idx = threadIdx.x; idx < nr * row_vecs; idx += blockDim.x) {

@@ -129,6 +129,22 @@ def test_host_plan_errors(lib):
     assert e.value.status == lib._abi.JN_ESHAPE
 
 
+def test_request_signature_tells_splits_apart(lib):
+    """The batch records the shape of the request list it was packed from, so
+    that an unpack given another split of the same samples (same total, other
+    per-request counts or canonical lengths) can be refused on the host."""
+    d = 64
+    T = [lib.Tenant(7, d)] * 2
+    a = lib.jn_pack_maps_host(_reqs(lib, [0, 0, 1], [[3, 4], [5], [2, 2]], [8, 8, 4]), T, d, 1)
+    b = lib.jn_pack_maps_host(_reqs(lib, [0, 0, 1], [[3, 4], [5], [2, 2]], [8, 8, 4]), T, d, 16)
+    c = lib.jn_pack_maps_host(_reqs(lib, [0, 0, 1], [[3], [4, 5], [2, 2]], [8, 8, 4]), T, d, 1)
+    e = lib.jn_pack_maps_host(_reqs(lib, [0, 0, 1], [[3, 4], [5], [2, 2]], [8, 9, 4]), T, d, 1)
+    f = lib.jn_pack_maps_host(_reqs(lib, [0, 0, 1], [[1, 1], [1], [1, 1]], [8, 8, 4]), T, d, 1)
+    assert a["N"] == c["N"] == e["N"]
+    assert a["req_sig"] == b["req_sig"] == f["req_sig"]   # lengths and alignment do not enter
+    assert len({a["req_sig"], c["req_sig"], e["req_sig"]}) == 3
+
+
 # ------------------------------------------------------ expert validation ---
 
 def test_pack_tenant_sizes_match_plan(lib):

@@ -420,6 +420,20 @@ def test_errors_enqueue_nothing(jn):
         jn.jn_tenant_heads_fwd_bwd(st.ctx, st.packed, st.hidden, st.heads[:1], st.ios[:1], st.hd_ws)
     assert e.value.status == jn._abi.JN_EINVAL
 
+    # unpack with the same samples split differently over the requests: the
+    # packed sample positions would index past a request's buffer
+    from paper_2607_16074_amd import Request
+    resplit = [Request(0, st.requests[0].embeds[:5], st.requests[0].lengths[:5]),
+               Request(1, torch.cat([st.requests[0].embeds[5:], st.requests[1].embeds]),
+                       np.concatenate([st.requests[0].lengths[5:], st.requests[1].lengths]),
+                       st.requests[1].max_len)]
+    outs = [torch.full((len(q.lengths), q.max_len, st.model.backbone.d), 3, dtype=torch.int16, device="cuda")
+            for q in resplit]
+    before_out = [o.clone() for o in outs]
+    with pytest.raises(jn.JNError) as e:
+        jn.jn_unpack(st.ctx, st.packed, resplit, st.hidden, st.model.backbone.d * 2, outs)
+    assert e.value.status == jn._abi.JN_ESHAPE
+
     class _Wide:  # the same layers described with a width beyond the kernels' range
         struct = jn._abi.jn_backbone.from_buffer_copy(st.model.backbone.struct)
     _Wide.struct.d, _Wide.struct.n_heads = 4224, 33
@@ -428,3 +442,4 @@ def test_errors_enqueue_nothing(jn):
     assert e.value.status == jn._abi.JN_EUNSUPPORTED
     torch.cuda.synchronize()
     assert torch.equal(before, st.hidden)
+    assert all(torch.equal(a, b) for a, b in zip(outs, before_out))
