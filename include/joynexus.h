@@ -275,6 +275,26 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* ctx, const jn_packed* p, const void* h
                                   const jn_head* heads, const jn_head_io* io, int32_t G,
                                   void* ws, size_t ws_bytes, float* pooled);
 
+/* Allocation-free variant of jn_tenant_heads_fwd_bwd, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments (minus the
+ * workspace), same kernels, same results bit for bit.  The workspace is a
+ * library-owned device array of JN_HEADS_SCRATCH_BYTES per GPU, created with
+ * the library and held until the process ends; its index tables are staged
+ * through a fixed 1 MiB pinned buffer that jn_ctx_create allocates.  The call
+ * allocates nothing (no hipMalloc / hipFree / pinned allocation).  Nothing in
+ * the array needs to start at zero: every value a call reads was written by
+ * that call.
+ * Errors (nothing enqueued): JN_ENOSPACE when jn_heads_workspace_size exceeds
+ * JN_HEADS_SCRATCH_BYTES or the tables exceed 1 MiB; the other statuses as
+ * for jn_tenant_heads_fwd_bwd.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (other streams or contexts) race and must be ordered by the caller. */
+#define JN_HEADS_SCRATCH_BYTES (64u << 20)
+jn_status jn_tenant_heads_fwd_bwd_noalloc(jn_ctx* ctx, const jn_packed* p, const void* hidden,
+                                          const jn_head* heads, const jn_head_io* io, int32_t G,
+                                          float* pooled);
+
 /* ------------------------------------------------------- action expert --- */
 
 /* Per-tenant sample counts and valid prefix rows of a group (host only): the

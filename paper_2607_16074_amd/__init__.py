@@ -23,7 +23,8 @@ _lib = _abi.load()
 __all__ = [
     "JNError", "Context", "Request", "Tenant", "Backbone", "Head", "HeadIO",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group", "jn_backbone_workspace_size",
-    "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_unpack",
+    "jn_backbone_forward", "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_tenant_heads_fwd_bwd_noalloc",
+    "HEADS_SCRATCH_BYTES", "jn_unpack",
     "Expert", "ExpertIO", "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
     "AdamWTenant", "jn_adamw_workspace_size", "jn_tenant_adamw_step",
     "Collector", "InferPlan", "jn_infer_workspace_size",
@@ -303,6 +304,20 @@ def jn_tenant_heads_fwd_bwd(ctx: Context, packed: Packed, hidden, heads: Sequenc
     ha, ia = _head_arrays(heads, ios)
     _check(_lib.jn_tenant_heads_fwd_bwd(ctx.handle, C.byref(packed.struct), _ptr(hidden), ha, ia, len(heads),
                                         _ptr(ws), ws.numel() * ws.element_size(), _ptr(pooled)), ctx)
+
+
+# Size of the library-owned workspace of the allocation-free heads call
+# (JN_HEADS_SCRATCH_BYTES in joynexus.h).
+HEADS_SCRATCH_BYTES = 64 << 20
+
+
+def jn_tenant_heads_fwd_bwd_noalloc(ctx: Context, packed: Packed, hidden, heads: Sequence[Head],
+                                    ios: Sequence[HeadIO], pooled=None):
+    """The heads call on the library's own per-GPU scratch array (no
+    workspace argument; allocates nothing)."""
+    ha, ia = _head_arrays(heads, ios)
+    _check(_lib.jn_tenant_heads_fwd_bwd_noalloc(ctx.handle, C.byref(packed.struct), _ptr(hidden), ha, ia,
+                                                len(heads), _ptr(pooled)), ctx)
 
 
 # ------------------------------------------------------- action expert ------

@@ -22,7 +22,7 @@ EXPORTS = (
     "jn_ctx_trace_read",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group",
     "jn_backbone_workspace_size", "jn_backbone_forward",
-    "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd",
+    "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_tenant_heads_fwd_bwd_noalloc",
     "jn_pack_tenant_sizes", "jn_experts_workspace_size", "jn_tenant_experts_fwd_bwd",
     "jn_adamw_workspace_size", "jn_tenant_adamw_step",
     "jn_unpack",
@@ -165,6 +165,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "jn_heads_workspace_size": (C.c_int, [P(jn_packed), P(jn_head), C.c_int32, P(C.c_size_t)]),
         "jn_tenant_heads_fwd_bwd": (C.c_int, [V, P(jn_packed), V, P(jn_head), P(jn_head_io), C.c_int32, V,
                                               C.c_size_t, V]),
+        "jn_tenant_heads_fwd_bwd_noalloc": (C.c_int, [V, P(jn_packed), V, P(jn_head), P(jn_head_io), C.c_int32,
+                                                      V]),
         "jn_pack_tenant_sizes": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
                                            P(C.c_int32), P(C.c_int64)]),
         "jn_experts_workspace_size": (C.c_int, [P(jn_packed), P(jn_expert), P(jn_expert_io), C.c_int32,

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <deque>
 #include <functional>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -16,6 +17,43 @@
 #include "jn_internal.h"
 
 using namespace jnx;
+
+// ------------------------------------------------- library-owned scratch ---
+
+// Workspace of jn_tenant_heads_fwd_bwd_noalloc: one array per GPU, held
+// until the process ends.  Host code never uses its name as an address (on
+// the host it is a stand-in symbol); the device address comes from
+// hipGetSymbolAddress, once per device, and is kept per device.
+namespace {
+constexpr size_t kHeadsScratchBytes = size_t(JN_HEADS_SCRATCH_BYTES);
+constexpr size_t kFixedStageBytes = size_t(1) << 20;
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) char scratch[kHeadsScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+bool g_scratch_done[kMaxDevices] = {};
+
+// Device address of `scratch` on `dev` (which must be the current device);
+// nullptr if the runtime could not resolve it.
+void* scratch_address(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_done[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      ptr = nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+    g_scratch_done[dev] = true;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
 
 // --------------------------------------------------------------- context ---
 
@@ -48,6 +86,13 @@ struct jn_ctx {
   std::vector<TraceRec> recs;
   std::vector<hipEvent_t> pool;
   size_t pool_used = 0;
+  // allocation-free entry points: the device's library-owned scratch array
+  // (resolved at creation) and a pinned staging buffer of fixed size for
+  // their tables, allocated at creation and never grown
+  void* scratch = nullptr;
+  void* fixed_host = nullptr;
+  hipEvent_t fixed_ev = nullptr;
+  bool fixed_pending = false;
 };
 
 namespace {
@@ -125,6 +170,24 @@ jn_status stage_copy(jn_ctx* c, void* dst, const void* src, size_t bytes) {
   JN_HIP(c, hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, c->stream), "hipMemcpyAsync(H2D)");
   JN_HIP(c, hipEventRecord(s.ev, c->stream), "hipEventRecord(staging)");
   s.pending = true;
+  return JN_OK;
+}
+
+// Stage a table through the context's fixed pinned buffer (the
+// allocation-free entry points): never allocates; JN_ENOSPACE if the table
+// does not fit.
+jn_status stage_copy_fixed(jn_ctx* c, void* dst, const void* src, size_t bytes) {
+  if (bytes == 0) return JN_OK;
+  if (bytes > kFixedStageBytes)
+    return fail(c, JN_ENOSPACE, "tables of %zu B exceed the %zu B fixed staging buffer", bytes, kFixedStageBytes);
+  if (c->fixed_pending) {
+    JN_HIP(c, hipEventSynchronize(c->fixed_ev), "hipEventSynchronize(fixed staging)");
+    c->fixed_pending = false;
+  }
+  std::memcpy(c->fixed_host, src, bytes);
+  JN_HIP(c, hipMemcpyAsync(dst, c->fixed_host, bytes, hipMemcpyHostToDevice, c->stream), "hipMemcpyAsync(H2D)");
+  JN_HIP(c, hipEventRecord(c->fixed_ev, c->stream), "hipEventRecord(fixed staging)");
+  c->fixed_pending = true;
   return JN_OK;
 }
 
@@ -327,6 +390,13 @@ jn_status jn_ctx_create(jn_ctx** out, void* hip_stream) {
       return JN_EHIP;
     }
   }
+  if (hipEventCreateWithFlags(&c->fixed_ev, hipEventDisableTiming) != hipSuccess ||
+      hipHostMalloc(&c->fixed_host, kFixedStageBytes, hipHostMallocDefault) != hipSuccess) {
+    c->fixed_host = nullptr;
+    jn_ctx_destroy(c);
+    return JN_EHIP;
+  }
+  c->scratch = scratch_address(c->device);
   *out = c;
   return JN_OK;
 }
@@ -338,6 +408,9 @@ void jn_ctx_destroy(jn_ctx* c) {
     if (s.host) hipHostFree(s.host);
     if (s.ev) hipEventDestroy(s.ev);
   }
+  if (c->fixed_pending) hipEventSynchronize(c->fixed_ev);
+  if (c->fixed_host) hipHostFree(c->fixed_host);
+  if (c->fixed_ev) hipEventDestroy(c->fixed_ev);
   if (!c->recs.empty()) hipEventSynchronize(c->recs.back().stop);
   for (hipEvent_t e : c->pool) hipEventDestroy(e);
   delete c;
@@ -700,9 +773,14 @@ jn_status jn_heads_workspace_size(const jn_packed* p, const jn_head* heads, int3
   return JN_OK;
 }
 
-jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_head* heads,
-                                  const jn_head_io* io, int32_t G, void* ws, size_t ws_bytes, float* pooled) {
-  if (!c) return JN_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// Body of both heads entry points; `fixed` = the allocation-free variant
+// (tables staged through the context's fixed pinned buffer).
+jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_head* heads, const jn_head_io* io,
+                    int32_t G, void* ws, size_t ws_bytes, float* pooled, bool fixed) {
   if (!valid_packed(p)) return fail(c, JN_EINVAL, "invalid packed batch");
   if (!hidden || !io || !ws) return fail(c, JN_EINVAL, "null hidden, io or workspace");
   if (((uintptr_t)hidden) % 16 != 0 || p->d % 8 != 0)
@@ -846,7 +924,8 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hid
   std::memcpy(img.data(), losses.data(), lbytes);
   std::memcpy(img.data() + (hp.descs - hp.losses), descs.data(), dbytes);
   std::memcpy(img.data() + (hp.tiles - hp.losses), tiles.data(), tbytes);
-  st = stage_copy(c, w + hp.losses, img.data(), hp.tiles - hp.losses + tbytes);
+  st = fixed ? stage_copy_fixed(c, w + hp.losses, img.data(), hp.tiles - hp.losses + tbytes)
+             : stage_copy(c, w + hp.losses, img.data(), hp.tiles - hp.losses + tbytes);
   if (st != JN_OK) return st;
   const LossDesc* dl = (const LossDesc*)(w + hp.losses);
   const HeadGemm* dd = (const HeadGemm*)(w + hp.descs);
@@ -865,6 +944,30 @@ jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hid
       JN_TRACED(c, JN_OP_HEAD_BWD, r.second, 0, 0, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off),
                 "head bwd");
   return JN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+jn_status jn_tenant_heads_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_head* heads,
+                                  const jn_head_io* io, int32_t G, void* ws, size_t ws_bytes, float* pooled) {
+  if (!c) return JN_EINVAL;
+  return heads_run(c, p, hidden, heads, io, G, ws, ws_bytes, pooled, false);
+}
+
+jn_status jn_tenant_heads_fwd_bwd_noalloc(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_head* heads,
+                                          const jn_head_io* io, int32_t G, float* pooled) {
+  if (!c) return JN_EINVAL;
+  if (!c->scratch) return fail(c, JN_EHIP, "the library scratch array has no device address on device %d", c->device);
+  if (valid_packed(p) && heads && G == p->G && check_heads(nullptr, p, heads, G) == JN_OK) {
+    HeadPlan hp;
+    head_layout(p, heads, G, &hp, false);
+    if (hp.total > kHeadsScratchBytes)
+      return fail(c, JN_ENOSPACE, "heads need %zu B of workspace; the allocation-free call has %zu B", hp.total,
+                  kHeadsScratchBytes);
+  }
+  return heads_run(c, p, hidden, heads, io, G, c->scratch, kHeadsScratchBytes, pooled, true);
 }
 
 // ---------------------------------------------------------------- unpack ---

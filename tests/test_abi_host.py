@@ -31,6 +31,12 @@ def test_library_exports_every_declared_symbol(lib):
     assert set(names) == set(_abi.EXPORTS)
 
 
+def test_noalloc_scratch_size_matches_header(lib):
+    text = open(HEADER).read()
+    m = re.search(r"#define JN_HEADS_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == lib.HEADS_SCRATCH_BYTES
+
+
 def test_struct_layout_matches_c(tmp_path, lib):
     """sizeof / offsetof from the C compiler against the ctypes mirror."""
     from paper_2607_16074_amd import _abi
