@@ -153,13 +153,18 @@ def test_variant_grouped_equals_isolated_bitwise(jn):
 
 
 @pytest.mark.parametrize("cfg", [6, 7])
-def test_variant_2b_sampled(jn, cfg):
+def test_variant_2b_sampled(jn, cfg, margin):
     """The 2B-shaped variants at full size in the benchmark's launch
-    configuration; the oracle runs the first sample of the first tenant."""
+    configuration: one sample of every tenant against the stored oracle
+    values (hidden rows and pooled features); the oracle run here on the
+    first sample of the first tenant (all rows)."""
+    from test_gpu_parity import check_golden
     wl = W.make_workload(cfg)
     _say(f"config {cfg}: {wl.spec.name}")
     st = run(wl)
+    check_golden(wl, st, margin)
     worst = check(wl, st, keys=[(0, 0)])
+    margin(f"cfg{cfg} hidden, 1 sample all rows, max-rel", worst, BF16_TOL)
     _say(f"  hidden max-rel {worst:.3e}")
 
 
