@@ -41,6 +41,8 @@
 // gate and up weight rows are interleaved in 16-row blocks as they are
 // loaded, so the gate and up accumulators of an output column land in the
 // same lane.
+#include <algorithm>
+
 #include "jn_device.h"
 #include "jn_internal.h"
 
@@ -725,9 +727,16 @@ int gemm_split(int epi, int32_t M, int32_t N, int32_t K) {
   return S;
 }
 
+static int32_t gemm_tail_split(int epi, int32_t M, int32_t N, int32_t K, int32_t* m1, int* t1, int* t2);
+
 size_t gemm_split_bytes(int epi, int32_t M, int32_t N, int32_t K) {
   const int S = gemm_split(epi, M, N, K);
-  return S > 1 ? (size_t)S * M * N * sizeof(float) : 0;
+  size_t bytes = S > 1 ? (size_t)S * M * N * sizeof(float) : 0;
+  int32_t m1;
+  int t1, t2;
+  const int32_t St = gemm_tail_split(epi, M, N, K, &m1, &t1, &t2);
+  if (St > 1) bytes = std::max(bytes, (size_t)St * (M - m1) * N * sizeof(float));
+  return bytes;
 }
 
 // One launch over all rows of g with tile shape t (0: 256x256 ring loop,
@@ -738,6 +747,42 @@ static hipError_t launch_rows(hipStream_t s, int epi, GemmArgs g, int t) {
     case 1: return launch_tile<256, 128, 4, 2>(s, epi, g);
     default: return launch_tile<128, 128, 2, 2>(s, epi, g);
   }
+}
+
+// Split-K: S launches' worth of K ranges as one grid (blockIdx.y = range),
+// fp32 partials into split_ws, then their sum in range order with the
+// epilogue (EPI_BF16, EPI_RESID_F32 or EPI_GELU_BF16).
+static hipError_t launch_split(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, int64_t ldb,
+                               void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int t, int32_t S,
+                               void* split_ws) {
+  GemmArgs g{};
+  g.X = reinterpret_cast<const uint16_t*>(A);
+  g.W = reinterpret_cast<const uint16_t*>(B);
+  g.C = split_ws;
+  g.ldx = lda;
+  g.ldw = ldb;
+  g.ldc = N;
+  g.M = M;
+  g.N = N;
+  g.K = K / S;
+  g.split_c = (int64_t)M * N;
+  hipError_t e;
+  switch (t) {
+    case 0: e = launch_ring(s, EPI_F32, g, S); break;
+    case 1: e = launch_tile<256, 128, 4, 2>(s, EPI_F32, g, S); break;
+    default: e = launch_tile<128, 128, 2, 2>(s, EPI_F32, g, S); break;
+  }
+  if (e != hipSuccess) return e;
+  const int64_t work = (int64_t)M * (N / 4);
+  const dim3 grid((unsigned)((work + 255) / 256));
+  const float* part = reinterpret_cast<const float*>(split_ws);
+  switch (epi) {
+    case EPI_BF16: splitk_reduce_kernel<EPI_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
+    case EPI_RESID_F32: splitk_reduce_kernel<EPI_RESID_F32><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
+    case EPI_GELU_BF16: splitk_reduce_kernel<EPI_GELU_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 // Row split against the last, partly filled wave of tiles: rows [0, m1) run
@@ -782,43 +827,40 @@ static void gemm_plan_rows(int epi, int32_t M, int32_t N, int32_t K, int* t1, in
   }
 }
 
+// The row-split tail of a long contraction runs split over K on 256x256 ring
+// tiles.  A tail of at most 128 ring tiles on 128x128 tiles keeps the matrix
+// cores ~18% busy (each such tile moves twice the operand bytes per flop of a
+// ring tile; measured on the K=16384 down projection of the 2B-shaped
+// backbone, 1,801 rows: ~0.3 ms per launch), against ~60% on ring tiles; split
+// S ways (the largest power of two with tiles * S <= kSplitCUs, K/S >= 1024
+// and K % (64 S) == 0) the tail fills one wave of ring tiles and a reduction
+// adds the S fp32 partials in range order.  Only for K >= kTailSplitK: there
+// the 128x128 tail costs more than a tenth of the launch.  A tail row summed
+// in K ranges differs in the last bits from the same row computed in one
+// pass (in another batch it may not lie in a tail), so for such launches
+// grouped and isolated runs agree to rounding instead of bitwise.  Returns S
+// (1: no split) with the row plan of gemm_plan_rows.
+constexpr int32_t kTailSplitK = 8192;
+
+static int32_t gemm_tail_split(int epi, int32_t M, int32_t N, int32_t K, int32_t* m1, int* t1, int* t2) {
+  gemm_plan_rows(epi, M, N, K, t1, m1, t2);
+  if (*m1 >= M || *m1 <= 0 || K < kTailSplitK) return 1;
+  if (epi != EPI_BF16 && epi != EPI_RESID_F32 && epi != EPI_GELU_BF16) return 1;
+  if (N % 4 != 0) return 1;
+  const int64_t tiles = (int64_t)((M - *m1 + 255) / 256) * ((N + 255) / 256);
+  int32_t S = 1;
+  while (S < 16 && tiles * (2 * S) <= kSplitCUs && K % (kBK * 2 * S) == 0 && K / (2 * S) >= 1024) S *= 2;
+  return S;
+}
+
 hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const void* B, const void* B2, int64_t ldb,
                        void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, int tile_hint, void* split_ws,
                        size_t split_bytes) {
   if (M <= 0 || N <= 0 || K <= 0 || K % kBK != 0 || N % 32 != 0) return hipErrorInvalidValue;
   int t_split = 0, S = 1;
   if (tile_hint <= 0) gemm_plan(epi, M, N, K, &t_split, &S);
-  if (S > 1 && split_ws && split_bytes >= (size_t)S * M * N * sizeof(float)) {
-    GemmArgs g{};
-    g.X = reinterpret_cast<const uint16_t*>(A);
-    g.W = reinterpret_cast<const uint16_t*>(B);
-    g.C = split_ws;
-    g.ldx = lda;
-    g.ldw = ldb;
-    g.ldc = N;
-    g.M = M;
-    g.N = N;
-    g.K = K / S;
-    g.split_c = (int64_t)M * N;
-    hipError_t e;
-    switch (t_split) {
-      case 0: e = launch_ring(s, EPI_F32, g, S); break;
-      case 1: e = launch_tile<256, 128, 4, 2>(s, EPI_F32, g, S); break;
-      default: e = launch_tile<128, 128, 2, 2>(s, EPI_F32, g, S); break;
-    }
-    if (e != hipSuccess) return e;
-    const int64_t work = (int64_t)M * (N / 4);
-    const dim3 grid((unsigned)((work + 255) / 256));
-    const float* part = reinterpret_cast<const float*>(split_ws);
-    switch (epi) {
-      case EPI_BF16: splitk_reduce_kernel<EPI_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
-      case EPI_RESID_F32:
-        splitk_reduce_kernel<EPI_RESID_F32><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc);
-        break;
-      default: splitk_reduce_kernel<EPI_GELU_BF16><<<grid, 256, 0, s>>>(part, S, g.split_c, M, N, C, ldc); break;
-    }
-    return hipGetLastError();
-  }
+  if (S > 1 && split_ws && split_bytes >= (size_t)S * M * N * sizeof(float))
+    return launch_split(s, epi, A, lda, B, ldb, C, ldc, M, N, K, t_split, S, split_ws);
   GemmArgs g{};
   g.X = reinterpret_cast<const uint16_t*>(A);
   g.W = reinterpret_cast<const uint16_t*>(B);
@@ -835,15 +877,19 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
   }
   int t1, t2;
   int32_t m1;
-  gemm_plan_rows(epi, M, N, K, &t1, &m1, &t2);
+  const int32_t St = gemm_tail_split(epi, M, N, K, &m1, &t1, &t2);
   if (m1 > 0) {
     g.M = m1;
     const hipError_t e = launch_rows(s, epi, g, t1);
     if (e != hipSuccess || m1 == M) return e;
   }
   const size_t esize = (epi == EPI_RESID_F32 || epi == EPI_F32) ? 4 : 2;
+  void* Ct = static_cast<char*>(C) + (size_t)m1 * ldc * esize;
+  const void* At = reinterpret_cast<const uint16_t*>(A) + (int64_t)m1 * lda;
+  if (St > 1 && split_ws && split_bytes >= (size_t)St * (M - m1) * N * sizeof(float))
+    return launch_split(s, epi, At, lda, B, ldb, Ct, ldc, M - m1, N, K, 0, St, split_ws);
   g.X += (int64_t)m1 * lda;
-  g.C = static_cast<char*>(C) + (size_t)m1 * ldc * esize;
+  g.C = Ct;
   g.M = M - m1;
   return launch_rows(s, epi, g, t2);
 }

@@ -85,6 +85,23 @@ Group make_group(Rng& r, int G, int d, int max_reqs_per_tenant, int max_n, int m
   return g;
 }
 
+// One tenant, one request of n samples of exactly len rows.
+Group fixed_group(int d, int n, int len) {
+  Group g;
+  g.opts.d_model = d;
+  g.opts.align = 1;
+  g.ten.assign(1, jn_tenant{0x1234, d, 0});
+  g.lens.assign(1, std::vector<int32_t>(n, len));
+  jn_request q{};
+  q.tenant = 0;
+  q.n_samples = n;
+  q.max_len = len;
+  q.embeds = dev((size_t)n * len * d * 2);
+  q.lengths = g.lens[0].data();
+  g.req.push_back(q);
+  return g;
+}
+
 struct Packed {
   jn_pack_sizes sz{};
   jn_packed p{};
@@ -249,12 +266,19 @@ void check_backbones(jn_ctx* c) {
       {4, 768, 12, 0, 3072, 0, 0, 0.f, 1, 32, 244, 1},    // 12 heads of 64
       {1, 512, 4, 0, 1408, 1, 0, 0.f, 1, 1, 3, 64},       // one short sample (split-K launches)
       {2, 384, 6, 0, 1408, 1, 0, 0.f, 2, 70, 320, 1},     // widths that are not multiples of 256
+      {1, 2048, 8, 0, 8192, 1, 0, 0.f, 1, 40, 256, 1},    // long-K down projection: split row-split tail
   };
   for (const Case& cs : cases) {
-    Group g = make_group(r, cs.G, cs.d, cs.reqs, cs.n, cs.max_len, cs.align);
+    // the long-K case as 10,240 rows: 40 token tiles x 8 weight tiles, a
+    // row-split tail of 2,048 rows
+    Group g = cs.f >= 8192 ? fixed_group(cs.d, 40, 256) : make_group(r, cs.G, cs.d, cs.reqs, cs.n, cs.max_len, cs.align);
     Packed k = pack(c, g);
+    const long long l0 = jn_fake_launches;
     Bb b = make_backbone(2, cs.d, cs.H, cs.Hkv, cs.f, cs.glu, cs.causal, cs.theta);
     run_backbone(c, b, k);
+    // per layer: 2 norms, qkv, attention, o, geglu, down; + final norm; the
+    // split tail adds a partial launch and a reduction to the down projection
+    if (cs.f >= 8192) CHECK(jn_fake_launches - l0 == 2 * (2 + 1 + 1 + 2 + 1 + 3) + 1);
     CHECK(jn_ctx_set_trace(c, 1) == JN_OK);
     run_backbone(c, b, k);
     std::vector<jn_trace_entry> tr(4096);
