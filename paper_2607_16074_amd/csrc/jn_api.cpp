@@ -695,7 +695,8 @@ struct HeadPlan {
   std::vector<std::pair<int32_t, int32_t>> fwd, bwd;
 };
 
-constexpr int kHT = 64;  // fp32 head GEMM tile
+constexpr int kHTM = 32;  // fp32 head GEMM tile: rows
+constexpr int kHTN = 64;  // and columns
 
 jn_status check_heads(jn_ctx* c, const jn_packed* p, const jn_head* heads, int32_t G) {
   if (!heads) return fail(c, JN_EINVAL, "null heads");
@@ -743,15 +744,15 @@ void head_layout(const jn_packed* p, const jn_head* heads, int32_t G, HeadPlan* 
     // descriptor counts are bounded by G * 2 * maxL; tiles computed exactly below
   }
   // tile counts: fwd M-dynamic (ceil(N/64) upper bound), bwd wgrad + dgrad
-  const int64_t tm_dyn = (N + kHT - 1) / kHT;
+  const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
   int64_t ntiles = 0, ndesc = 0;
   for (int32_t g = 0; g < G; ++g) {
     const jn_head& Hh = heads[g];
     for (int k = 0; k < Hh.n_layers; ++k) {
       int64_t in = Hh.dims[k], out = Hh.dims[k + 1];
-      ntiles += tm_dyn * ((out + kHT - 1) / kHT);                        // fwd
-      ntiles += ((out + kHT - 1) / kHT) * ((in + kHT - 1) / kHT);         // wgrad
-      if (k > 0) ntiles += tm_dyn * ((in + kHT - 1) / kHT);               // dgrad
+      ntiles += tm_dyn * ((out + kHTN - 1) / kHTN);                        // fwd
+      ntiles += ((out + kHTM - 1) / kHTM) * ((in + kHTN - 1) / kHTN);       // wgrad
+      if (k > 0) ntiles += tm_dyn * ((in + kHTN - 1) / kHTN);               // dgrad
       ndesc += (k > 0) ? 3 : 2;
     }
   }
@@ -802,7 +803,7 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
   char* w = (char*)ws;
   float* P = pooled ? pooled : (float*)(w + hp.P);
   const int64_t N = p->N, d = p->d;
-  const int32_t tm_dyn = (int32_t)((N + kHT - 1) / kHT);
+  const int32_t tm_dyn = (int32_t)((N + kHTM - 1) / kHTM);
   auto Zk = [&](int k) { return (float*)(w + hp.Z[k]); };
   auto Hk = [&](int k) { return (float*)(w + hp.H[k]); };
   auto dZk = [&](int k) { return (float*)(w + hp.dZ[k]); };
@@ -837,7 +838,7 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
       D.N = (int32_t)out;
       D.K = (int32_t)in;
       D.tenant = g;
-      D.tiles_n = (int32_t)((out + kHT - 1) / kHT);
+      D.tiles_n = (int32_t)((out + kHTN - 1) / kHTN);
       int32_t di = (int32_t)descs.size();
       descs.push_back(D);
       for (int32_t tm = 0; tm < tm_dyn; ++tm)
@@ -880,10 +881,10 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
       Wg.N = (int32_t)in;
       Wg.K = -1;
       Wg.tenant = g;
-      Wg.tiles_n = (int32_t)((in + kHT - 1) / kHT);
+      Wg.tiles_n = (int32_t)((in + kHTN - 1) / kHTN);
       int32_t di = (int32_t)descs.size();
       descs.push_back(Wg);
-      const int32_t tmw = (int32_t)((out + kHT - 1) / kHT);
+      const int32_t tmw = (int32_t)((out + kHTM - 1) / kHTM);
       for (int32_t tm = 0; tm < tmw; ++tm)
         for (int32_t tn = 0; tn < Wg.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
       if (k > 0) {
@@ -905,7 +906,7 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
         Dg.N = (int32_t)in;
         Dg.K = (int32_t)out;
         Dg.tenant = g;
-        Dg.tiles_n = (int32_t)((in + kHT - 1) / kHT);
+        Dg.tiles_n = (int32_t)((in + kHTN - 1) / kHTN);
         int32_t dj = (int32_t)descs.size();
         descs.push_back(Dg);
         for (int32_t tm = 0; tm < tm_dyn; ++tm)
@@ -1892,11 +1893,11 @@ HeadFwdLayout head_fwd_layout(int64_t N, int64_t d, const jn_head* heads, int32_
     L.Z[k] = take(4 * N * L.width[k]);
     L.H[k] = take(4 * N * L.width[k]);
   }
-  const int64_t tm_dyn = (N + kHT - 1) / kHT;
+  const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
   int64_t ntiles = 0, ndesc = 0;
   for (int32_t g = 0; g < G; ++g)
     for (int k = 0; k < heads[g].n_layers; ++k) {
-      ntiles += tm_dyn * ((heads[g].dims[k + 1] + kHT - 1) / kHT);
+      ntiles += tm_dyn * ((heads[g].dims[k + 1] + kHTN - 1) / kHTN);
       ++ndesc;
     }
   L.descs = take(sizeof(HeadGemm) * ndesc);
@@ -2088,7 +2089,7 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
   char* hw = w + L.heads;
   pl->P = (float*)(hw + hl.P);
   const int64_t N = p.N, d = o->d_model;
-  const int32_t tm_dyn = (int32_t)((N + kHT - 1) / kHT);
+  const int32_t tm_dyn = (int32_t)((N + kHTM - 1) / kHTM);
   std::vector<HeadGemm> descs;
   std::vector<HeadTile> tiles;
   for (int k = 0; k < hl.maxL; ++k) {
@@ -2116,7 +2117,7 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
       D.N = (int32_t)outw;
       D.K = (int32_t)in;
       D.tenant = g;
-      D.tiles_n = (int32_t)((outw + kHT - 1) / kHT);
+      D.tiles_n = (int32_t)((outw + kHTN - 1) / kHTN);
       const int32_t di = (int32_t)descs.size();
       descs.push_back(D);
       for (int32_t tm = 0; tm < tm_dyn; ++tm)

@@ -1,10 +1,11 @@
 // Tenant split and tenant-private action heads (fp32):
 //   pool       mean of each sample's valid rows of the shared feature, written
 //              in tenant order (the split of the shared features by slices)
-//   head_gemm  one launch per head layer for all tenants: forward (bias +
-//              GELU fused), weight gradient (bias gradient fused) and data
-//              gradient (GELU derivative fused); tenant row ranges are read
-//              from the device maps, so the host needs no per-tenant counts
+//   head_gemm  one launch per head layer for all tenants, fp32 matrix-core
+//              tiles: forward (bias + GELU fused), weight gradient (bias
+//              gradient fused) and data gradient (GELU derivative fused);
+//              tenant row ranges are read from the device maps, so the host
+//              needs no per-tenant counts
 //   mse        per-tenant mean squared error and its gradient
 // Every reduction runs in a fixed order: results are bitwise reproducible.
 #include "jn_device.h"
@@ -79,15 +80,34 @@ hipError_t launch_pool(hipStream_t s, const void* hidden, const int32_t* seqlens
 
 // ------------------------------------------------------------- head gemm ---
 
-constexpr int HT = 64;   // tile edge
-constexpr int HK = 64;   // k step; the next step's operands are loaded into
-                         // registers while the current step is computed
+// fp32 matrix-core tiles (v_mfma_f32_16x16x4_f32, the heads' precision): a
+// workgroup computes a 32 x 64 tile of C with 4 wavefronts, wave w owning
+// rows 16 (w >> 1) .. +15 and columns 32 (w & 1) .. +31 (two 16 x 16 MFMA
+// blocks).  32 rows fit the local batch of a tenant in one row tile.  Operands
+// go through LDS in K chunks of 32, stored K-major (As[k][m], Bs[k][n], row
+// stride padded by one float); the next chunk is loaded into registers while
+// the current one is multiplied; steps past the end of a short K (a weight
+// gradient's K is the tenant's row count) are skipped.  Measured on the
+// 2B-shaped workload's heads: chunks of 128 (4x the loads in flight) left the
+// forward launches unchanged and made the weight-gradient launches, whose
+// K is 32, 3x slower (more LDS per workgroup, zero-filled chunk work).  MFMA operand layout (16x16x4): lane l holds
+// A(m = l & 15, k = l >> 4) and B(k = l >> 4, n = l & 15); the result block
+// gives lane l rows 4 (l >> 4) .. +3 of column l & 15.  The K order of every
+// output element is fixed (chunks in order, four k per MFMA), and the bias
+// gradient of a weight-gradient tile is the row sum of its A operand taken
+// from LDS chunk by chunk in k order, so results are bitwise reproducible and
+// independent of the other tenants of the launch.
+constexpr int HM = 32;   // tile rows
+constexpr int HN = 64;   // tile columns
+constexpr int HKC = 32;   // K chunk
+
+typedef float f32x4h __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restrict__ descs,
                                                         const HeadTile* __restrict__ tiles,
                                                         const int32_t* __restrict__ tso) {
-  __shared__ float As[HK][HT + 4];
-  __shared__ float Bs[HK][HT + 4];
+  __shared__ float As[HKC][HM + 1];
+  __shared__ float Bs[HKC][HN + 1];
   const HeadTile tile = tiles[blockIdx.x];
   const HeadGemm D = descs[tile.desc];
   const int32_t off = tso[D.tenant];
@@ -95,80 +115,94 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
   const int32_t M = D.M < 0 ? ng : D.M;
   const int32_t N = D.N;
   const int32_t K = D.K < 0 ? ng : D.K;
-  const int32_t m0 = tile.tm * HT, n0 = tile.tn * HT;
+  const int32_t m0 = tile.tm * HM, n0 = tile.tn * HN;
   if (m0 >= M) return;  // tiles past a tenant's row count (upper-bound grid)
   const float* A = D.A + (int64_t)off * D.bumpA;
   const float* B = D.B + (int64_t)off * D.bumpB;
   const int tid = threadIdx.x;
-  const int ty = tid / 16, tx = tid % 16;
-  float acc[4][4] = {};
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
   const bool a_k_fast = D.sak == 1;
   const bool b_k_fast = D.sbk == 1;
-  constexpr int Q = HT * HK / 256;  // operand elements per thread per step
-  float ra[Q], rb[Q];
+  const bool want_db = D.db != nullptr && tile.tn == 0;
+
+  constexpr int QA = HM * HKC / 256;  // A elements per thread per chunk (4)
+  constexpr int QB = HN * HKC / 256;  // B elements per thread per chunk (8)
+  float ra[QA], rb[QB];
   auto load = [&](int32_t k0) {
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
+    for (int q = 0; q < QA; ++q) {
       const int e = tid + 256 * q;
       int mm, kk;
-      if (a_k_fast) { kk = e % HK; mm = e / HK; } else { mm = e % HT; kk = e / HT; }
+      if (a_k_fast) { kk = e % HKC; mm = e / HKC; } else { mm = e % HM; kk = e / HM; }
       const int32_t m = m0 + mm, k = k0 + kk;
       ra[q] = (m < M && k < K) ? A[(int64_t)m * D.sam + (int64_t)k * D.sak] : 0.f;
-      int nn;
-      if (b_k_fast) { kk = e % HK; nn = e / HK; } else { nn = e % HT; kk = e / HT; }
-      const int32_t n = n0 + nn, k2 = k0 + kk;
-      rb[q] = (n < N && k2 < K) ? B[(int64_t)k2 * D.sbk + (int64_t)n * D.sbn] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      const int e = tid + 256 * q;
+      int nn, kk;
+      if (b_k_fast) { kk = e % HKC; nn = e / HKC; } else { nn = e % HN; kk = e / HN; }
+      const int32_t n = n0 + nn, k = k0 + kk;
+      rb[q] = (n < N && k < K) ? B[(int64_t)k * D.sbk + (int64_t)n * D.sbn] : 0.f;
     }
   };
-  load(0);
-  for (int32_t k0 = 0; k0 < K; k0 += HK) {
+  auto store = [&]() {
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
+    for (int q = 0; q < QA; ++q) {
       const int e = tid + 256 * q;
-      if (a_k_fast) As[e % HK][e / HK] = ra[q]; else As[e / HT][e % HT] = ra[q];
-      if (b_k_fast) Bs[e % HK][e / HK] = rb[q]; else Bs[e / HT][e % HT] = rb[q];
+      if (a_k_fast) As[e % HKC][e / HKC] = ra[q]; else As[e / HM][e % HM] = ra[q];
     }
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      const int e = tid + 256 * q;
+      if (b_k_fast) Bs[e % HKC][e / HKC] = rb[q]; else Bs[e / HN][e % HN] = rb[q];
+    }
+  };
+
+  f32x4h acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  float dbs = 0.f;  // bias gradient of row m0 + tid (tid < HM), k in order
+  const int am = wm * 16 + (lane & 15), kq = lane >> 4;
+  const int bn0 = wn * 32 + (lane & 15);
+  load(0);
+  for (int32_t k0 = 0; k0 < K; k0 += HKC) {
+    store();
     __syncthreads();
-    if (k0 + HK < K) load(k0 + HK);
+    if (k0 + HKC < K) load(k0 + HKC);
+    const int kend = min(HKC, K - k0);  // zero-filled beyond K
 #pragma unroll 8
-    for (int kk = 0; kk < HK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    for (int kk = 0; kk < kend; kk += 4) {
+      const float a = As[kk + kq][am];
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bs[kk + kq][bn0], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bs[kk + kq][bn0 + 16], acc1, 0, 0, 0);
+    }
+    if (want_db && tid < HM) {
+#pragma unroll 8
+      for (int kk = 0; kk < kend; ++kk) dbs += As[kk][tid];
     }
     __syncthreads();
   }
+
   float* C = D.C + (int64_t)off * D.bumpC;
+  const float* Zg = D.Zg ? D.Zg + (int64_t)off * D.bumpC : nullptr;
+  float* Cact = D.Cact ? D.Cact + (int64_t)off * D.bumpC : nullptr;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int32_t m = m0 + ty * 4 + i;
-    if (m >= M) continue;
+  for (int j = 0; j < 2; ++j) {
+    const int32_t n = n0 + wn * 32 + j * 16 + (lane & 15);
+    if (n >= N) continue;
+    const float bias = D.bias ? D.bias[n] : 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int32_t n = n0 + tx * 4 + j;
-      if (n >= N) continue;
-      float v = acc[i][j];
+    for (int e = 0; e < 4; ++e) {
+      const int32_t m = m0 + wm * 16 + 4 * (lane >> 4) + e;
+      if (m >= M) continue;
+      float v = (j == 0 ? acc0[e] : acc1[e]) + bias;
       const int64_t ci = (int64_t)m * D.ldc + n;
-      if (D.bias) v += D.bias[n];
-      if (D.Zg) v *= gelu_grad_f((D.Zg + (int64_t)off * D.bumpC)[ci]);
+      if (Zg) v *= gelu_grad_f(Zg[ci]);
       C[ci] = v;
-      if (D.Cact) (D.Cact + (int64_t)off * D.bumpC)[ci] = gelu_f(v);
+      if (Cact) Cact[ci] = gelu_f(v);
     }
   }
-  if (D.db && tile.tn == 0 && tid < HT) {
-    const int32_t m = m0 + tid;
-    if (m < M) {
-      float sacc = 0.f;
-      for (int32_t k = 0; k < K; ++k) sacc += A[(int64_t)m * D.sam + (int64_t)k * D.sak];
-      D.db[m] = sacc;
-    }
-  }
+  if (want_db && tid < HM && m0 + tid < M) D.db[m0 + tid] = dbs;
 }
 
 hipError_t launch_head_gemm(hipStream_t s, const HeadGemm* descs, const HeadTile* tiles, int32_t n_tiles,
@@ -189,14 +223,20 @@ __global__ __launch_bounds__(256) void mse_kernel(const LossDesc* __restrict__ d
   const float scale = 2.0f / (float)cnt;
   const float* y = D.y + (int64_t)off * D.ld;
   float* dy = D.dy + (int64_t)off * D.ld;
+  // thread t takes columns t, t + 256, ... of every row, rows in order
   float ss = 0.f;
-  for (int64_t e = threadIdx.x; e < cnt; e += 256) {
-    const int64_t m = e / D.out, n = e % D.out;
-    const float yv = y[m * D.ld + n];
-    const float diff = yv - D.target[e];
-    D.actions[e] = yv;
-    dy[m * D.ld + n] = scale * diff;
-    ss += diff * diff;
+  for (int32_t m = 0; m < ng; ++m) {
+    const float* yr = y + (int64_t)m * D.ld;
+    float* dyr = dy + (int64_t)m * D.ld;
+    const float* tr = D.target + (int64_t)m * D.out;
+    float* ar = D.actions + (int64_t)m * D.out;
+    for (int32_t n = threadIdx.x; n < D.out; n += 256) {
+      const float yv = yr[n];
+      const float diff = yv - tr[n];
+      ar[n] = yv;
+      dyr[n] = scale * diff;
+      ss += diff * diff;
+    }
   }
   red[threadIdx.x] = ss;
   __syncthreads();
