@@ -355,25 +355,25 @@ __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_grouped_kernel(const G
   gemm_tile<BN, BM, WGN, WGM, EPI>(g, b - g.tile_start, lds);
 }
 
-// Epilogues of the 256x256 ring loop that stage the tile through the (then
-// free) LDS so that global memory sees whole rows: 16-byte lanes, each wave
-// instruction covering complete 128-byte lines.  Written directly from the
-// MFMA layout, each lane would touch 8 or 16 bytes of 16 different rows per
-// instruction.  Measured on the 2048-wide shapes: QKV (bf16) 1.70-1.78 ->
-// 1.61 ms, O (fp32 residual, K=2048) 0.716 -> 0.690 ms; the GeGLU tile (half
-// as many columns, GELU-bound) gains nothing and keeps the direct path.
-// The caller has passed a barrier after the last fragment read.
-//
-// bf16 / GELU-bf16: the whole 256 x 256 tile (row stride padded by 16 bytes,
-// 132 KB), then 32 rows per wave, 2 rows per instruction.
-template <int EPI>
-__device__ __forceinline__ void ring_epilogue_bf16(const GemmArgs& g, const f32x4 (&acc)[8][4], uint16_t* lds,
+// bf16 / GELU-bf16 epilogue of the 256x256 ring loop: the tile is staged
+// through the (then free) LDS, row stride padded by 16 bytes (132 KB), so that
+// global memory sees whole rows (16-byte lanes, 256 / NW rows per wave, 2 rows
+// per instruction); written directly from the MFMA layout, each lane would
+// touch 8 bytes of 16 different rows per instruction.  The caller has passed a
+// barrier after the loop's last LDS access.  Wave w holds accumulator rows
+// wm * 16 TM ...  The GeGLU tile (GELU-bound) and the fp32 residual add keep
+// the direct path: with four waves the staged residual add (two 128-row halves,
+// each read-add-write of C behind a barrier) measured 0.83 ms on the 2048x2048
+// O projection against 0.75 direct, and 4.21 against 3.78 ms on the down
+// projection.
+template <int EPI, int TM, int NW>
+__device__ __forceinline__ void ring_epilogue_bf16(const GemmArgs& g, const f32x4 (&acc)[8][TM], uint16_t* lds,
                                                    int32_t tm, int32_t tn, int wn, int wm, int wave, int lane) {
   constexpr int OS = 256 + 8;  // LDS row stride (elements)
   const int q4 = (lane >> 4) * 4;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = wm * 64 + j * 16 + (lane & 15);
+  for (int j = 0; j < TM; ++j) {
+    const int row = wm * 16 * TM + j * 16 + (lane & 15);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       float v[4];
@@ -387,90 +387,46 @@ __device__ __forceinline__ void ring_epilogue_bf16(const GemmArgs& g, const f32x
   __builtin_amdgcn_s_barrier();
   const int c = lane & 31, rr = lane >> 5;  // 32 chunks of 16 bytes per row
   const int32_t n = tn * 256 + c * 8;
+  constexpr int RW = 256 / NW;  // rows per wave
 #pragma unroll
-  for (int it = 0; it < 16; ++it) {
-    const int row = wave * 32 + it * 2 + rr;
+  for (int it = 0; it < RW / 2; ++it) {
+    const int row = wave * RW + it * 2 + rr;
     const int32_t m = tm * 256 + row;
     const uint4 v = *reinterpret_cast<const uint4*>(lds + row * OS + c * 8);
     if (m < g.M && n < g.N) *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(g.C) + (int64_t)m * g.ldc + n) = v;
   }
 }
 
-// fp32 residual add: two halves of 128 token rows (row stride padded by 16
-// bytes, 130 KB each); in each half the waves holding those rows write them,
-// then every wave adds 16 whole 1 KB rows into C.
-__device__ __forceinline__ void ring_epilogue_resid(const GemmArgs& g, const f32x4 (&acc)[8][4], uint16_t* lds,
-                                                    int32_t tm, int32_t tn, int wn, int wm, int wave, int lane) {
-  constexpr int OS = 256 + 4;  // LDS row stride (floats)
-  float* const ot = reinterpret_cast<float*>(lds);
-  const int q4 = (lane >> 4) * 4;
-  const int32_t n = tn * 256 + lane * 4;
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    if ((wm >> 1) == half) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = (wm & 1) * 64 + j * 16 + (lane & 15);
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          *reinterpret_cast<float4*>(ot + row * OS + wn * 128 + i * 16 + q4) =
-              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-      }
-    }
-    wait_lgkmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    float4 cv[16];
-#pragma unroll
-    for (int it = 0; it < 16; ++it) {
-      const int32_t m = tm * 256 + half * 128 + wave * 16 + it;
-      if (m < g.M && n < g.N)
-        cv[it] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g.C) + (int64_t)m * g.ldc + n);
-    }
-#pragma unroll
-    for (int it = 0; it < 16; ++it) {
-      const int row = wave * 16 + it;
-      const int32_t m = tm * 256 + half * 128 + row;
-      if (m < g.M && n < g.N) {
-        const float4 a = *reinterpret_cast<const float4*>(ot + row * OS + lane * 4);
-        float4 o = cv[it];
-        o.x += a.x;
-        o.y += a.y;
-        o.z += a.z;
-        o.w += a.w;
-        *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.C) + (int64_t)m * g.ldc + n) = o;
-      }
-    }
-    if (half == 0) {  // the second half's writes reuse the buffer
-      wait_lgkmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-    }
-  }
+// Buffer resource of a row-major bf16 panel starting at `base`, `bytes` long
+// (loads past the end return zero).  Word 3 is the CDNA raw-buffer format.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const uint16_t* base, int64_t bytes) {
+  const int32_t n = (int32_t)min(bytes, (int64_t)0x7fffffff);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, n, 0x00020000);
 }
 
-// Ring-buffered ping-pong loop of the 256x256 tile (8 wavefronts).  Waves w
-// and w+4 share a SIMD; group 0 (waves 0-3) and group 1 (waves 4-7)
-// alternate between a memory phase (all 24 fragments of one K=64 slab from
-// LDS) and a compute phase (the slab's 64 MFMAs, which only read registers),
-// one workgroup barrier per phase, group 1 one phase behind group 0.  The LDS
-// holds two weight slots and three token slots of one slab each (5 x 32 KB =
-// 160 KB).  Group 0 fetches the weight half of slab kt+1 as one burst at the
-// start of its memory phase of slab kt; group 1 fetches the token half of
-// slab kt+3, spread over its compute phase of slab kt, into the slot slab kt
-// used.  Token rows are thus requested two slabs ahead of their first read,
-// weight rows one slab ahead; every wave waits for its own DMA before the
-// barrier that precedes the first read of that slab.  Measured on the
-// 2048-wide shapes: a third slot took the K=16384 residual projection from
-// 4.81 to 4.50 ms over a two-slot ping-pong loop (32x32x16 form), which was
-// itself 9.5% faster there than the interleaved loop; giving the third slot
-// to the token operand instead of the weights made the 2B-shaped step
-// 0.8-2.6% faster (the weight slabs, read by every XCD at about the same
-// time, arrive sooner than the token slabs).  Issuing the token DMA in the
-// first half of the compute phase instead of spreading it over the whole
-// phase made the step 3% slower.  Split-K ranges come from blockIdx.y as in
-// gemm_kernel.
+// Ring-buffered loop of the 256x256 tile on 4 wavefronts, one per SIMD, each
+// 128 weight rows x 128 tokens (64 accumulator blocks, kept in the
+// accumulation registers).  Per K=64 slab kt, phase 0 runs the first k-half's
+// 64 MFMAs while reading the second half's fragments and fetching the token
+// half of slab kt+2; every wave then waits for its own DMA of slab kt+1 and a
+// workgroup barrier; phase 1 runs the second half's MFMAs while reading slab
+// kt+1's first-half fragments and fetching the weight half of slab kt+2.  The
+// LDS holds two weight slots and three token slots (5 x 32 KB = 160 KB): a
+// slot is refilled only after the barrier that follows its last fragment
+// read.  The stream has no branches: past the last slab the DMAs repeat slab
+// KT-1 into free slots and the fragment reads read a free slot, so every
+// phase issues the same instructions; each DMA is one buffer load to LDS with
+// a per-lane 32-bit offset and the slab offset in a scalar register.
+// Measured on the 2048-wide shapes against the 8-wave ping-pong loop it
+// replaces (two waves per SIMD alternating memory and compute phases): GeGLU
+// 8.27 -> 7.36 ms, QKV 1.63 -> 1.50 ms.  Per-phase cycle stamps showed what
+// the 8-wave loop and the first 4-wave versions lost: each conditional branch
+// in the MFMA stream cost 30-50 cycles of issue, and global_load_lds with a
+// 64-bit address computed per instruction cost more than the buffer form.
+// Split-K ranges come from blockIdx.y as in gemm_kernel.
 template <int EPI>
-__global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
-  constexpr int BN = 256, BM = 256, WGN = 2, WGM = 4;
+__global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
+  constexpr int BN = 256, BM = 256, WGN = 2, WGM = 2;
   constexpr int WN = BN / WGN, WM = BM / WGM;
   constexpr int TN = WN / 16, TM = WM / 16;
   constexpr int NI = 8;            // 1 KB DMA instructions per wave per half-slab
@@ -485,22 +441,39 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave / WGM, wm = wave % WGM;
-  const int grp = wave >> 2, sub = wave & 3;
 
-  // group 0: weight rows 64*sub .. +63 of the tile; group 1: token rows
-  const uint16_t* src[NI];
+  // panels of this tile: token rows tm*256.., weight rows (GeGLU: gate and up
+  // columns tn*128..) -- rows past the end are clamped to the last one
+  const int32_t m0 = tm * BM;
+  const int32_t c0 = GLU ? tn * (BN / 2) : tn * BN;
+  const uint16_t* const xb = g.X + (int64_t)m0 * g.ldx;
+  const uint16_t* const wb = g.W + (int64_t)c0 * g.ldw;
+  const uint16_t* const wb2 = GLU ? g.W2 + (int64_t)c0 * g.ldw : wb;
+  const __amdgpu_buffer_rsrc_t xr = panel_rsrc(xb, (int64_t)(M - m0) * g.ldx * 2);
+  const __amdgpu_buffer_rsrc_t wr = panel_rsrc(wb, (int64_t)(g.N - c0) * g.ldw * 2);
+  const __amdgpu_buffer_rsrc_t wr2 = panel_rsrc(wb2, (int64_t)(g.N - c0) * g.ldw * 2);
+  // wave w fetches rows 64w .. 64w+63 of both halves, 8 rows per instruction
+  uint32_t xo[NI], wo[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
-    const int r = 64 * sub + 8 * i + (lane >> 3);
+    const int r = 64 * wave + 8 * i + (lane >> 3);
     const int chunk = (lane & 7) ^ lds_swz(r);
-    if (grp == 1)
-      src[i] = g.X + (int64_t)min(tm * BM + r, M - 1) * g.ldx + chunk * 8;
-    else
-      src[i] = weight_row<GLU>(g.W, g.W2, g.ldw, tn, BN, r, g.N) + chunk * 8;
+    xo[i] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * g.ldx + chunk * 8) * 2);
+    const int32_t col = GLU ? min(c0 + (r >> 5) * 16 + (r & 15), g.N - 1) : min(c0 + r, g.N - 1);
+    wo[i] = (uint32_t)(((int64_t)(col - c0) * g.ldw + chunk * 8) * 2);
   }
-  const int dro = sub * NI * 512;  // this wave's 1 KB blocks inside a slot
+  const int dro = wave * NI * 512;         // this wave's 1 KB blocks inside a slot
   uint16_t* const ring2 = lds;             // weight slabs, slot kt % 2
   uint16_t* const ring3 = lds + 2 * SLOT;  // token slabs, slot kt % 3
+  // DMA i of slab `slab` into a slot; in GeGLU tiles, instruction i covers
+  // weight rows of one 16-row block, all gate (W) or all up (W2)
+#define JN_DMA_W(i, slab, slot)                                                                                  \
+  __builtin_amdgcn_raw_ptr_buffer_load_lds((GLU && (((i) >> 1) & 1)) ? wr2 : wr,                                \
+                                           JN_LPTR(ring2 + (slot) * SLOT + dro + (i) * 512), 16, wo[i],         \
+                                           (slab) * (kBK * 2), 0, 0)
+#define JN_DMA_X(i, slab, slot)                                                                                  \
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, JN_LPTR(ring3 + (slot) * SLOT + dro + (i) * 512), 16, xo[i],      \
+                                           (slab) * (kBK * 2), 0, 0)
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -512,105 +485,112 @@ __global__ __launch_bounds__(512, 1) void gemm_ring_kernel(GemmArgs g0) {
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = wm * WM + (lane & 15);
 
-  // prologue: slab 0 whole, token halves of slabs 1 and 2 in flight; group 1
-  // then waits one extra barrier, which puts it one phase behind group 0
-  if (grp == 0) {
+  // prologue: slabs 0 and 1 (both halves), then slab 0's first-half fragments
+  {
+    const int s1 = min(1, KT - 1);
 #pragma unroll
-    for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(ring2 + dro + i * 512), 16, 0, 0);
-    wait_vmcnt<0>();
-  } else {
+    for (int i = 0; i < NI; ++i) JN_DMA_W(i, 0, 0);
 #pragma unroll
-    for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(ring3 + dro + i * 512), 16, 0, 0);
-    if (KT > 1) {
+    for (int i = 0; i < NI; ++i) JN_DMA_X(i, 0, 0);
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(ring3 + SLOT + dro + i * 512), 16, 0, 0);
-      wait_vmcnt<NI>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    for (int i = 0; i < NI; ++i) JN_DMA_X(i, s1, 1);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) JN_DMA_W(i, s1, 1);
+    wait_vmcnt<2 * NI>();
   }
   __builtin_amdgcn_s_barrier();
-  if (grp == 1) {
-    if (KT > 2) {
+  bf16x8 fa[TN + TM], fb[TN + TM];  // first-half / second-half fragments: weights, then tokens
+  {
+    const int pos = quad ^ sw;
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + 2 * kBK), JN_LPTR(ring3 + 2 * SLOT + dro + i * 512), 16, 0,
-                                         0);
-    }
-    __builtin_amdgcn_s_barrier();
+    for (int i = 0; i < TN; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(ring2 + (wrow + 16 * i) * kBK + pos * 8);
+#pragma unroll
+    for (int j = 0; j < TM; ++j) fa[TN + j] = *reinterpret_cast<const bf16x8*>(ring3 + (xrow + 16 * j) * kBK + pos * 8);
   }
+  wait_lgkmcnt<0>();
 
-  bf16x8 fw[2][TN], fx[2][TM];
   int slot3 = 0;  // kt % 3
   for (int kt = 0; kt < KT; ++kt) {
-    const uint16_t* cw = ring2 + (kt & 1) * SLOT;
-    const uint16_t* cx = ring3 + slot3 * SLOT;
-    // ---- memory phase: slab kt's fragments (+ group 0: weight half of slab kt+1)
-    __builtin_amdgcn_sched_barrier(0);
-    if (grp == 0 && kt + 1 < KT) {
-      uint16_t* const fdst = ring2 + ((kt + 1) & 1) * SLOT + dro;
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + (kt + 1) * kBK), JN_LPTR(fdst + i * 512), 16, 0, 0);
-    }
-#pragma unroll
-    for (int step = 0; step < 2; ++step) {
-      const int pos = (4 * step + quad) ^ sw;
-      gemm_frags<TN>(fw[step], cw, wrow, pos);
-      gemm_frags<TM>(fx[step], cx, xrow, pos);
-    }
-    wait_lgkmcnt<0>();
-    if (grp == 1) {  // token half of slab kt+1 (the one of kt+2 may stay in flight)
-      if (kt + 2 < KT)
-        wait_vmcnt<NI>();
-      else
-        wait_vmcnt<0>();
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    // ---- compute phase: 64 MFMAs from registers (+ group 1: token half of slab kt+3)
-    const bool fill = grp == 1 && kt + 3 < KT;
-    uint16_t* const gdst = ring3 + slot3 * SLOT + dro;
-#pragma unroll
-    for (int step = 0; step < 2; ++step) {
+    const int slot2 = kt & 1;
+    const int next3 = slot3 == 2 ? 0 : slot3 + 1;   // (kt + 1) % 3
+    const int prev3 = slot3 == 0 ? 2 : slot3 - 1;   // (kt + 2) % 3
+    const int sf = min(kt + 2, KT - 1);             // slab fetched this iteration
+    // ---- phase 0: first k-half MFMAs; second-half fragments; token DMA of slab kt+2
+    {
+      const uint16_t* cw = ring2 + slot2 * SLOT;
+      const uint16_t* cx = ring3 + slot3 * SLOT;
+      const int pos = (4 + quad) ^ sw;
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int q = 0; q < TN * TM; ++q) {
         const int i = q / TM, j = q % TM;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[step][i], fx[step][j], acc[i][j], 0, 0, 0);
-        const int d = step * TN * TM + q;
-        if ((d & 7) == 7 && fill)
-          __builtin_amdgcn_global_load_lds(JN_GPTR(src[d >> 3] + (kt + 3) * kBK), JN_LPTR(gdst + (d >> 3) * 512), 16,
-                                           0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fa[TN + j], acc[i][j], 0, 0, 0);
+        if ((q & 3) == 0) {
+          const int f = q >> 2;
+          if (f < TN)
+            fb[f] = *reinterpret_cast<const bf16x8*>(cw + (wrow + 16 * f) * kBK + pos * 8);
+          else
+            fb[f] = *reinterpret_cast<const bf16x8*>(cx + (xrow + 16 * (f - TN)) * kBK + pos * 8);
+        }
+        if ((q & 7) == 6) JN_DMA_X(q >> 3, sf, prev3);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if (grp == 0) wait_vmcnt<0>();  // weight half of slab kt+1
+    // slab kt+1 landed (the token DMA of slab kt+2, issued last, may stay in flight)
+    wait_lgkmcnt<0>();
+    wait_vmcnt<NI>();
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    slot3 = slot3 == 2 ? 0 : slot3 + 1;
+    // ---- phase 1: second k-half MFMAs; slab kt+1's first-half fragments; weight DMA of slab kt+2
+    {
+      const uint16_t* nw = ring2 + (slot2 ^ 1) * SLOT;
+      const uint16_t* nx = ring3 + next3 * SLOT;
+      const int pos = quad ^ sw;
+#pragma unroll
+      for (int q = 0; q < TN * TM; ++q) {
+        const int i = q / TM, j = q % TM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[i], fb[TN + j], acc[i][j], 0, 0, 0);
+        if ((q & 3) == 0) {
+          const int f = q >> 2;
+          if (f < TN)
+            fa[f] = *reinterpret_cast<const bf16x8*>(nw + (wrow + 16 * f) * kBK + pos * 8);
+          else
+            fa[f] = *reinterpret_cast<const bf16x8*>(nx + (xrow + 16 * (f - TN)) * kBK + pos * 8);
+        }
+        if ((q & 7) == 6) JN_DMA_W(q >> 3, sf, slot2);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    wait_lgkmcnt<0>();
+    slot3 = next3;
   }
-  if (grp == 0) __builtin_amdgcn_s_barrier();  // equal barrier counts in both groups
+#undef JN_DMA_W
+#undef JN_DMA_X
+  wait_vmcnt<0>();  // the repeated slabs' DMAs land before the LDS is reused or released
 
-  if constexpr (EPI == EPI_BF16 || EPI == EPI_GELU_BF16)
-    ring_epilogue_bf16<EPI>(g, acc, lds, tm, tn, wn, wm, wave, lane);
-  else if constexpr (EPI == EPI_RESID_F32)
-    ring_epilogue_resid(g, acc, lds, tm, tn, wn, wm, wave, lane);
-  else
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_GELU_BF16) {
+    __builtin_amdgcn_s_barrier();
+    ring_epilogue_bf16<EPI, TM, 4>(g, acc, lds, tm, tn, wn, wm, wave, lane);
+  } else {
     gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
+  }
 }
 
-// The 256x256 ring loop over all tiles of g (grid.y = split-K ranges).
+template <int BN, int BM, int WGN, int WGM>
+static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1);
+
+// The 256x256 ring loop over all tiles of g (grid.y = split-K ranges).  Its
+// per-lane panel offsets are 32-bit: leading dimensions beyond 4M elements
+// take the 256x128 loop (same MFMA sequence per output element).
 static hipError_t launch_ring(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1) {
+  if ((int64_t)256 * std::max(g.ldx, g.ldw) * 2 > (int64_t)0x7fffffff)
+    return launch_tile<256, 128, 4, 2>(s, epi, g, splits);
   const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
   g.tiles_m = (g.M + 255) / 256;
   g.tiles_n = (NL + 255) / 256;
   g.tile_start = 0;
-  const dim3 grid(g.tiles_m * g.tiles_n, splits), block(512);
+  const dim3 grid(g.tiles_m * g.tiles_n, splits), block(256);
   switch (epi) {
     case EPI_BF16: gemm_ring_kernel<EPI_BF16><<<grid, block, 0, s>>>(g); break;
     case EPI_GELU_BF16: gemm_ring_kernel<EPI_GELU_BF16><<<grid, block, 0, s>>>(g); break;
@@ -623,7 +603,7 @@ static hipError_t launch_ring(hipStream_t s, int epi, GemmArgs g, int32_t splits
 }
 
 template <int BN, int BM, int WGN, int WGM>
-static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1) {
+static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits) {
   const int32_t NL = epi == EPI_GEGLU_BF16 ? 2 * g.N : g.N;
   g.tiles_m = (g.M + BM - 1) / BM;
   g.tiles_n = (NL + BN - 1) / BN;
