@@ -230,26 +230,22 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = BN + wm * WM + (lane & 15);
 
-  // prologue: slabs 0 and 1 in flight
+  // prologue: slab 0; slab kt+1 is fetched during slab kt's first half
 #pragma unroll
   for (int i = 0; i < NI; ++i)
     __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(dst0 + i * 512), 16, 0, 0);
-  if (KT > 1) {
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + kBK), JN_LPTR(dst0 + STAGE + i * 512), 16, 0, 0);
-    wait_vmcnt<NI>();
-  } else {
-    wait_vmcnt<0>();
-  }
+  wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
 
+  // The loop body has no branches (each one in the MFMA stream costs tens of
+  // cycles of issue): the last slab's fetch repeats slab KT-1 into the free
+  // buffer, and its next-slab fragment reads read that buffer.
   bf16x8 fw[2][TN], fx[2][TM];
   gemm_frags<TN>(fw[0], lds, wrow, quad ^ sw);
   gemm_frags<TM>(fx[0], lds, xrow, quad ^ sw);
   for (int kt = 0; kt < KT; ++kt) {
     const uint16_t* cur = lds + (kt & 1) * STAGE;
-    const bool fill = kt >= 1 && kt + 1 < KT;  // slab kt+1 goes into the buffer slab kt-1 used
+    const int sf = min(kt + 1, KT - 1);  // slab fetched into the buffer slab kt-1 used
     uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
 #pragma unroll
     for (int step = 0; step < 2; ++step) {
@@ -257,7 +253,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
         const int pos = (4 + quad) ^ sw;
         gemm_frags<TN>(fw[1], cur, wrow, pos);
         gemm_frags<TM>(fx[1], cur, xrow, pos);
-      } else if (kt + 1 < KT) {
+      } else {
         wait_vmcnt<0>();
         wait_lgkmcnt<0>();
         __builtin_amdgcn_s_barrier();
@@ -275,13 +271,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
 #pragma unroll
         for (int e = 0; e < PER; ++e) {
           const int d = (step * TN * TM + q) * PER + e;
-          if (d < NI && fill)
-            __builtin_amdgcn_global_load_lds(JN_GPTR(src[d] + (kt + 1) * kBK), JN_LPTR(fdst + d * 512), 16, 0, 0);
+          if (d < NI)
+            __builtin_amdgcn_global_load_lds(JN_GPTR(src[d] + sf * kBK), JN_LPTR(fdst + d * 512), 16, 0, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
+  wait_lgkmcnt<0>();
+  wait_vmcnt<0>();  // the repeated slab's DMA lands before the LDS is released
 
   gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
 }
