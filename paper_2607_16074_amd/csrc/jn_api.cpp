@@ -1267,9 +1267,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
 
   // ---- recording helpers
   auto gemm = [&](int epi, std::vector<GemmArgs> probs) {
-    int32_t maxm = 0;
-    for (auto& g : probs) maxm = std::max(maxm, g.M);
-    const int shape = gemm_grouped_tile_shape(maxm);
+    const int shape = gemm_grouped_tile_shape(probs.data(), (int32_t)probs.size());
     const int32_t tiles = gemm_grouped_prepare(probs.data(), (int32_t)probs.size(), shape);
     if (tiles < 0) rec.bad_gemm = true;
     const size_t at = rec.add(probs.data(), sizeof(GemmArgs) * probs.size());

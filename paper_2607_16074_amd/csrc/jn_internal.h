@@ -69,7 +69,7 @@ struct GemmArgs {
 // the problems, calls gemm_grouped_prepare (tile ranges, returns the tile
 // total, or -1 if a problem is not M, N, K > 0 with K % 64 == 0 and
 // N % 32 == 0), uploads them and launches.  shape from gemm_grouped_tile_shape.
-int gemm_grouped_tile_shape(int32_t max_m);
+int gemm_grouped_tile_shape(const GemmArgs* probs, int32_t nprob);
 int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape);
 hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
                                int shape);

@@ -421,21 +421,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const uint16_t* bas
 // the 8-wave loop and the first 4-wave versions lost: each conditional branch
 // in the MFMA stream cost 30-50 cycles of issue, and global_load_lds with a
 // 64-bit address computed per instruction cost more than the buffer form.
-// Split-K ranges come from blockIdx.y as in gemm_kernel.
+// Tile pid of problem g; lds holds 5 x 32 KB.
 template <int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
+__device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16_t* __restrict__ lds) {
   constexpr int BN = 256, BM = 256, WGN = 2, WGM = 2;
   constexpr int WN = BN / WGN, WM = BM / WGM;
   constexpr int TN = WN / 16, TM = WM / 16;
   constexpr int NI = 8;            // 1 KB DMA instructions per wave per half-slab
   constexpr int SLOT = 256 * kBK;  // elements per half-slab slot
   constexpr bool GLU = EPI == EPI_GEGLU_BF16;
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * SLOT];
-  const GemmArgs g = split_range(g0);
   const int32_t M = g.M, K = g.K;
 
   int32_t tm, tn;
-  tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+  tile_of(pid, g.tiles_m, g.tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wn = wave / WGM, wm = wave % WGM;
@@ -575,6 +573,25 @@ __global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
   }
 }
 
+// One launch of ring tiles over g (split-K ranges from blockIdx.y as in
+// gemm_kernel).
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * 256 * kBK];
+  ring_tile<EPI>(split_range(g0), blockIdx.x, lds);
+}
+
+// Grouped ring tiles: problem p owns tiles [tile_start, tile_start + tiles).
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_grouped_ring_kernel(const GemmArgs* __restrict__ probs, int32_t nprob) {
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * 256 * kBK];
+  const int32_t b = blockIdx.x;
+  int32_t p = 0;
+  while (p + 1 < nprob && probs[p + 1].tile_start <= b) ++p;
+  const GemmArgs g = probs[p];
+  ring_tile<EPI>(g, b - g.tile_start, lds);
+}
+
 template <int BN, int BM, int WGN, int WGM>
 static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits = 1);
 
@@ -614,6 +631,24 @@ static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits
     JN_GEMM_CASE(EPI_GELU_BF16)
     JN_GEMM_CASE(EPI_RESID_F32)
     JN_GEMM_CASE(EPI_GEGLU_BF16)
+    JN_GEMM_CASE(EPI_F32)
+    JN_GEMM_CASE(EPI_GELU_SAVE)
+    JN_GEMM_CASE(EPI_GELUGRAD_BF16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef JN_GEMM_CASE
+  return hipGetLastError();
+}
+
+static hipError_t launch_grouped_ring(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob,
+                                      int32_t total_tiles) {
+  dim3 grid(total_tiles), block(256);
+#define JN_GEMM_CASE(E) \
+  case E: gemm_grouped_ring_kernel<E><<<grid, block, 0, s>>>(dprobs, nprob); break;
+  switch (epi) {
+    JN_GEMM_CASE(EPI_BF16)
+    JN_GEMM_CASE(EPI_RESID_F32)
     JN_GEMM_CASE(EPI_F32)
     JN_GEMM_CASE(EPI_GELU_SAVE)
     JN_GEMM_CASE(EPI_GELUGRAD_BF16)
@@ -872,10 +907,24 @@ hipError_t launch_gemm(hipStream_t s, int epi, const void* A, int64_t lda, const
   return launch_rows(s, epi, g, t2);
 }
 
-int gemm_grouped_tile_shape(int32_t max_m) { return max_m >= 1024 ? 1 : 2; }
+// Ring tiles (shape 0) once the largest problem has kGroupedRingRows rows and
+// every leading dimension fits their 32-bit panel offsets; then 256x128 and
+// 128x128 interleaved tiles.
+constexpr int32_t kGroupedRingRows = 512;
+
+int gemm_grouped_tile_shape(const GemmArgs* probs, int32_t nprob) {
+  int32_t max_m = 0;
+  bool ring_ok = true;
+  for (int32_t p = 0; p < nprob; ++p) {
+    max_m = std::max(max_m, probs[p].M);
+    if ((int64_t)256 * std::max(probs[p].ldx, probs[p].ldw) * 2 > (int64_t)0x7fffffff) ring_ok = false;
+  }
+  if (ring_ok && max_m >= kGroupedRingRows) return 0;
+  return max_m >= 1024 ? 1 : 2;
+}
 
 int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
-  const int BN = shape == 1 ? 256 : 128, BM = 128;
+  const int BN = shape == 2 ? 128 : 256, BM = shape == 0 ? 256 : 128;
   int32_t total = 0;
   for (int32_t p = 0; p < nprob; ++p) {
     const GemmArgs& g = probs[p];
@@ -891,6 +940,7 @@ int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
 hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
                                int shape) {
   if (nprob <= 0 || total_tiles <= 0) return hipErrorInvalidValue;
+  if (shape == 0) return launch_grouped_ring(s, epi, dprobs, nprob, total_tiles);
   if (shape == 1) return launch_grouped_tile<256, 128, 4, 2>(s, epi, dprobs, nprob, total_tiles);
   return launch_grouped_tile<128, 128, 2, 2>(s, epi, dprobs, nprob, total_tiles);
 }
