@@ -17,7 +17,14 @@ The backbone is frozen: nothing flows back into the shared features.
 ``rnd=True`` rounds to bf16 exactly where the GPU stores a GEMM
 operand in bf16 (forward: every GEMM input activation; backward: every
 incoming gradient before it meets a GEMM), computing everything else in
-fp64.  That is the GPU's precision contract.  It does not make the two
+fp64.  Attention's matrix products take bf16 operands too: q, k and v are
+stored in bf16 by their projections, the probabilities are rounded before
+they meet v (unnormalised, relative to the row maximum; the row sum that
+normalises the output stays unrounded), and in the backward the incoming
+output gradient is rounded before it meets v and the probabilities, the
+recomputed (normalised) probabilities before they meet it, and the score
+gradient before it meets q and k; the row term sum(dO * O) uses the
+unrounded values.  That is the GPU's precision contract.  It does not make the two
 agree to fp32 rounding: a value that lands near a bf16 rounding boundary
 can round the other way on the GPU, which moves it by one bf16 step, and
 the change propagates.  fp32-sized perturbations before every rounding point
@@ -105,13 +112,45 @@ def _gelu(u):
     return 0.5 * u * (1.0 + torch.tanh(c * (u + 0.044715 * u ** 3)))
 
 
-def _attn(q, k, v, heads):
-    """Bidirectional multi-head attention: q [Lq, d], k/v [Lk, d]."""
+class _AttnRnd(torch.autograd.Function):
+    """One head of softmax(q k^T * scale) v with the GPU's bf16 operands of
+    every product (q, k, v already bf16-valued); see the module docstring."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, scale):
+        s = (q @ k.T) * scale
+        m = torch.max(s, dim=-1, keepdim=True).values
+        pu = torch.exp(s - m)
+        lsum = torch.sum(pu, dim=-1, keepdim=True)
+        o = (_round_bf16(pu) @ v) / lsum
+        ctx.save_for_backward(q, k, v, o, m + torch.log(lsum))
+        ctx.scale = scale
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        q, k, v, o, lse = ctx.saved_tensors
+        p = torch.exp((q @ k.T) * ctx.scale - lse)
+        dor = _round_bf16(do)
+        drow = torch.sum(do * o, dim=-1, keepdim=True)
+        ds = p * (dor @ v.T - drow)
+        dv = _round_bf16(p).T @ dor
+        dsr = _round_bf16(ds)
+        return (dsr @ k) * ctx.scale, (dsr.T @ q) * ctx.scale, dv, None
+
+
+def _attn(q, k, v, heads, rnd=False):
+    """Bidirectional multi-head attention: q [Lq, d], k/v [Lk, d]; with rnd the
+    GPU's bf16 operands of the attention products (q, k, v rounded by the
+    caller)."""
     Lq, d = q.shape
     hd = d // heads
     out = []
     for h in range(heads):
         sl = slice(h * hd, (h + 1) * hd)
+        if rnd:
+            out.append(_AttnRnd.apply(q[:, sl], k[:, sl], v[:, sl], 1.0 / np.sqrt(hd)))
+            continue
         s = (q[:, sl] @ k[:, sl].T) / np.sqrt(hd)
         out.append(torch.softmax(s, dim=-1) @ v[:, sl])
     return torch.cat(out, dim=1)
@@ -166,13 +205,13 @@ def expert_forward(P, n_layers: int, heads: int, eps: float, u: Sequence[np.ndar
             g = lambda k: P[f"{l}.{k}"]  # noqa: E731
             d = x.shape[1]
             h = _q(_rms(x, g("g1"), eps), rnd)
-            qkv = linear(h, g("wqkv_s"), rnd)
-            a = _attn(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], heads)
+            qkv = _q(linear(h, g("wqkv_s"), rnd), rnd)
+            a = _attn(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], heads, rnd)
             x = x + linear(_q(a, rnd), g("wo_s"), rnd)
             h = _q(_rms(x, g("g2"), eps), rnd)
-            q = linear(h, g("wq_c"), rnd)
-            kv = linear(zt, g("wkv_c"), rnd)
-            a = _attn(q, kv[:, :d], kv[:, d:], heads)
+            q = _q(linear(h, g("wq_c"), rnd), rnd)
+            kv = _q(linear(zt, g("wkv_c"), rnd), rnd)
+            a = _attn(q, kv[:, :d], kv[:, d:], heads, rnd)
             x = x + linear(_q(a, rnd), g("wo_c"), rnd)
             h = _q(_rms(x, g("g3"), eps), rnd)
             m = _q(_gelu(linear(h, g("w_up"), rnd)), rnd)

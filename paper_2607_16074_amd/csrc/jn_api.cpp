@@ -1035,7 +1035,7 @@ struct ExpPlan {
 // Workspace regions (byte offsets); per-layer saves are arrays of offsets.
 struct ExpLayout {
   size_t arena = 0, arena_bytes = 0;
-  size_t x, xf, yb, ub, vel, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, tq, tb, dkv, dkvb, gx, part,
+  size_t x, xf, yb, ub, vel, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, dsum, tb, dkvb, gx, part,
       TA, TB, WT, dwinp, dwoutp;
   std::vector<size_t> x1, x2, x3, h1, h2, h3, qkv, os, osb, lses, qc, kv, oc, ocb, lsec, pre, mb;
   size_t total = 0;
@@ -1154,9 +1154,8 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.dx = take(4 * Na * d);
   Ly.dxb = take(2 * Na * d);
   Ly.tf = take(4 * Na * d);
-  Ly.tq = take(4 * Na * 3 * d);
+  Ly.dsum = take(4 * Na * H);
   Ly.tb = take(2 * Na * wmax);
-  Ly.dkv = take(4 * Pz * 2 * d);
   Ly.dkvb = take(2 * Pz * 2 * d);
   Ly.gx = take(4 * Na * d);
   Ly.part = take(4 * G * 16 * d);
@@ -1172,12 +1171,12 @@ ExpLayout exp_layout(const ExpPlan& P) {
     Ly.h1.push_back(take(2 * Na * d));
     Ly.h2.push_back(take(2 * Na * d));
     Ly.h3.push_back(take(2 * Na * d));
-    Ly.qkv.push_back(take(4 * Na * 3 * d));
+    Ly.qkv.push_back(take(2 * Na * 3 * d));
     Ly.os.push_back(take(4 * Na * d));
     Ly.osb.push_back(take(2 * Na * d));
     Ly.lses.push_back(take(4 * Na * H));
-    Ly.qc.push_back(take(4 * Na * d));
-    Ly.kv.push_back(take(4 * Pz * 2 * d));
+    Ly.qc.push_back(take(2 * Na * d));
+    Ly.kv.push_back(take(2 * Pz * 2 * d));
     Ly.oc.push_back(take(4 * Na * d));
     Ly.ocb.push_back(take(2 * Na * d));
     Ly.lsec.push_back(take(4 * Na * H));
@@ -1469,13 +1468,14 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     // self-attention block
     rows_copy(F(Ly.x), false, F(Ly.x1[l]), false, P.Na, d);
     rms_fwd(Ly.x1[l], g1, Ly.h1[l]);
-    rows_gemm(EPI_F32, B(Ly.h1[l]), d, Wl(l, &jn_expert_layer::wqkv_s), 3 * d, F(Ly.qkv[l]), 3 * d, true);
+    rows_gemm(EPI_BF16, B(Ly.h1[l]), d, Wl(l, &jn_expert_layer::wqkv_s), 3 * d, B(Ly.qkv[l]), 3 * d, false);
     {
       AttnArgs A{};
-      A.Q = F(Ly.qkv[l]);
-      A.K = F(Ly.qkv[l]);
-      A.V = F(Ly.qkv[l]);
+      A.Q = B(Ly.qkv[l]);
+      A.K = B(Ly.qkv[l]);
+      A.V = B(Ly.qkv[l]);
       A.O = F(Ly.os[l]);
+      A.Ob = B(Ly.osb[l]);
       A.lse = F(Ly.lses[l]);
       A.ldq = 3 * d;
       A.ldkv = 3 * d;
@@ -1489,19 +1489,18 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, false);
     }
-    rows_copy(F(Ly.os[l]), false, B(Ly.osb[l]), true, P.Na, d);
     rows_gemm(EPI_RESID_F32, B(Ly.osb[l]), d, Wl(l, &jn_expert_layer::wo_s), d, F(Ly.x), d, true);
     // cross-attention block
     rows_copy(F(Ly.x), false, F(Ly.x2[l]), false, P.Na, d);
     rms_fwd(Ly.x2[l], g2, Ly.h2[l]);
-    rows_gemm(EPI_F32, B(Ly.h2[l]), d, Wl(l, &jn_expert_layer::wq_c), d, F(Ly.qc[l]), d, true);
-    per_tenant_gemm(EPI_F32, [&](int32_t g) {
+    rows_gemm(EPI_BF16, B(Ly.h2[l]), d, Wl(l, &jn_expert_layer::wq_c), d, B(Ly.qc[l]), d, false);
+    per_tenant_gemm(EPI_BF16, [&](int32_t g) {
       GemmArgs a{};
       a.X = B(Ly.z) + P.zoff[g] * dp;
       a.ldx = dp;
       a.W = (const uint16_t*)ex[g].layers[l].wkv_c;
       a.ldw = dp;
-      a.C = F(Ly.kv[l]) + P.zoff[g] * 2 * d;
+      a.C = B(Ly.kv[l]) + P.zoff[g] * 2 * d;
       a.ldc = 2 * d;
       a.M = (int32_t)P.Pz[g];
       a.N = (int32_t)(2 * d);
@@ -1510,10 +1509,11 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     });
     {
       AttnArgs A{};
-      A.Q = F(Ly.qc[l]);
-      A.K = F(Ly.kv[l]);
-      A.V = F(Ly.kv[l]);
+      A.Q = B(Ly.qc[l]);
+      A.K = B(Ly.kv[l]);
+      A.V = B(Ly.kv[l]);
       A.O = F(Ly.oc[l]);
+      A.Ob = B(Ly.ocb[l]);
       A.lse = F(Ly.lsec[l]);
       A.zoff = (const int32_t*)(w + Ly.zoff);
       A.kv_cap = P.Pzt;
@@ -1529,7 +1529,6 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, false);
     }
-    rows_copy(F(Ly.oc[l]), false, B(Ly.ocb[l]), true, P.Na, d);
     rows_gemm(EPI_RESID_F32, B(Ly.ocb[l]), d, Wl(l, &jn_expert_layer::wo_c), d, F(Ly.x), d, true);
     // MLP block
     rows_copy(F(Ly.x), false, F(Ly.x3[l]), false, P.Na, d);
@@ -1591,15 +1590,16 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
     {
       AttnArgs A{};
-      A.Q = F(Ly.qc[l]);
-      A.K = F(Ly.kv[l]);
-      A.V = F(Ly.kv[l]);
+      A.Q = B(Ly.qc[l]);
+      A.K = B(Ly.kv[l]);
+      A.V = B(Ly.kv[l]);
       A.O = F(Ly.oc[l]);
       A.lse = F(Ly.lsec[l]);
+      A.dsum = F(Ly.dsum);
       A.dO = F(Ly.tf);
-      A.dQ = F(Ly.tq);
-      A.dK = F(Ly.dkv);
-      A.dV = F(Ly.dkv);
+      A.dQ = B(Ly.tb);
+      A.dK = B(Ly.dkvb);
+      A.dV = B(Ly.dkvb);
       A.zoff = (const int32_t*)(w + Ly.zoff);
       A.kv_cap = P.Pzt;
       A.ldq = d;
@@ -1618,8 +1618,6 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, true);
     }
-    rows_copy(F(Ly.tq), false, B(Ly.tb), true, P.Na, d);
-    rows_copy(F(Ly.dkv), false, B(Ly.dkvb), true, P.Pzt, 2 * d);
     trans_rows(B(Ly.tb), d, B(Ly.TA), false);
     trans_rows(B(Ly.h2[l]), d, B(Ly.TB), false);
     wgrad(d, d, Gl(l, &jn_expert_layer_grads::wq_c), false);
@@ -1638,15 +1636,16 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
     {
       AttnArgs A{};
-      A.Q = F(Ly.qkv[l]);
-      A.K = F(Ly.qkv[l]);
-      A.V = F(Ly.qkv[l]);
+      A.Q = B(Ly.qkv[l]);
+      A.K = B(Ly.qkv[l]);
+      A.V = B(Ly.qkv[l]);
       A.O = F(Ly.os[l]);
       A.lse = F(Ly.lses[l]);
+      A.dsum = F(Ly.dsum);
       A.dO = F(Ly.tf);
-      A.dQ = F(Ly.tq);
-      A.dK = F(Ly.tq);
-      A.dV = F(Ly.tq);
+      A.dQ = B(Ly.tb);
+      A.dK = B(Ly.tb);
+      A.dV = B(Ly.tb);
       A.ldq = 3 * d;
       A.ldkv = 3 * d;
       A.ldo = d;
@@ -1663,7 +1662,6 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, true);
     }
-    rows_copy(F(Ly.tq), false, B(Ly.tb), true, P.Na, 3 * d);
     trans_rows(B(Ly.tb), 3 * d, B(Ly.TA), false);
     trans_rows(B(Ly.h1[l]), d, B(Ly.TB), false);
     wgrad(3 * d, d, Gl(l, &jn_expert_layer_grads::wqkv_s), false);

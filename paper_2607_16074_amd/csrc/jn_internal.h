@@ -199,15 +199,17 @@ hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gai
 // kv0 = zoff[k], Lk = zoff[k+1] - zoff[k] (cross, clamped to kv_cap) or the
 // sample's own query rows (self, zoff null).
 struct AttnArgs {
-  const float* Q;
-  const float* K;
-  const float* V;
-  float* O;        // forward output / backward input
-  float* lse;      // forward output / backward input, [rows][nheads]
+  const uint16_t* Q;  // bf16
+  const uint16_t* K;
+  const uint16_t* V;
+  float* O;        // forward output / backward input (fp32)
+  uint16_t* Ob;    // forward output, bf16 copy of O (leading dimension ldo)
+  float* lse;      // forward output / backward input, [rows][nheads], log2 domain
+  float* dsum;     // backward scratch, [rows][nheads]: sum(dO * O) per query
   const float* dO;
-  float* dQ;
-  float* dK;
-  float* dV;
+  uint16_t* dQ;    // bf16 gradients
+  uint16_t* dK;
+  uint16_t* dV;
   const int32_t* zoff;
   int64_t ldq, ldkv, ldo, lddq, lddkv, kv_cap;
   int32_t kcol, vcol, dkcol, dvcol;

@@ -8,9 +8,9 @@
 //   prefix       tenant-ordered copy of every sample's valid backbone rows
 //   rmsnorm      per-tenant-gain RMSNorm forward (fp32 -> bf16) and backward
 //                (fp32), gain gradients by fixed-order column sums
-//   attention    fp32 self- / cross-attention forward and backward on the
-//                fp32 matrix cores, per (sample, head); a sample's queries
-//                never see another sample's keys
+//   attention    self- / cross-attention forward and backward on the bf16
+//                matrix cores, per (sample, head); a sample's queries never
+//                see another sample's keys
 //   loss         per-tenant mean squared error and its gradient
 #include "jn_device.h"
 #include "jn_internal.h"
@@ -382,25 +382,81 @@ hipError_t launch_xrms_bwd(hipStream_t s, const float* x, const void* const* gai
 }
 
 // -------------------------------------------------------------- attention ---
-// fp32 attention on the fp32 matrix cores (v_mfma_f32_32x32x2_f32).  Queries:
-// rows q_row0 + 0..Lq-1 of Q (Lq <= 64, two groups of 32); keys / values: rows
-// kv_row0 .. + Lk - 1 of K / V.  Self attention: the sample's own action rows;
-// cross attention: the sample's rows of the tenant-ordered prefix (zoff), so a
-// query never sees another sample's keys.
+// Self- / cross-attention of the expert on the bf16 matrix cores
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation and softmax statistics).
+// Queries: rows q_row0 + 0..Lq-1 of Q (Lq <= 64: four 16-row blocks, one per
+// wave); keys / values: rows kv_row0 .. + Lk - 1 of K / V.  Self attention:
+// the sample's own action rows; cross attention: the sample's rows of the
+// tenant-ordered prefix (zoff), so a query never sees another sample's keys.
+// Q, K, V are bf16 (their projections store them so); the probabilities are
+// rounded to bf16 before they meet V, and in the backward the incoming output
+// gradient, the recomputed probabilities and the score gradient before they
+// meet their products.  The softmax runs in the log2 domain: lse holds
+// m + log2(l) of the scaled scores.
 //
-// MFMA lane layout (32x32x2): lane l supplies A[l & 31][l >> 5] and
-// B[l >> 5][l & 31]; accumulator r of lane l is C[mrow(r, l)][l & 31].  Scores
-// are computed transposed, S^T = K Q^T, so each lane owns one query column and
-// softmax statistics need one exchange with lane l ^ 32.  In P V the k index of
-// step t pairs key kfor(t, half) with the half's lane, which is exactly the key
-// whose score that lane holds in register t: P never leaves registers.
+// MFMA layouts (16x16x32): A (16 x 32) -- lane l supplies row l & 15,
+// k-slots 8 (l >> 4) .. +7; B (32 x 16) -- column l & 15, the same k-slots;
+// D -- lane l holds rows 4 (l >> 4) .. +3 of column l & 15.  Scores are
+// formed transposed where the lane should own a query (S^T = K Q^T: lane =
+// query, registers = 4 keys of each 16-key block), so a query's row
+// statistics need only exchanges with lanes l ^ 16 and l ^ 32.  Products
+// whose contraction runs over the rows of a row-major LDS tile (V^T P^T,
+// K^T dS^T, dO^T P, Q^T dS) read their A operand with ds_read_b64_tr_b16:
+// lane (g, j) of 16-lane group g addresses row 32 c + 4 g + j / 4 (and +16)
+// at column 16 t + 4 (j % 4) and receives column 16 t + j of rows
+// 32 c + 4 g .. +3 and 32 c + 16 + 4 g .. +3, so k-slot s of lane (g, j)
+// is row 32 c + 4 g + (s & 3) + 16 (s >> 2) -- the order in which the lane
+// already holds the matching B values (register e of blocks 2c and 2c+1).
+// Every LDS tile row is a permutation of its 16-byte chunks (chunk c at
+// c ^ swz(row)) so that both the 16-byte fragment reads and the transposed
+// reads touch each bank once per 256 bytes.
 
-typedef float f32x16v __attribute__((ext_vector_type(16)));
+typedef __bf16 xbf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 xbf16x4 __attribute__((ext_vector_type(4)));
+typedef float xf32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int mrow(int r, int half) { return 8 * (r >> 2) + 4 * half + (r & 3); }
+#define XA_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
+#define XA_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-__device__ __forceinline__ f32x16v mfma32(float a, float b, f32x16v c) {
-  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+template <int HD>
+__device__ __forceinline__ int xa_swz(int r) {
+  if constexpr (HD == 64) {
+    const int x = (r >> 1) & 7;  // 2 rows per 256-byte bank row: bit-reversed row pair
+    return ((x & 1) << 2) | (x & 2) | (x >> 2);
+  } else {
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  }
+}
+
+// 16-byte fragment: logical chunk c (8 elements) of row r of an LDS tile
+template <int HD>
+__device__ __forceinline__ xbf16x8 xa_frag(const uint16_t* t, int r, int c) {
+  return *reinterpret_cast<const xbf16x8*>(t + r * HD + ((c ^ xa_swz<HD>(r)) * 8));
+}
+
+// transposed A operand: rows 32 c + 4 g + {0..3, 16..19} of column 16 t + j
+// (lane (g, j)); swz = xa_swz(4 g + j / 4), shared by those rows
+template <int HD>
+__device__ __forceinline__ xbf16x8 xa_tr(const uint16_t* t, int c, int ct, int quad, int j16, int swz) {
+  const int col = ct * 16 + 4 * (j16 & 3);
+  const int pos = (((col >> 3) ^ swz) * 8) + (col & 7);
+  const int r0 = c * 32 + 4 * quad + (j16 >> 2);
+  const xbf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) xbf16x4*)(t + r0 * HD + pos));
+  const xbf16x4 hi =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) xbf16x4*)(t + (r0 + 16) * HD + pos));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+__device__ __forceinline__ xf32x4 xa_mfma(xbf16x8 a, xbf16x8 b, xf32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 8 fp32 values -> bf16 operand (round to nearest even)
+__device__ __forceinline__ xbf16x8 xa_pack8(const float* v) {
+  xbf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (__bf16)v[e];
+  return r;
 }
 
 __device__ __forceinline__ void attn_rows(const AttnArgs& A, int32_t k, int32_t& q0, int32_t& Lq, int64_t& kv0,
@@ -417,354 +473,317 @@ __device__ __forceinline__ void attn_rows(const AttnArgs& A, int32_t k, int32_t&
   }
 }
 
-// Stage rows j0 .. j0+63 of K and V (head h, zero past Lk) into LDS with row
-// stride SKV floats.  ds_read_b32 serves each half-wave from 32 banks, so an
-// odd stride makes "one row per lane" reads conflict-free; "one column per
-// lane" reads are conflict-free for any stride.
-template <int HD, int SKV>
-__device__ __forceinline__ void attn_stage_kv(const AttnArgs& A, int64_t kv0, int32_t Lk, int32_t j0, int h,
-                                              float* sk, float* sv) {
-  for (int e = threadIdx.x; e < 64 * HD / 4; e += 256) {
-    const int rr = e / (HD / 4), c = 4 * (e % (HD / 4));
-    float4 kq = make_float4(0.f, 0.f, 0.f, 0.f), vq = kq;
-    if (j0 + rr < Lk) {
-      const int64_t row = kv0 + j0 + rr;
-      kq = *reinterpret_cast<const float4*>(A.K + row * A.ldkv + A.kcol + h * HD + c);
-      vq = *reinterpret_cast<const float4*>(A.V + row * A.ldkv + A.vcol + h * HD + c);
-    }
-    float* kd = sk + rr * SKV + c;
-    float* vd = sv + rr * SKV + c;
-    kd[0] = kq.x; kd[1] = kq.y; kd[2] = kq.z; kd[3] = kq.w;
-    vd[0] = vq.x; vd[1] = vq.y; vd[2] = vq.z; vd[3] = vq.w;
-  }
-}
-
-// reg[i] = row[2i + half], i < HD/2, through 16-byte loads
+// K and V tiles of 64 keys ([64][HD] bf16 each, swizzled), double buffered,
+// moved by direct DMA: 1 KB instructions, lane -> (row RPI v + lane / CPR,
+// chunk (lane % CPR) ^ swz(row)); rows past the sample repeat its last row.
 template <int HD>
-__device__ __forceinline__ void attn_row_regs(const float* row, int half, float (&reg)[HD / 2]) {
+struct XaTiles {
+  static constexpr int CPR = HD / 8, RPI = 512 / HD, TILE = 64 * HD, NDMA = 2 * TILE / 512, DPW = NDMA / 4;
+  __device__ __forceinline__ static void issue(uint16_t* stage, const uint16_t* Kb, const uint16_t* Vb, int64_t ld,
+                                               int64_t kv0, int32_t Lk, int32_t j0, int wave, int lane) {
 #pragma unroll
-  for (int j = 0; j < HD / 4; ++j) {
-    const float4 f = *reinterpret_cast<const float4*>(row + 4 * j);
-    reg[2 * j] = half ? f.y : f.x;
-    reg[2 * j + 1] = half ? f.w : f.z;
+    for (int k = 0; k < DPW; ++k) {
+      const int u = wave * DPW + k;
+      const bool isv = u >= NDMA / 2;
+      const int v = isv ? u - NDMA / 2 : u;
+      const int r = v * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ xa_swz<HD>(r);
+      const int64_t key = kv0 + min(j0 + r, Lk - 1);
+      const uint16_t* src = (isv ? Vb : Kb) + key * ld + c * 8;
+      __builtin_amdgcn_global_load_lds(XA_GPTR(src), XA_LPTR(stage + u * 512), 16, 0, 0);
+    }
   }
-}
+};
 
-// Forward: one workgroup per (sample, head); wave w takes query group w & 1
-// and the 32-key blocks of parity w >> 1 of every 64-key tile; the two key
-// halves merge their (max, sum, output) at the end.
+// Forward: one workgroup per (sample, head), wave w = queries 16 w ..;
+// O = softmax(Q K^T scale) V in fp32 (and a bf16 copy), lse per query.
 template <int HD>
-__global__ __launch_bounds__(256) void xattn_fwd_kernel(AttnArgs A) {
-  constexpr int SKV = HD + 1;
-  constexpr int NT = HD / 2, NCB = HD / 32;
-  __shared__ float smem[2 * 64 * SKV];
-  float* sk = smem;
-  float* sv = smem + 64 * SKV;
+__global__ __launch_bounds__(256, 2) void xattn_fwd_kernel(AttnArgs A) {
+  using T = XaTiles<HD>;
+  constexpr int NQC = HD / 32, NOT = HD / 16;
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2 * T::TILE];
   const int k = blockIdx.x, h = blockIdx.y;
   int32_t q0, Lq, Lk;
   int64_t kv0;
   attn_rows(A, k, q0, Lq, kv0, Lk);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = wave & 1, par = wave >> 1, half = lane >> 5, col = lane & 31;
-  const int q = 32 * g + col;
-  const bool qlive = q < Lq, glive = 32 * g < Lq;
-  float qreg[NT];
-  attn_row_regs<HD>(A.Q + (int64_t)(q0 + min(q, Lq - 1)) * A.ldq + h * HD, half, qreg);
-  if (!qlive) {
+  if (Lk <= 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int j16 = lane & 15, quad = lane >> 4;
+  const int qi = wave * 16 + j16;  // this lane's query
+  const int64_t qrow = q0 + min(qi, Lq - 1);
+  const float sl2 = A.scale * 1.4426950408889634f;
+  xbf16x8 qf[NQC];
 #pragma unroll
-    for (int i = 0; i < NT; ++i) qreg[i] = 0.f;
-  }
-  f32x16v o[NCB];
+  for (int c = 0; c < NQC; ++c) qf[c] = *reinterpret_cast<const xbf16x8*>(A.Q + qrow * A.ldq + h * HD + c * 32 + quad * 8);
+  const uint16_t* Kb = A.K + A.kcol + h * HD;
+  const uint16_t* Vb = A.V + A.vcol + h * HD;
+  const int vswz = xa_swz<HD>(4 * quad + (j16 >> 2));
+
+  xf32x4 o[NOT];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[cb][r] = 0.f;
+  for (int t = 0; t < NOT; ++t) o[t] = xf32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
-  for (int32_t j0 = 0; j0 < Lk; j0 += 64) {
-    __syncthreads();
-    attn_stage_kv<HD, SKV>(A, kv0, Lk, j0, h, sk, sv);
-    __syncthreads();
-    const int32_t kb = j0 + 32 * par;
-    if (kb >= Lk || !glive) continue;
-    f32x16v sc;
+  const int32_t ntiles = (Lk + 63) / 64;
+  T::issue(&lds[0][0], Kb, Vb, A.ldkv, kv0, Lk, 0, wave, lane);
+  for (int32_t jt = 0; jt < ntiles; ++jt) {
+    const int32_t j0 = jt * 64;
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();  // tile jt landed; tile jt-1's buffer is free
+    T::issue(&lds[(jt + 1) & 1][0], Kb, Vb, A.ldkv, kv0, Lk, min(j0 + 64, (ntiles - 1) * 64), wave, lane);
+    const uint16_t* Ks = &lds[jt & 1][0];
+    const uint16_t* Vs = Ks + T::TILE;
+    xf32x4 s[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sc[r] = 0.f;
-    const float* kr = sk + (32 * par + col) * SKV + half;
-#pragma unroll 16
-    for (int i = 0; i < NT; ++i) sc = mfma32(kr[2 * i], qreg[i], sc);
+    for (int kb = 0; kb < 4; ++kb) s[kb] = xf32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NQC; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) s[kb] = xa_mfma(xa_frag<HD>(Ks, kb * 16 + j16, 4 * c + quad), qf[c], s[kb]);
+    if (j0 + 64 > Lk) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (j0 + kb * 16 + quad * 4 + e >= Lk) s[kb][e] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      sc[r] = (kb + mrow(r, half) < Lk) ? sc[r] * A.scale : -INFINITY;
-      mx = fmaxf(mx, sc[r]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx);
-    const float alpha = __expf(m - mn);
-    float ps = 0.f;
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      sc[r] = __expf(sc[r] - mn);
-      ps += sc[r];
-    }
-    ps += __shfl_xor(ps, 32, 64);
-    l = l * alpha + ps;
-    m = mn;
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[kb][e]);
+    const float m_new = fmaxf(m, max_xor32(max_xor16(mx)) * sl2);
+    const float alpha = exp2f(m - m_new);
+    l *= alpha;
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
+    for (int t = 0; t < NOT; ++t) o[t] *= alpha;
+    m = m_new;
+    float lsum = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[cb][r] *= alpha;
-      const float* vr = sv + (32 * par) * SKV + 32 * cb + col;
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int t = 0; t < 16; ++t) o[cb] = mfma32(vr[mrow(t, half) * SKV], sc[t], o[cb]);
-    }
-  }
-  // merge the two key halves of each query group
-  constexpr int MS = NCB * 16 + 2;
-  __syncthreads();
-  float* mb = smem + (g * 64 + lane) * MS;
-  if (par == 1) {
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mb[cb * 16 + r] = o[cb][r];
-    mb[NCB * 16] = m;
-    mb[NCB * 16 + 1] = l;
-  }
-  __syncthreads();
-  if (par == 1 || !qlive) return;
-  {
-    const float m1 = mb[NCB * 16], l1 = mb[NCB * 16 + 1];
-    const float mn = fmaxf(m, m1);
-    const float a0 = m == -INFINITY ? 0.f : __expf(m - mn), a1 = m1 == -INFINITY ? 0.f : __expf(m1 - mn);
-    l = l * a0 + l1 * a1;
-    m = mn;
-    const float inv = 1.f / l;
-    float* orow = A.O + (int64_t)(q0 + q) * A.ldo + h * HD;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (o[cb][4 * a4 + e] * a0 + mb[cb * 16 + 4 * a4 + e] * a1) * inv;
-        *reinterpret_cast<float4*>(orow + 32 * cb + 8 * a4 + 4 * half) = make_float4(v[0], v[1], v[2], v[3]);
+      for (int e = 0; e < 4; ++e) {
+        s[kb][e] = exp2f(fmaf(s[kb][e], sl2, -m));
+        lsum += s[kb][e];
       }
-    if (half == 0) A.lse[(int64_t)(q0 + q) * A.nheads + h] = m + __logf(l);
+    l += sum_xor32(sum_xor16(lsum));
+    xbf16x8 pf[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pf[c][e] = (__bf16)s[2 * c][e];
+        pf[c][4 + e] = (__bf16)s[2 * c + 1][e];
+      }
+#pragma unroll
+    for (int t = 0; t < NOT; ++t)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) o[t] = xa_mfma(xa_tr<HD>(Vs, c, t, quad, j16, vswz), pf[c], o[t]);
   }
+  __builtin_amdgcn_s_waitcnt(0);  // the repeated last tile's DMA lands before the LDS is released
+  if (qi >= Lq) return;
+  const float inv = 1.f / l;
+  const int64_t row = q0 + qi;
+  float* orow = A.O + row * A.ldo + h * HD + quad * 4;
+  uint16_t* brow = A.Ob + row * A.ldo + h * HD + quad * 4;
+#pragma unroll
+  for (int t = 0; t < NOT; ++t) {
+    const float v0 = o[t][0] * inv, v1 = o[t][1] * inv, v2 = o[t][2] * inv, v3 = o[t][3] * inv;
+    *reinterpret_cast<float4*>(orow + t * 16) = make_float4(v0, v1, v2, v3);
+    *reinterpret_cast<uint2*>(brow + t * 16) = make_uint2(pack_bf2(v0, v1), pack_bf2(v2, v3));
+  }
+  if (quad == 0) A.lse[row * A.nheads + h] = m + __log2f(l);
 }
 
-// Backward, query side: dQ = scale * dS K with dS = P * (dP - D), P recomputed
-// from the saved log-sum-exp, dP^T = V dO^T, D = rowsum(dO * O).  Same wave
-// roles as the forward; the key halves' partial dQ are summed at the end.
+// Backward, query side: dQ = scale dS K, dS = P (dP - D), P from the saved
+// lse, dP^T = V dO^T, D = sum(dO * O) per query (also written to dsum for
+// the key side).  Same layout as the forward.
 template <int HD>
-__global__ __launch_bounds__(256) void xattn_bwd_dq_kernel(AttnArgs A) {
-  constexpr int SKV = HD + 1;
-  constexpr int NT = HD / 2, NCB = HD / 32;
-  __shared__ float smem[2 * 64 * SKV];
-  float* sk = smem;
-  float* sv = smem + 64 * SKV;
+__global__ __launch_bounds__(256, 2) void xattn_bwd_dq_kernel(AttnArgs A) {
+  using T = XaTiles<HD>;
+  constexpr int NQC = HD / 32, NOT = HD / 16;
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2 * T::TILE];
   const int k = blockIdx.x, h = blockIdx.y;
   int32_t q0, Lq, Lk;
   int64_t kv0;
   attn_rows(A, k, q0, Lq, kv0, Lk);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = wave & 1, par = wave >> 1, half = lane >> 5, col = lane & 31;
-  const int q = 32 * g + col;
-  const bool qlive = q < Lq, glive = 32 * g < Lq;
-  float qreg[NT], dreg[NT];
-  float Dq = 0.f, lse = 0.f;
+  if (Lk <= 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int j16 = lane & 15, quad = lane >> 4;
+  const int qi = wave * 16 + j16;
+  const int64_t qrow = q0 + min(qi, Lq - 1);
+  const float sl2 = A.scale * 1.4426950408889634f;
+  xbf16x8 qf[NQC], df[NQC];
+  float Dq = 0.f;
   {
-    const int64_t row = q0 + min(q, Lq - 1);
-    attn_row_regs<HD>(A.Q + row * A.ldq + h * HD, half, qreg);
-    attn_row_regs<HD>(A.dO + row * A.ldo + h * HD, half, dreg);
-    const float* orr = A.O + row * A.ldo + h * HD;
+    const float* drow = A.dO + qrow * A.ldo + h * HD;
+    const float* orow = A.O + qrow * A.ldo + h * HD;
 #pragma unroll
-    for (int j = 0; j < HD / 4; ++j) {
-      const float4 f = *reinterpret_cast<const float4*>(orr + 4 * j);
-      Dq = fmaf(dreg[2 * j], half ? f.y : f.x, Dq);
-      Dq = fmaf(dreg[2 * j + 1], half ? f.w : f.z, Dq);
+    for (int c = 0; c < NQC; ++c) {
+      qf[c] = *reinterpret_cast<const xbf16x8*>(A.Q + qrow * A.ldq + h * HD + c * 32 + quad * 8);
+      float v[8];
+      const float4 d0 = *reinterpret_cast<const float4*>(drow + c * 32 + quad * 8);
+      const float4 d1 = *reinterpret_cast<const float4*>(drow + c * 32 + quad * 8 + 4);
+      const float4 o0 = *reinterpret_cast<const float4*>(orow + c * 32 + quad * 8);
+      const float4 o1 = *reinterpret_cast<const float4*>(orow + c * 32 + quad * 8 + 4);
+      v[0] = d0.x; v[1] = d0.y; v[2] = d0.z; v[3] = d0.w; v[4] = d1.x; v[5] = d1.y; v[6] = d1.z; v[7] = d1.w;
+      df[c] = xa_pack8(v);
+      Dq = fmaf(d0.x, o0.x, Dq); Dq = fmaf(d0.y, o0.y, Dq); Dq = fmaf(d0.z, o0.z, Dq); Dq = fmaf(d0.w, o0.w, Dq);
+      Dq = fmaf(d1.x, o1.x, Dq); Dq = fmaf(d1.y, o1.y, Dq); Dq = fmaf(d1.z, o1.z, Dq); Dq = fmaf(d1.w, o1.w, Dq);
     }
-    Dq += __shfl_xor(Dq, 32, 64);
-    if (!qlive) {
-      Dq = 0.f;
-#pragma unroll
-      for (int i = 0; i < NT; ++i) qreg[i] = dreg[i] = 0.f;
-    }
-    lse = qlive ? A.lse[row * A.nheads + h] : 0.f;
+    Dq = sum_xor32(sum_xor16(Dq));
   }
-  f32x16v dq[NCB];
+  const float lse = A.lse[qrow * A.nheads + h];
+  if (qi < Lq && quad == 0) A.dsum[(q0 + qi) * A.nheads + h] = Dq;
+  const uint16_t* Kb = A.K + A.kcol + h * HD;
+  const uint16_t* Vb = A.V + A.vcol + h * HD;
+  const int tswz = xa_swz<HD>(4 * quad + (j16 >> 2));
+
+  xf32x4 dq[NOT];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb)
+  for (int t = 0; t < NOT; ++t) dq[t] = xf32x4{0.f, 0.f, 0.f, 0.f};
+  const int32_t ntiles = (Lk + 63) / 64;
+  T::issue(&lds[0][0], Kb, Vb, A.ldkv, kv0, Lk, 0, wave, lane);
+  for (int32_t jt = 0; jt < ntiles; ++jt) {
+    const int32_t j0 = jt * 64;
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    T::issue(&lds[(jt + 1) & 1][0], Kb, Vb, A.ldkv, kv0, Lk, min(j0 + 64, (ntiles - 1) * 64), wave, lane);
+    const uint16_t* Ks = &lds[jt & 1][0];
+    const uint16_t* Vs = Ks + T::TILE;
+    xf32x4 s[4], dp[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dq[cb][r] = 0.f;
-  for (int32_t j0 = 0; j0 < Lk; j0 += 64) {
-    __syncthreads();
-    attn_stage_kv<HD, SKV>(A, kv0, Lk, j0, h, sk, sv);
-    __syncthreads();
-    const int32_t kb = j0 + 32 * par;
-    if (kb >= Lk || !glive) continue;
-    f32x16v sc, dp;
+    for (int kb = 0; kb < 4; ++kb) s[kb] = dp[kb] = xf32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
-    const float* kr = sk + (32 * par + col) * SKV + half;
-    const float* vr = sv + (32 * par + col) * SKV + half;
-#pragma unroll 16
-    for (int i = 0; i < NT; ++i) {
-      sc = mfma32(kr[2 * i], qreg[i], sc);
-      dp = mfma32(vr[2 * i], dreg[i], dp);
-    }
+    for (int c = 0; c < NQC; ++c)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const bool ok = qlive && kb + mrow(r, half) < Lk;
-      const float p = ok ? __expf(sc[r] * A.scale - lse) : 0.f;
-      sc[r] = p * (dp[r] - Dq);  // dS
-    }
+      for (int kb = 0; kb < 4; ++kb) {
+        s[kb] = xa_mfma(xa_frag<HD>(Ks, kb * 16 + j16, 4 * c + quad), qf[c], s[kb]);
+        dp[kb] = xa_mfma(xa_frag<HD>(Vs, kb * 16 + j16, 4 * c + quad), df[c], dp[kb]);
+      }
+    xbf16x8 dsf[2];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      const float* kc = sk + (32 * par) * SKV + 32 * cb + col;
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int t = 0; t < 16; ++t) dq[cb] = mfma32(kc[mrow(t, half) * SKV], sc[t], dq[cb]);
-    }
+      for (int e = 0; e < 4; ++e) {
+        const bool live = j0 + kb * 16 + quad * 4 + e < Lk;
+        const float pv = live ? exp2f(fmaf(s[kb][e], sl2, -lse)) : 0.f;
+        dsf[kb >> 1][(kb & 1) * 4 + e] = (__bf16)(pv * (dp[kb][e] - Dq));
+      }
+#pragma unroll
+    for (int t = 0; t < NOT; ++t)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) dq[t] = xa_mfma(xa_tr<HD>(Ks, c, t, quad, j16, tswz), dsf[c], dq[t]);
   }
-  constexpr int MS = NCB * 16;
-  __syncthreads();
-  float* mb = smem + (g * 64 + lane) * MS;
-  if (par == 1) {
+  __builtin_amdgcn_s_waitcnt(0);
+  if (qi >= Lq) return;
+  uint16_t* out = A.dQ + (q0 + qi) * A.lddq + h * HD + quad * 4;
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mb[cb * 16 + r] = dq[cb][r];
-  }
-  __syncthreads();
-  if (par == 1 || !qlive) return;
-  float* qrow = A.dQ + (int64_t)(q0 + q) * A.lddq + h * HD;
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-    for (int a4 = 0; a4 < 4; ++a4) {
-      float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (dq[cb][4 * a4 + e] + mb[cb * 16 + 4 * a4 + e]) * A.scale;
-      *reinterpret_cast<float4*>(qrow + 32 * cb + 8 * a4 + 4 * half) = make_float4(v[0], v[1], v[2], v[3]);
-    }
+  for (int t = 0; t < NOT; ++t)
+    *reinterpret_cast<uint2*>(out + t * 16) = make_uint2(pack_bf2(dq[t][0] * A.scale, dq[t][1] * A.scale),
+                                                         pack_bf2(dq[t][2] * A.scale, dq[t][3] * A.scale));
 }
 
-// Backward, key side: one wave per 32-key block (grid z covers the longest
-// sample).  Scores are computed untransposed here, S = Q K^T (lane = key,
-// registers = queries), so P and dS are already the B operands of
-// dV^T = dO^T P and dK^T = Q^T dS with the query index permuted as in the
-// forward: nothing is transposed through memory.
+// Backward, key side: one workgroup per (sample, head, 64-key tile), wave w =
+// keys 16 w ..; the sample's queries (<= 64, zero rows past Lq) and its
+// bf16-rounded output gradients sit in LDS.  Scores untransposed, S = Q K^T
+// (lane = key, registers = 4 queries of each 16-query block), so P and dS
+// are already the B operands of dV^T = dO^T P and dK^T = Q^T dS.
 template <int HD>
-__global__ __launch_bounds__(256, 1) void xattn_bwd_dkv_kernel(AttnArgs A) {
-  constexpr int SQ = HD + 1;
-  constexpr int NT = HD / 2, NCB = HD / 32;
-  __shared__ float sq[64 * SQ], sdo[64 * SQ];
-  __shared__ float sD[64], sL[64];
+__global__ __launch_bounds__(256, 2) void xattn_bwd_dkv_kernel(AttnArgs A) {
+  constexpr int NQC = HD / 32, NOT = HD / 16, CPR = HD / 8;
+  __shared__ __attribute__((aligned(1024))) uint16_t qt[64 * HD];
+  __shared__ __attribute__((aligned(1024))) uint16_t dt[64 * HD];
+  __shared__ float lse_s[64], d_s[64];
   const int k = blockIdx.x, h = blockIdx.y;
   int32_t q0, Lq, Lk;
   int64_t kv0;
   attn_rows(A, k, q0, Lq, kv0, Lk);
-  if ((int32_t)blockIdx.z * 128 >= Lk) return;  // uniform over the workgroup
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = lane >> 5, col = lane & 31;
-  for (int e = threadIdx.x; e < 64 * HD / 4; e += 256) {
-    const int rr = e / (HD / 4), c = 4 * (e % (HD / 4));
-    float4 qq = make_float4(0.f, 0.f, 0.f, 0.f), dd = qq;
-    if (rr < Lq) {
-      qq = *reinterpret_cast<const float4*>(A.Q + (int64_t)(q0 + rr) * A.ldq + h * HD + c);
-      dd = *reinterpret_cast<const float4*>(A.dO + (int64_t)(q0 + rr) * A.ldo + h * HD + c);
+  const int32_t j0 = blockIdx.z * 64;
+  if (j0 >= Lk) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j16 = lane & 15, quad = lane >> 4;
+  const float sl2 = A.scale * 1.4426950408889634f;
+  // stage Q and bf16(dO): 64 rows x CPR chunks of 8 elements
+  for (int e = tid; e < 64 * CPR; e += 256) {
+    const int r = e / CPR, c = e % CPR;
+    const int pos = r * HD + ((c ^ xa_swz<HD>(r)) * 8);
+    uint4 qv = make_uint4(0, 0, 0, 0), dv = make_uint4(0, 0, 0, 0);
+    if (r < Lq) {
+      const int64_t row = q0 + r;
+      qv = *reinterpret_cast<const uint4*>(A.Q + row * A.ldq + h * HD + c * 8);
+      const float4 a = *reinterpret_cast<const float4*>(A.dO + row * A.ldo + h * HD + c * 8);
+      const float4 b = *reinterpret_cast<const float4*>(A.dO + row * A.ldo + h * HD + c * 8 + 4);
+      dv = make_uint4(pack_bf2(a.x, a.y), pack_bf2(a.z, a.w), pack_bf2(b.x, b.y), pack_bf2(b.z, b.w));
     }
-    float* qd = sq + rr * SQ + c;
-    float* dd2 = sdo + rr * SQ + c;
-    qd[0] = qq.x; qd[1] = qq.y; qd[2] = qq.z; qd[3] = qq.w;
-    dd2[0] = dd.x; dd2[1] = dd.y; dd2[2] = dd.z; dd2[3] = dd.w;
+    *reinterpret_cast<uint4*>(qt + pos) = qv;
+    *reinterpret_cast<uint4*>(dt + pos) = dv;
   }
-  {
-    // D[q] = sum_c dO[q][c] O[q][c]: 4 threads per query, 16-byte loads
-    const int qq = threadIdx.x >> 2, part = threadIdx.x & 3;
-    float acc = 0.f;
-    if (qq < Lq) {
-      const float* orow = A.O + (int64_t)(q0 + qq) * A.ldo + h * HD;
-      const float* drow = A.dO + (int64_t)(q0 + qq) * A.ldo + h * HD;
-      for (int c = 4 * part; c < HD; c += 16) {
-        const float4 o4 = *reinterpret_cast<const float4*>(orow + c);
-        const float4 d4 = *reinterpret_cast<const float4*>(drow + c);
-        acc = fmaf(o4.x, d4.x, fmaf(o4.y, d4.y, fmaf(o4.z, d4.z, fmaf(o4.w, d4.w, acc))));
-      }
-    }
-    acc += __shfl_xor(acc, 1, 64);
-    acc += __shfl_xor(acc, 2, 64);
-    if (part == 0) {
-      sD[qq] = acc;
-      sL[qq] = qq < Lq ? A.lse[(int64_t)(q0 + qq) * A.nheads + h] : 0.f;
-    }
+  if (tid < 64) {
+    const bool live = tid < Lq;
+    lse_s[tid] = live ? A.lse[(q0 + tid) * A.nheads + h] : INFINITY;  // P = 0 past Lq
+    d_s[tid] = live ? A.dsum[(q0 + tid) * A.nheads + h] : 0.f;
   }
   __syncthreads();
-  const int32_t kb = (int32_t)blockIdx.z * 128 + 32 * wave;
-  if (kb >= Lk) return;  // no barrier follows
-  const bool kvalid = kb + col < Lk;  // this lane's key
-  float kreg[NT], vreg[NT];
-  {
-    const int64_t row = kv0 + min(kb + col, Lk - 1);
-    attn_row_regs<HD>(A.K + row * A.ldkv + A.kcol + h * HD, half, kreg);
-    attn_row_regs<HD>(A.V + row * A.ldkv + A.vcol + h * HD, half, vreg);
+
+  const int32_t key = j0 + wave * 16 + j16;  // this lane's key
+  const int64_t krow = kv0 + min(key, Lk - 1);
+  xbf16x8 kf[NQC], vf[NQC];
+#pragma unroll
+  for (int c = 0; c < NQC; ++c) {
+    kf[c] = *reinterpret_cast<const xbf16x8*>(A.K + krow * A.ldkv + A.kcol + h * HD + c * 32 + quad * 8);
+    vf[c] = *reinterpret_cast<const xbf16x8*>(A.V + krow * A.ldkv + A.vcol + h * HD + c * 32 + quad * 8);
   }
-  f32x16v dk[NCB], dv[NCB];
+  // S[q][key] and dP[q][key] for the four 16-query blocks
+  xf32x4 s[4], dp[4];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb)
+  for (int qb = 0; qb < 4; ++qb) s[qb] = dp[qb] = xf32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dk[cb][r] = dv[cb][r] = 0.f;
-  for (int g = 0; 32 * g < Lq; ++g) {
-    f32x16v sc, dp;
+  for (int c = 0; c < NQC; ++c)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sc[r] = dp[r] = 0.f;
-    const float* qa = sq + (32 * g + col) * SQ + half;
-    const float* da = sdo + (32 * g + col) * SQ + half;
-#pragma unroll 16
-    for (int i = 0; i < NT; ++i) {
-      sc = mfma32(qa[2 * i], kreg[i], sc);  // S[query 32g + mrow(r)][key kb + col]
-      dp = mfma32(da[2 * i], vreg[i], dp);
+    for (int qb = 0; qb < 4; ++qb) {
+      s[qb] = xa_mfma(xa_frag<HD>(qt, qb * 16 + j16, 4 * c + quad), kf[c], s[qb]);
+      dp[qb] = xa_mfma(xa_frag<HD>(dt, qb * 16 + j16, 4 * c + quad), vf[c], dp[qb]);
     }
+  // P and dS as B operands: k-slot s of chunk c is query 32 c + 4 quad + (s & 3) + 16 (s >> 2)
+  xbf16x8 pb[2], db[2];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int qq = 32 * g + mrow(r, half);
-      const bool ok = kvalid && qq < Lq;
-      const float p = ok ? __expf(sc[r] * A.scale - sL[qq]) : 0.f;
-      dp[r] = p * (dp[r] - sD[qq]);  // dS
-      sc[r] = p;
+  for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int q = qb * 16 + quad * 4 + e;
+      const float pv = exp2f(fmaf(s[qb][e], sl2, -lse_s[q]));
+      pb[qb >> 1][(qb & 1) * 4 + e] = (__bf16)pv;
+      db[qb >> 1][(qb & 1) * 4 + e] = (__bf16)(pv * (dp[qb][e] - d_s[q]));
     }
+  const int tswz = xa_swz<HD>(4 * quad + (j16 >> 2));
+  xf32x4 dv[NOT], dk[NOT];
 #pragma unroll
-    for (int t = 0; t < 16; ++t) {
-      const int qr = 32 * g + mrow(t, half);
+  for (int t = 0; t < NOT; ++t) {
+    dv[t] = dk[t] = xf32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        dv[cb] = mfma32(sdo[qr * SQ + 32 * cb + col], sc[t], dv[cb]);
-        dk[cb] = mfma32(sq[qr * SQ + 32 * cb + col], dp[t], dk[cb]);
-      }
+    for (int c = 0; c < 2; ++c) {
+      dv[t] = xa_mfma(xa_tr<HD>(dt, c, t, quad, j16, tswz), pb[c], dv[t]);
+      dk[t] = xa_mfma(xa_tr<HD>(qt, c, t, quad, j16, tswz), db[c], dk[t]);
     }
   }
-  // dV^T / dK^T accumulators: lane = key kb + col, register r = column 32cb + mrow(r, half)
-  if (!kvalid) return;
-  const int64_t row = kv0 + kb + col;
-  float* dvr = A.dV + row * A.lddkv + A.dvcol + h * HD;
-  float* dkr = A.dK + row * A.lddkv + A.dkcol + h * HD;
+  if (key >= Lk) return;
+  // lane holds dV^T / dK^T rows (head dims) 16 t + 4 quad .. +3 of its key
+  uint16_t* vrow = A.dV + (kv0 + key) * A.lddkv + A.dvcol + h * HD + quad * 4;
+  uint16_t* krw = A.dK + (kv0 + key) * A.lddkv + A.dkcol + h * HD + quad * 4;
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-    for (int a4 = 0; a4 < 4; ++a4) {
-      const int c = 32 * cb + 8 * a4 + 4 * half;
-      *reinterpret_cast<float4*>(dvr + c) =
-          make_float4(dv[cb][4 * a4], dv[cb][4 * a4 + 1], dv[cb][4 * a4 + 2], dv[cb][4 * a4 + 3]);
-      *reinterpret_cast<float4*>(dkr + c) =
-          make_float4(dk[cb][4 * a4] * A.scale, dk[cb][4 * a4 + 1] * A.scale, dk[cb][4 * a4 + 2] * A.scale,
-                      dk[cb][4 * a4 + 3] * A.scale);
-    }
+  for (int t = 0; t < NOT; ++t) {
+    *reinterpret_cast<uint2*>(vrow + t * 16) = make_uint2(pack_bf2(dv[t][0], dv[t][1]), pack_bf2(dv[t][2], dv[t][3]));
+    *reinterpret_cast<uint2*>(krw + t * 16) =
+        make_uint2(pack_bf2(dk[t][0] * A.scale, dk[t][1] * A.scale), pack_bf2(dk[t][2] * A.scale, dk[t][3] * A.scale));
+  }
 }
 
 hipError_t launch_xattn(hipStream_t s, const AttnArgs& A, int32_t nsamples, bool backward) {
   if (A.Lq > 64 || A.Lq < 1 || A.max_lk < 1) return hipErrorInvalidValue;
-  const dim3 grid(nsamples, A.nheads), gk(nsamples, A.nheads, (A.max_lk + 127) / 128);
+  const dim3 grid(nsamples, A.nheads), gk(nsamples, A.nheads, (A.max_lk + 63) / 64);
   switch (A.hd) {
     case 64:
       if (backward) {

@@ -51,4 +51,4 @@ def pytest_terminal_summary(terminalreporter, exitstatus, config):
     tr = terminalreporter
     tr.write_line("worst measured errors (test | quantity | value / bar):")
     for name, what, value, bar in store:
-        tr.write_line(f"  {name} | {what} | {value:.2e} / {bar:.0e}")
+        tr.write_line(f"  {name} | {what} | {value:.2e} / {bar:.2g}")

@@ -1,7 +1,7 @@
 """GPU parity of the action-expert tenant stage against the fp64 oracle.
 
-The oracle runs with the GPU's rounding points (bf16 GEMM operands, see
-``oracle.expert``) and takes the GPU's backbone rows as each sample's
+The oracle runs with the GPU's rounding points (bf16 operands of every
+GEMM and of the attention products, see ``oracle.expert``) and takes the GPU's backbone rows as each sample's
 prefix, so the expert stage is checked on its own (stage-wise).  Bars: loss
 within 1e-3 relative; predictions and every weight / gain gradient within
 1e-2 relative L2 per tensor (a gradient whose norm is below 1e-4 of the
@@ -13,9 +13,10 @@ a value that lands on the other side of a bf16 rounding boundary changes by
 2^-8 and the change propagates; ``test_oracle_expert`` pins that floor.  The GPU is also compared with the plain fp64 definition (``rnd=False``,
 no rounding anywhere): its distance to it is at most the distance between
 the two oracle modes (pinned at the config-4 expert shapes in
-``test_oracle_expert``: <= 5e-3 for predictions, loss and every gradient)
-plus its distance to the rounding mode (the 5e-3 floor above), so the bar is
-twice that sum, 2e-2 relative, for every compared quantity.  Grouped
+``test_oracle_expert``: 5.4e-3 at most for predictions, loss and every
+gradient, pinned below 7e-3) plus its distance to the rounding mode (the 5e-3
+floor above), so the bar is twice that sum, 2.4e-2 relative, for every
+compared quantity.  Grouped
 execution must equal isolated per-tenant execution bitwise: every output
 element is reduced in an order that does not depend on which other tenants
 share the batch.
@@ -35,7 +36,7 @@ pytestmark = pytest.mark.gpu
 
 LOSS_TOL = 1e-3     # relative
 TOL = 1e-2          # predictions and gradients, relative L2 (twice the worst rounding-noise floor)
-EXACT_TOL = 2e-2    # against the plain fp64 definition: twice (mode distance + noise floor)
+EXACT_TOL = 2.4e-2  # against the plain fp64 definition: twice (mode distance 7e-3 + noise floor 5e-3)
 
 
 def _say(msg):

@@ -98,6 +98,38 @@ def test_expert_rounding_mode_is_close_to_fp64():
     assert abs(a["loss"] - b["loss"]) < 1e-2 * a["loss"]
 
 
+def test_attention_rounding_points_reduce_to_softmax_attention():
+    """The bf16-operand attention of the rounding mode (its own backward:
+    dV = P^T dO, dS = P * (dO V^T - rowsum(dO * O)), dQ = dS K s, dK = dS^T Q s)
+    is the plain softmax attention once rounding is the identity: forward and
+    every input gradient match torch autograd of softmax(q k^T s) v to fp64
+    rounding.  A dropped term, a wrong scale or a transposed product in the
+    hand-written backward fails this."""
+    rng = np.random.default_rng(11)
+    q0, k0, v0 = (torch.tensor(rng.normal(size=sh)) for sh in ((7, 48), (13, 48), (13, 48)))
+    gout = torch.tensor(rng.normal(size=(7, 48)))
+    orig = ex._round_bf16
+    try:
+        ex._round_bf16 = lambda t: t
+        q, k, v = (x.clone().requires_grad_(True) for x in (q0, k0, v0))
+        a = ex._attn(q, k, v, 3, rnd=True)
+        (a * gout).sum().backward()
+    finally:
+        ex._round_bf16 = orig
+    q2, k2, v2 = (x.clone().requires_grad_(True) for x in (q0, k0, v0))
+    b = torch.cat([torch.softmax(q2[:, h * 16:(h + 1) * 16] @ k2[:, h * 16:(h + 1) * 16].T / 4.0, dim=-1)
+                   @ v2[:, h * 16:(h + 1) * 16] for h in range(3)], dim=1)
+    (b * gout).sum().backward()
+    assert torch.allclose(a, b, rtol=1e-12, atol=1e-13)
+    for x, y in ((q, q2), (k, k2), (v, v2)):
+        assert torch.allclose(x.grad, y.grad, rtol=1e-10, atol=1e-12)
+    # with real rounding the result moves, by about the bf16 step
+    qr, kr, vr = (ex._round_bf16(x) for x in (q0, k0, v0))
+    c = ex._attn(qr, kr, vr, 3, rnd=True)
+    rel = float(torch.linalg.norm(c - b.detach()) / torch.linalg.norm(b.detach()))
+    assert 1e-4 < rel < 2e-2, rel
+
+
 def test_bf16_rounding_noise_floor():
     """The parity bar of the GPU expert rests on this: with bf16 rounding
     points, fp32-sized perturbations (relative 2^-22) before each rounding
@@ -134,8 +166,10 @@ def test_rounding_mode_distance_at_config4_shapes(cfg):
     derived from this distance: at the real expert shapes (6 layers, d 1024,
     8 heads, ffn 4096, chunk 50, 768-wide prefixes of ~830 rows; the plain
     regression of config 4 and the flow-matching objective of preset 8) the
-    bf16-faithful mode and the plain fp64 mode differ by 1e-3 .. 5e-3
-    relative in predictions, loss and every gradient.  Two samples of the
+    bf16-faithful mode and the plain fp64 mode differ by 1e-3 .. 7e-3
+    relative in predictions, loss and every gradient (measured: 5.4e-3 and
+    4.3e-3 with the attention products on bf16 operands; 4.6e-3 and 4.3e-3
+    with bf16 GEMM operands only).  Two samples of the
     tenant with the fewest samples; the tenant's own embedding rows (N(0,1),
     the scale of the final-normed backbone rows) stand in for its prefix."""
     import dataclasses
@@ -155,4 +189,4 @@ def test_rounding_mode_distance_at_config4_shapes(cfg):
     for k in b["grads"]:
         dist[k] = np.linalg.norm(a["grads"][k] - b["grads"][k]) / max(np.linalg.norm(b["grads"][k]), floor)
     worst = max(dist.values())
-    assert 1e-3 < worst < 5e-3, worst
+    assert 1e-3 < worst < 7e-3, worst
