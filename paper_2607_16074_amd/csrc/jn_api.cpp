@@ -58,7 +58,8 @@ void* scratch_address(int dev) {
 // --------------------------------------------------------------- context ---
 
 namespace {
-constexpr int kSlots = 8;
+constexpr int kSlots = 8;      // staging slots at context creation
+constexpr int kMaxSlots = 64;  // the ring grows to this many before the host waits
 struct StageSlot {
   void* host = nullptr;
   size_t cap = 0;
@@ -78,7 +79,7 @@ struct jn_ctx {
   hipStream_t stream = nullptr;
   int device = 0;
   std::string err;
-  StageSlot slots[kSlots];
+  std::vector<StageSlot> slots = std::vector<StageSlot>(kSlots);
   int next = 0;
   // launch trace (measurement only): a pair of timing events around every
   // kernel launch while enabled
@@ -149,11 +150,20 @@ hipError_t traced(jn_ctx* c, int32_t op, int64_t M, int64_t N, int64_t K, F&& la
 
 // Stage `bytes` of host data in pinned memory and copy it to `dst` on the
 // context stream.  Slots are reused round-robin; a slot is rewritten only
-// after the copy that last read it has completed.
+// after the copy that last read it has completed.  When the next slot's copy
+// is still in flight the ring grows by a slot instead (up to kMaxSlots), so
+// the host does not wait on the device while the device runs behind by fewer
+// than kMaxSlots uploads.
 jn_status stage_copy(jn_ctx* c, void* dst, const void* src, size_t bytes) {
   if (bytes == 0) return JN_OK;
+  if (c->slots[c->next].pending && hipEventQuery(c->slots[c->next].ev) == hipErrorNotReady &&
+      c->slots.size() < (size_t)kMaxSlots) {
+    StageSlot fresh;
+    JN_HIP(c, hipEventCreateWithFlags(&fresh.ev, hipEventDisableTiming), "hipEventCreate(staging)");
+    c->slots.insert(c->slots.begin() + c->next, fresh);
+  }
   StageSlot& s = c->slots[c->next];
-  c->next = (c->next + 1) % kSlots;
+  c->next = (c->next + 1) % (int)c->slots.size();
   if (s.pending) {
     JN_HIP(c, hipEventSynchronize(s.ev), "hipEventSynchronize(staging)");
     s.pending = false;

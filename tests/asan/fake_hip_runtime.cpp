@@ -83,6 +83,13 @@ hipError_t hipEventDestroy(hipEvent_t e) {
 }
 hipError_t hipEventRecord(hipEvent_t e, hipStream_t) { return e ? hipSuccess : hipErrorInvalidValue; }
 hipError_t hipEventSynchronize(hipEvent_t e) { return e ? hipSuccess : hipErrorInvalidValue; }
+// every other query reports the work as still in flight, so callers' "not
+// ready" paths (the staging ring growing) run under the sanitizer too
+hipError_t hipEventQuery(hipEvent_t e) {
+  static unsigned calls = 0;
+  if (!e) return hipErrorInvalidValue;
+  return (++calls & 1) ? hipErrorNotReady : hipSuccess;
+}
 hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b) {
   if (!a || !b) return hipErrorInvalidValue;
   *ms = 0.f;

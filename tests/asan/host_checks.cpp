@@ -114,8 +114,11 @@ Packed pack(jn_ctx* c, Group& g) {
   CHECK(jn_pack_plan(g.req.data(), (int)g.req.size(), g.ten.data(), (int)g.ten.size(), &g.opts, &k.sz) == JN_OK);
   k.maps = dev(k.sz.map_bytes);
   k.tokens = dev(k.sz.token_bytes);
-  CHECK(jn_pack_group(c, g.req.data(), (int)g.req.size(), g.ten.data(), (int)g.ten.size(), &g.opts, k.maps,
-                      k.sz.map_bytes, k.tokens, k.sz.token_bytes, &k.p) == JN_OK);
+  // repeated uploads: the staging ring grows while copies are reported in
+  // flight, then reuses its slots
+  for (int rep = 0; rep < 100; ++rep)
+    CHECK(jn_pack_group(c, g.req.data(), (int)g.req.size(), g.ten.data(), (int)g.ten.size(), &g.opts, k.maps,
+                        k.sz.map_bytes, k.tokens, k.sz.token_bytes, &k.p) == JN_OK);
   // undersized buffers are refused
   jn_packed tmp{};
   CHECK(jn_pack_group(c, g.req.data(), (int)g.req.size(), g.ten.data(), (int)g.ten.size(), &g.opts, k.maps,
