@@ -696,7 +696,7 @@ struct HeadPlan {
   std::vector<int64_t> width;      // per layer index k: max output width
   size_t P = 0, Z0 = 0, total = 0; // offsets
   std::vector<size_t> Z, H, dZ;    // per k
-  size_t descs = 0, tiles = 0;
+  size_t descs = 0, tiles = 0, part = 0, lpart = 0;
   std::vector<HeadGemm> dv;
   std::vector<HeadTile> tv;
   std::vector<LossDesc> lv;
@@ -726,6 +726,8 @@ jn_status check_heads(jn_ctx* c, const jn_packed* p, const jn_head* heads, int32
 }
 
 // Workspace layout: pooled P [N][d] | per layer k: Z_k, H_k, dZ_k [N][width_k] |
+// split-K partial sums (the largest ksplit x N x width of any split launch) |
+// per-tenant loss partial sums (16 G floats) |
 // loss descriptors | gemm descriptors | tiles.  Tenant g's rows of every
 // [N][*] buffer are its tenant-order rows [off_g, off_g + n_g).
 void head_layout(const jn_packed* p, const jn_head* heads, int32_t G, HeadPlan* hp, bool with_descs) {
@@ -753,19 +755,25 @@ void head_layout(const jn_packed* p, const jn_head* heads, int32_t G, HeadPlan* 
   if (!with_descs) {
     // descriptor counts are bounded by G * 2 * maxL; tiles computed exactly below
   }
-  // tile counts: fwd M-dynamic (ceil(N/64) upper bound), bwd wgrad + dgrad
+  // tile counts: fwd M-dynamic (ceil(N/32) upper bound), bwd wgrad + dgrad;
+  // a split descriptor has ksplit tiles per output tile plus one reduce tile
   const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
-  int64_t ntiles = 0, ndesc = 0;
+  int64_t ntiles = 0, ndesc = 0, part_elems = 0;
   for (int32_t g = 0; g < G; ++g) {
     const jn_head& Hh = heads[g];
     for (int k = 0; k < Hh.n_layers; ++k) {
       int64_t in = Hh.dims[k], out = Hh.dims[k + 1];
-      ntiles += tm_dyn * ((out + kHTN - 1) / kHTN);                        // fwd
-      ntiles += ((out + kHTM - 1) / kHTM) * ((in + kHTN - 1) / kHTN);       // wgrad
-      if (k > 0) ntiles += tm_dyn * ((in + kHTN - 1) / kHTN);               // dgrad
+      const int64_t sf = head_ksplit(in), sd = head_ksplit(out);
+      ntiles += tm_dyn * ((out + kHTN - 1) / kHTN) * (sf + (sf > 1));           // fwd
+      ntiles += ((out + kHTM - 1) / kHTM) * ((in + kHTN - 1) / kHTN);           // wgrad
+      if (k > 0) ntiles += tm_dyn * ((in + kHTN - 1) / kHTN) * (sd + (sd > 1)); // dgrad
       ndesc += (k > 0) ? 3 : 2;
+      if (sf > 1) part_elems = std::max(part_elems, sf * N * hp->width[k]);
+      if (k > 0 && sd > 1) part_elems = std::max(part_elems, sd * N * hp->width[k - 1]);
     }
   }
+  hp->part = take(4 * part_elems);
+  hp->lpart = take(4 * 16 * G);
   hp->losses = take(sizeof(LossDesc) * G);
   hp->descs = take(sizeof(HeadGemm) * ndesc);
   hp->tiles = take(sizeof(HeadTile) * ntiles);
@@ -820,7 +828,25 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
 
   std::vector<HeadGemm> descs;
   std::vector<HeadTile> tiles;
-  std::vector<std::pair<int32_t, int32_t>> fwd_rng, bwd_rng;
+  std::vector<std::pair<int32_t, int32_t>> fwd_rng, bwd_rng, fwd_red, bwd_red;
+  // a descriptor whose K is long enough is split into K ranges whose sums go
+  // to the partial area (plane = the [N][width] extent of its C buffer)
+  float* const part = (float*)(w + hp.part);
+  auto split_desc = [&](HeadGemm& D, int64_t plane) {
+    D.ksplit = head_ksplit(D.K);
+    if (D.ksplit > 1) {
+      D.part = part;
+      D.part_plane = plane;
+    }
+  };
+  // reduce tiles of the split descriptors among tiles [t0, end): appended
+  // after them, returned as a range
+  auto reduce_tiles = [&](int32_t t0) {
+    const int32_t t1 = (int32_t)tiles.size();
+    for (int32_t t = t0; t < t1; ++t)
+      if (descs[tiles[t].desc].ksplit > 1 && tiles[t].tk == 0) tiles.push_back(HeadTile{tiles[t].desc, tiles[t].tm, tiles[t].tn, 0});
+    return std::make_pair(t1, (int32_t)tiles.size() - t1);
+  };
   // forward, one launch per layer index
   for (int k = 0; k < hp.maxL; ++k) {
     int32_t t0 = (int32_t)tiles.size();
@@ -849,12 +875,15 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
       D.K = (int32_t)in;
       D.tenant = g;
       D.tiles_n = (int32_t)((out + kHTN - 1) / kHTN);
+      split_desc(D, N * hp.width[k]);
       int32_t di = (int32_t)descs.size();
       descs.push_back(D);
-      for (int32_t tm = 0; tm < tm_dyn; ++tm)
-        for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
+      for (int32_t tk = 0; tk < D.ksplit; ++tk)
+        for (int32_t tm = 0; tm < tm_dyn; ++tm)
+          for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, tk});
     }
     fwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+    fwd_red.push_back(reduce_tiles(t0));
   }
   // loss: y = Z_{L-1} rows, dY -> dZ_{L-1}
   std::vector<LossDesc> losses(G);
@@ -917,13 +946,16 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
         Dg.K = (int32_t)out;
         Dg.tenant = g;
         Dg.tiles_n = (int32_t)((in + kHTN - 1) / kHTN);
+        split_desc(Dg, N * hp.width[k - 1]);
         int32_t dj = (int32_t)descs.size();
         descs.push_back(Dg);
-        for (int32_t tm = 0; tm < tm_dyn; ++tm)
-          for (int32_t tn = 0; tn < Dg.tiles_n; ++tn) tiles.push_back(HeadTile{dj, tm, tn, 0});
+        for (int32_t tk = 0; tk < Dg.ksplit; ++tk)
+          for (int32_t tm = 0; tm < tm_dyn; ++tm)
+            for (int32_t tn = 0; tn < Dg.tiles_n; ++tn) tiles.push_back(HeadTile{dj, tm, tn, tk});
       }
     }
     bwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+    bwd_red.push_back(reduce_tiles(t0));
   }
 
   // one upload of every table: losses | descs | tiles (contiguous in ws)
@@ -945,15 +977,25 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
 
   JN_TRACED(c, JN_OP_POOL, p->T, p->d, p->N,
             launch_pool(s, hidden, p->seqlens, p->cu_seqlens, p->sample_tenant_rank, p->N, p->d, P), "pool");
-  for (auto& r : fwd_rng)
+  for (size_t i = 0; i < fwd_rng.size(); ++i) {
+    const auto r = fwd_rng[i], q = fwd_red[i];
     if (r.second)
       JN_TRACED(c, JN_OP_HEAD_FWD, r.second, 0, 0, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off),
                 "head fwd");
-  JN_TRACED(c, JN_OP_LOSS, G, 0, 0, launch_mse(s, dl, G, p->tenant_sample_off), "loss");
-  for (auto& r : bwd_rng)
+    if (q.second)
+      JN_TRACED(c, JN_OP_HEAD_FWD, q.second, 0, 0, launch_head_reduce(s, dd, dt + q.first, q.second, p->tenant_sample_off),
+                "head fwd reduce");
+  }
+  JN_TRACED(c, JN_OP_LOSS, G, 0, 0, launch_mse(s, dl, G, p->tenant_sample_off, (float*)(w + hp.lpart)), "loss");
+  for (size_t i = 0; i < bwd_rng.size(); ++i) {
+    const auto r = bwd_rng[i], q = bwd_red[i];
     if (r.second)
       JN_TRACED(c, JN_OP_HEAD_BWD, r.second, 0, 0, launch_head_gemm(s, dd, dt + r.first, r.second, p->tenant_sample_off),
                 "head bwd");
+    if (q.second)
+      JN_TRACED(c, JN_OP_HEAD_BWD, q.second, 0, 0, launch_head_reduce(s, dd, dt + q.first, q.second, p->tenant_sample_off),
+                "head bwd reduce");
+  }
   return JN_OK;
 }
 
@@ -1833,7 +1875,7 @@ struct jn_infer_plan {
   float* P = nullptr;
   const HeadGemm* dd = nullptr;
   const HeadTile* dt = nullptr;
-  std::vector<std::pair<int32_t, int32_t>> fwd_rng;
+  std::vector<std::pair<int32_t, int32_t>> fwd_rng, fwd_red;
   int32_t max_rows = 0;
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
@@ -1872,11 +1914,13 @@ void collector_prefix(const jn_collector* c, int32_t* count, int64_t* samples, b
   *samples = total;
 }
 
-// Forward-only head plan inside `w` (fwd tables only): P | Z_k | H_k | descs | tiles.
+// Forward-only head plan inside `w` (fwd tables only): P | Z_k | H_k | split-K
+// partials | descs | tiles.  A tenant's last layer writes the caller's action
+// buffer (rows from 0) and is never split.
 struct HeadFwdLayout {
   int maxL = 0;
   std::vector<int64_t> width;
-  size_t P = 0, descs = 0, tiles = 0, total = 0;
+  size_t P = 0, part = 0, descs = 0, tiles = 0, total = 0;
   std::vector<size_t> Z, H;
 };
 
@@ -1900,12 +1944,15 @@ HeadFwdLayout head_fwd_layout(int64_t N, int64_t d, const jn_head* heads, int32_
     L.H[k] = take(4 * N * L.width[k]);
   }
   const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
-  int64_t ntiles = 0, ndesc = 0;
+  int64_t ntiles = 0, ndesc = 0, part_elems = 0;
   for (int32_t g = 0; g < G; ++g)
     for (int k = 0; k < heads[g].n_layers; ++k) {
-      ntiles += tm_dyn * ((heads[g].dims[k + 1] + kHTN - 1) / kHTN);
+      const int64_t sk = k + 1 < heads[g].n_layers ? head_ksplit(heads[g].dims[k]) : 1;
+      ntiles += tm_dyn * ((heads[g].dims[k + 1] + kHTN - 1) / kHTN) * (sk + (sk > 1));
+      if (sk > 1) part_elems = std::max(part_elems, sk * N * L.width[k]);
       ++ndesc;
     }
+  L.part = take(4 * part_elems);
   L.descs = take(sizeof(HeadGemm) * ndesc);
   L.tiles = take(sizeof(HeadTile) * ntiles);
   L.total = o;
@@ -1977,10 +2024,15 @@ jn_status infer_enqueue(jn_ctx* c, const jn_infer_plan* pl) {
   if (st != JN_OK) return st;
   JN_TRACED(c, JN_OP_POOL, pk.T, pk.d, pk.N,
             launch_pool(s, pl->hidden, pk.seqlens, pk.cu_seqlens, pk.sample_tenant_rank, pk.N, pk.d, pl->P), "pool");
-  for (auto& r : pl->fwd_rng)
+  for (size_t i = 0; i < pl->fwd_rng.size(); ++i) {
+    const auto r = pl->fwd_rng[i], q = pl->fwd_red[i];
     if (r.second)
       JN_TRACED(c, JN_OP_HEAD_FWD, r.second, 0, 0,
                 launch_head_gemm(s, pl->dd, pl->dt + r.first, r.second, pk.tenant_sample_off), "head fwd");
+    if (q.second)
+      JN_TRACED(c, JN_OP_HEAD_FWD, q.second, 0, 0,
+                launch_head_reduce(s, pl->dd, pl->dt + q.first, q.second, pk.tenant_sample_off), "head fwd reduce");
+  }
   return JN_OK;
 }
 
@@ -2124,12 +2176,22 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
       D.K = (int32_t)in;
       D.tenant = g;
       D.tiles_n = (int32_t)((outw + kHTN - 1) / kHTN);
+      D.ksplit = last ? 1 : head_ksplit(in);
+      if (D.ksplit > 1) {
+        D.part = (float*)(hw + hl.part);
+        D.part_plane = N * hl.width[k];
+      }
       const int32_t di = (int32_t)descs.size();
       descs.push_back(D);
-      for (int32_t tm = 0; tm < tm_dyn; ++tm)
-        for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, 0});
+      for (int32_t tk = 0; tk < D.ksplit; ++tk)
+        for (int32_t tm = 0; tm < tm_dyn; ++tm)
+          for (int32_t tn = 0; tn < D.tiles_n; ++tn) tiles.push_back(HeadTile{di, tm, tn, tk});
     }
     pl->fwd_rng.emplace_back(t0, (int32_t)tiles.size() - t0);
+    const int32_t t1 = (int32_t)tiles.size();
+    for (int32_t t = t0; t < t1; ++t)
+      if (descs[tiles[t].desc].ksplit > 1 && tiles[t].tk == 0) tiles.push_back(tiles[t]);
+    pl->fwd_red.emplace_back(t1, (int32_t)tiles.size() - t1);
   }
   const size_t dbytes = sizeof(HeadGemm) * descs.size(), tbytes = sizeof(HeadTile) * tiles.size();
   if (hl.descs + dbytes > hl.tiles || hl.tiles + tbytes > hl.total) {

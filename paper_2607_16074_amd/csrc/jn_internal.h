@@ -123,21 +123,35 @@ struct HeadGemm {
   float* Cact;        // forward: also store gelu(C) (same ldc / bump as C)
   const float* Zg;    // data-gradient: C *= gelu'(Zg)  (same ldc / bump as C)
   float* db;          // weight-gradient: db[m] = sum_k A(m,k), by tn == 0 tiles
+  float* part;        // ksplit > 1: K range t of tile (m, n) writes its raw sum to
+                      // part[t * part_plane + off * bumpC + m * ldc + n]; the
+                      // reduce launch adds the ranges in order and applies the epilogue
+  int64_t part_plane;
   int64_t sam, sak, sbk, sbn, ldc;
   int64_t bumpA, bumpB, bumpC;
   int32_t M, N, K;
   int32_t tenant;
   int32_t tiles_n;
-  int32_t reserved;
+  int32_t ksplit;     // K ranges (1: the tile writes C with its epilogue)
 };
 struct HeadTile {
   int32_t desc;
   int32_t tm;
   int32_t tn;
-  int32_t reserved;
+  int32_t tk;  // K range (ksplit > 1)
 };
 hipError_t launch_head_gemm(hipStream_t s, const HeadGemm* descs, const HeadTile* tiles, int32_t n_tiles,
                             const int32_t* tenant_sample_off);
+// Sum of the K ranges of split descriptors, then bias / GELU' / GELU as in
+// the unsplit epilogue; tiles (desc, tm, tn, 0) of the split descriptors.
+hipError_t launch_head_reduce(hipStream_t s, const HeadGemm* descs, const HeadTile* tiles, int32_t n_tiles,
+                              const int32_t* tenant_sample_off);
+// K ranges of a head GEMM of contraction length K (a function of K only, so
+// a tenant's result does not depend on the rest of the batch).
+inline int32_t head_ksplit(int64_t K) {
+  const int64_t s = K / 256;
+  return K < 512 ? 1 : (int32_t)(s > 8 ? 8 : s);
+}
 
 // Per-tenant mean squared error over n_g * out elements:
 //   loss = mean((y - t)^2), dy = 2 (y - t) / (n_g * out), actions = y.
@@ -154,7 +168,8 @@ struct LossDesc {
   int32_t tenant;
   int32_t reserved;
 };
-hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tenant_sample_off);
+// part: 16 G floats of scratch (per-tenant partial sums, two launches).
+hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tenant_sample_off, float* part);
 
 // ---- action expert (k_expert.hip) ----
 // dst[r][c] = cvt(src[r][c]) for r < src_rows, c < src_cols, else 0; r < rows, c < cols.

@@ -117,6 +117,13 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
   const int32_t K = D.K < 0 ? ng : D.K;
   const int32_t m0 = tile.tm * HM, n0 = tile.tn * HN;
   if (m0 >= M) return;  // tiles past a tenant's row count (upper-bound grid)
+  // K range of this tile: all of K, or range tk of ksplit (chunk-aligned)
+  int32_t kb = 0, ke = K;
+  if (D.ksplit > 1) {
+    const int32_t kc = ((K + D.ksplit - 1) / D.ksplit + HKC - 1) / HKC * HKC;
+    kb = min(K, tile.tk * kc);
+    ke = min(K, kb + kc);
+  }
   const float* A = D.A + (int64_t)off * D.bumpA;
   const float* B = D.B + (int64_t)off * D.bumpB;
   const int tid = threadIdx.x;
@@ -136,7 +143,7 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
       int mm, kk;
       if (a_k_fast) { kk = e % HKC; mm = e / HKC; } else { mm = e % HM; kk = e / HM; }
       const int32_t m = m0 + mm, k = k0 + kk;
-      ra[q] = (m < M && k < K) ? A[(int64_t)m * D.sam + (int64_t)k * D.sak] : 0.f;
+      ra[q] = (m < M && k < ke) ? A[(int64_t)m * D.sam + (int64_t)k * D.sak] : 0.f;
     }
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
@@ -144,7 +151,7 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
       int nn, kk;
       if (b_k_fast) { kk = e % HKC; nn = e / HKC; } else { nn = e % HN; kk = e / HN; }
       const int32_t n = n0 + nn, k = k0 + kk;
-      rb[q] = (n < N && k < K) ? B[(int64_t)k * D.sbk + (int64_t)n * D.sbn] : 0.f;
+      rb[q] = (n < N && k < ke) ? B[(int64_t)k * D.sbk + (int64_t)n * D.sbn] : 0.f;
     }
   };
   auto store = [&]() {
@@ -164,12 +171,12 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
   float dbs = 0.f;  // bias gradient of row m0 + tid (tid < HM), k in order
   const int am = wm * 16 + (lane & 15), kq = lane >> 4;
   const int bn0 = wn * 32 + (lane & 15);
-  load(0);
-  for (int32_t k0 = 0; k0 < K; k0 += HKC) {
+  load(kb);
+  for (int32_t k0 = kb; k0 < ke; k0 += HKC) {
     store();
     __syncthreads();
-    if (k0 + HKC < K) load(k0 + HKC);
-    const int kend = min(HKC, K - k0);  // zero-filled beyond K
+    if (k0 + HKC < ke) load(k0 + HKC);
+    const int kend = min(HKC, ke - k0);  // zero-filled beyond the range
 #pragma unroll 8
     for (int kk = 0; kk < kend; kk += 4) {
       const float a = As[kk + kq][am];
@@ -183,6 +190,20 @@ __global__ __launch_bounds__(256) void head_gemm_kernel(const HeadGemm* __restri
     __syncthreads();
   }
 
+  if (D.ksplit > 1) {  // raw sum of this K range; the reduce launch finishes the tile
+    float* Pt = D.part + tile.tk * D.part_plane + (int64_t)off * D.bumpC;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int32_t n = n0 + wn * 32 + j * 16 + (lane & 15);
+      if (n >= N) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int32_t m = m0 + wm * 16 + 4 * (lane >> 4) + e;
+        if (m < M) Pt[(int64_t)m * D.ldc + n] = j == 0 ? acc0[e] : acc1[e];
+      }
+    }
+    return;
+  }
   float* C = D.C + (int64_t)off * D.bumpC;
   const float* Zg = D.Zg ? D.Zg + (int64_t)off * D.bumpC : nullptr;
   float* Cact = D.Cact ? D.Cact + (int64_t)off * D.bumpC : nullptr;
@@ -211,32 +232,79 @@ hipError_t launch_head_gemm(hipStream_t s, const HeadGemm* descs, const HeadTile
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------- mse ---
-
-__global__ __launch_bounds__(256) void mse_kernel(const LossDesc* __restrict__ descs,
-                                                  const int32_t* __restrict__ tso) {
-  __shared__ float red[256];
-  const LossDesc D = descs[blockIdx.x];
+// A long contraction (K >= 512) split into ksplit ranges keeps ~8x more
+// workgroups busy: the 2048-wide first layer of the 2B-shaped workload's
+// heads is 64 sequential K chunks per tile otherwise, each waiting for its
+// loads.  This launch finishes such tiles: thread t owns column n0 + t % 64
+// of rows m0 + t / 64 + 4 i; ranges are added in order, then the epilogue.
+__global__ __launch_bounds__(256) void head_reduce_kernel(const HeadGemm* __restrict__ descs,
+                                                          const HeadTile* __restrict__ tiles,
+                                                          const int32_t* __restrict__ tso) {
+  const HeadTile tile = tiles[blockIdx.x];
+  const HeadGemm D = descs[tile.desc];
   const int32_t off = tso[D.tenant];
   const int32_t ng = tso[D.tenant + 1] - off;
-  const int64_t cnt = (int64_t)ng * D.out;
+  const int32_t M = D.M < 0 ? ng : D.M;
+  const int32_t m0 = tile.tm * HM;
+  const int32_t n = tile.tn * HN + (threadIdx.x & 63);
+  if (m0 >= M || n >= D.N) return;
+  const float* Pt = D.part + (int64_t)off * D.bumpC;
+  float* C = D.C + (int64_t)off * D.bumpC;
+  const float* Zg = D.Zg ? D.Zg + (int64_t)off * D.bumpC : nullptr;
+  float* Cact = D.Cact ? D.Cact + (int64_t)off * D.bumpC : nullptr;
+  const float bias = D.bias ? D.bias[n] : 0.f;
+#pragma unroll
+  for (int i = 0; i < HM / 4; ++i) {
+    const int32_t m = m0 + (threadIdx.x >> 6) + 4 * i;
+    if (m >= M) break;
+    const int64_t ci = (int64_t)m * D.ldc + n;
+    float v = Pt[ci];
+    for (int32_t t = 1; t < D.ksplit; ++t) v += Pt[t * D.part_plane + ci];
+    v += bias;
+    if (Zg) v *= gelu_grad_f(Zg[ci]);
+    C[ci] = v;
+    if (Cact) Cact[ci] = gelu_f(v);
+  }
+}
+
+hipError_t launch_head_reduce(hipStream_t s, const HeadGemm* descs, const HeadTile* tiles, int32_t n_tiles,
+                              const int32_t* tso) {
+  head_reduce_kernel<<<n_tiles, 256, 0, s>>>(descs, tiles, tso);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------- mse ---
+
+// Block (tenant g, part b) of kMseParts takes elements [b c, (b + 1) c) of
+// the tenant's row-major [n_g][out] block (c = ceil(count / kMseParts)),
+// thread t every 256th of them in order; the block's partial sum of squared
+// errors goes to part[g kMseParts + b] (fixed-order tree), and a second
+// launch adds a tenant's parts in order.  One block per tenant measured
+// ~0.1 ms on the 2B-shaped workload (eight CUs waiting on their loads).
+constexpr int kMseParts = 16;
+
+__global__ __launch_bounds__(256) void mse_kernel(const LossDesc* __restrict__ descs,
+                                                  const int32_t* __restrict__ tso, float* __restrict__ part) {
+  __shared__ float red[256];
+  const int32_t g = blockIdx.x / kMseParts, b = blockIdx.x % kMseParts;
+  const LossDesc D = descs[g];
+  const int32_t off = tso[D.tenant];
+  const int32_t ng = tso[D.tenant + 1] - off;
+  const int32_t cnt = ng * D.out;
   const float scale = 2.0f / (float)cnt;
   const float* y = D.y + (int64_t)off * D.ld;
   float* dy = D.dy + (int64_t)off * D.ld;
-  // thread t takes columns t, t + 256, ... of every row, rows in order
+  const int32_t c = (cnt + kMseParts - 1) / kMseParts;
+  const int32_t e1 = min(cnt, (b + 1) * c);
   float ss = 0.f;
-  for (int32_t m = 0; m < ng; ++m) {
-    const float* yr = y + (int64_t)m * D.ld;
-    float* dyr = dy + (int64_t)m * D.ld;
-    const float* tr = D.target + (int64_t)m * D.out;
-    float* ar = D.actions + (int64_t)m * D.out;
-    for (int32_t n = threadIdx.x; n < D.out; n += 256) {
-      const float yv = yr[n];
-      const float diff = yv - tr[n];
-      ar[n] = yv;
-      dyr[n] = scale * diff;
-      ss += diff * diff;
-    }
+#pragma unroll 4
+  for (int32_t e = b * c + (int32_t)threadIdx.x; e < e1; e += 256) {
+    const int32_t m = e / D.out, n = e - m * D.out;
+    const float yv = y[(int64_t)m * D.ld + n];
+    const float diff = yv - D.target[e];
+    D.actions[e] = yv;
+    dy[(int64_t)m * D.ld + n] = scale * diff;
+    ss = fmaf(diff, diff, ss);
   }
   red[threadIdx.x] = ss;
   __syncthreads();
@@ -244,11 +312,26 @@ __global__ __launch_bounds__(256) void mse_kernel(const LossDesc* __restrict__ d
     if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) D.loss[0] = red[0] / (float)cnt;
+  if (threadIdx.x == 0) part[blockIdx.x] = red[0];
 }
 
-hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tso) {
-  mse_kernel<<<G, 256, 0, s>>>(descs, tso);
+__global__ __launch_bounds__(64) void mse_final_kernel(const LossDesc* __restrict__ descs,
+                                                       const int32_t* __restrict__ tso, const float* __restrict__ part,
+                                                       int32_t G) {
+  const int32_t g = blockIdx.x * 64 + threadIdx.x;
+  if (g >= G) return;
+  const LossDesc D = descs[g];
+  const int32_t cnt = (tso[D.tenant + 1] - tso[D.tenant]) * D.out;
+  float ss = 0.f;
+  for (int b = 0; b < kMseParts; ++b) ss += part[g * kMseParts + b];
+  D.loss[0] = ss / (float)cnt;
+}
+
+hipError_t launch_mse(hipStream_t s, const LossDesc* descs, int32_t G, const int32_t* tso, float* part) {
+  mse_kernel<<<G * kMseParts, 256, 0, s>>>(descs, tso, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  mse_final_kernel<<<(G + 63) / 64, 64, 0, s>>>(descs, tso, part, G);
   return hipGetLastError();
 }
 
