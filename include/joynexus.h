@@ -154,6 +154,8 @@ typedef struct jn_packed {
   int32_t R, G, N, T, d, max_seqlen, align;
   int32_t req_sig;         /* signature of the requests' (n_samples, max_len)
                               list, checked by jn_unpack                     */
+  int32_t max_tenant_n;    /* most samples of any one tenant (sizes the
+                              per-tenant launches; 0 = unknown, N is used)   */
   void* tokens;            /* device bf16 [T][d]; alignment rows are zero */
   int32_t* seqlens;
   int32_t* cu_seqlens;

@@ -67,6 +67,7 @@ _I32P = C.POINTER(C.c_int32)
 class jn_packed(C.Structure):
     _fields_ = [("R", C.c_int32), ("G", C.c_int32), ("N", C.c_int32), ("T", C.c_int32), ("d", C.c_int32),
                 ("max_seqlen", C.c_int32), ("align", C.c_int32), ("req_sig", C.c_int32),
+                ("max_tenant_n", C.c_int32),
                 ("tokens", C.c_void_p),
                 ("seqlens", _I32P), ("cu_seqlens", _I32P), ("sample_request", _I32P), ("sample_local", _I32P),
                 ("sample_tenant", _I32P), ("tenant_sample_off", _I32P), ("tenant_perm", _I32P),

@@ -322,6 +322,7 @@ void fill_packed(jn_packed* out, char* base, const MapLayout& m, const Plan& p, 
   out->d = o->d_model;
   out->max_seqlen = p.max_seqlen;
   out->align = o->align;
+  for (int32_t g = 0; g < G; ++g) out->max_tenant_n = std::max(out->max_tenant_n, p.toff[g + 1] - p.toff[g]);
   out->seqlens = (int32_t*)(base + m.seqlens);
   out->cu_seqlens = (int32_t*)(base + m.cu);
   out->sample_request = (int32_t*)(base + m.sreq);
@@ -375,8 +376,12 @@ int32_t request_signature(const jn_request* req, int32_t R) {
 bool valid_packed(const jn_packed* p) {
   return p && p->N > 0 && p->T > 0 && p->G > 0 && p->R > 0 && p->d > 0 && p->seqlens && p->cu_seqlens &&
          p->sample_request && p->sample_local && p->tenant_sample_off && p->sample_tenant_rank &&
-         p->req_table;
+         p->req_table && p->max_tenant_n >= 0 && p->max_tenant_n <= p->N;
 }
+
+// Row bound of a per-tenant launch: the largest tenant's samples when the
+// packing recorded it, else every sample.
+int64_t tenant_rows_bound(const jn_packed* p) { return p->max_tenant_n > 0 ? p->max_tenant_n : p->N; }
 
 }  // namespace
 
@@ -755,9 +760,10 @@ void head_layout(const jn_packed* p, const jn_head* heads, int32_t G, HeadPlan* 
   if (!with_descs) {
     // descriptor counts are bounded by G * 2 * maxL; tiles computed exactly below
   }
-  // tile counts: fwd M-dynamic (ceil(N/32) upper bound), bwd wgrad + dgrad;
-  // a split descriptor has ksplit tiles per output tile plus one reduce tile
-  const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
+  // tile counts: fwd M-dynamic (rows bounded by the largest tenant), bwd
+  // wgrad + dgrad; a split descriptor has ksplit tiles per output tile plus
+  // one reduce tile
+  const int64_t tm_dyn = (tenant_rows_bound(p) + kHTM - 1) / kHTM;
   int64_t ntiles = 0, ndesc = 0, part_elems = 0;
   for (int32_t g = 0; g < G; ++g) {
     const jn_head& Hh = heads[g];
@@ -821,7 +827,7 @@ jn_status heads_run(jn_ctx* c, const jn_packed* p, const void* hidden, const jn_
   char* w = (char*)ws;
   float* P = pooled ? pooled : (float*)(w + hp.P);
   const int64_t N = p->N, d = p->d;
-  const int32_t tm_dyn = (int32_t)((N + kHTM - 1) / kHTM);
+  const int32_t tm_dyn = (int32_t)((tenant_rows_bound(p) + kHTM - 1) / kHTM);
   auto Zk = [&](int k) { return (float*)(w + hp.Z[k]); };
   auto Hk = [&](int k) { return (float*)(w + hp.H[k]); };
   auto dZk = [&](int k) { return (float*)(w + hp.dZ[k]); };
@@ -1924,7 +1930,7 @@ struct HeadFwdLayout {
   std::vector<size_t> Z, H;
 };
 
-HeadFwdLayout head_fwd_layout(int64_t N, int64_t d, const jn_head* heads, int32_t G) {
+HeadFwdLayout head_fwd_layout(int64_t N, int64_t rows_bound, int64_t d, const jn_head* heads, int32_t G) {
   HeadFwdLayout L;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -1943,7 +1949,7 @@ HeadFwdLayout head_fwd_layout(int64_t N, int64_t d, const jn_head* heads, int32_
     L.Z[k] = take(4 * N * L.width[k]);
     L.H[k] = take(4 * N * L.width[k]);
   }
-  const int64_t tm_dyn = (N + kHTM - 1) / kHTM;
+  const int64_t tm_dyn = (rows_bound + kHTM - 1) / kHTM;
   int64_t ntiles = 0, ndesc = 0, part_elems = 0;
   for (int32_t g = 0; g < G; ++g)
     for (int k = 0; k < heads[g].n_layers; ++k) {
@@ -1996,7 +2002,9 @@ jn_status infer_layout(jn_ctx* c, const jn_request* req, int32_t R, const jn_ten
   }
   L->m = map_layout(p->N, p->T, G, R);
   L->bl = bb_layout(bb, p->T);
-  L->hl = head_fwd_layout(p->N, o->d_model, heads, G);
+  int32_t max_n = 0;
+  for (int32_t g = 0; g < G; ++g) max_n = std::max(max_n, p->toff[g + 1] - p->toff[g]);
+  L->hl = head_fwd_layout(p->N, max_n, o->d_model, heads, G);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -2147,7 +2155,7 @@ jn_status jn_infer_plan_create(jn_ctx* c, const jn_request* req, int32_t R, cons
   char* hw = w + L.heads;
   pl->P = (float*)(hw + hl.P);
   const int64_t N = p.N, d = o->d_model;
-  const int32_t tm_dyn = (int32_t)((N + kHTM - 1) / kHTM);
+  const int32_t tm_dyn = (int32_t)((tenant_rows_bound(&pl->packed) + kHTM - 1) / kHTM);
   std::vector<HeadGemm> descs;
   std::vector<HeadTile> tiles;
   for (int k = 0; k < hl.maxL; ++k) {
