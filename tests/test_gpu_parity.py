@@ -380,6 +380,23 @@ def test_grouped_equals_isolated_bitwise_geglu(jn):
     _grouped_equals_isolated(W.make_workload(spec))
 
 
+def test_head_k_split_ragged(jn):
+    """Head GEMMs whose contraction is split into K ranges with ragged ends
+    (K = 512, 600, 1030: ranges of 256, 320 and 288 columns, the last one
+    short) and a tenant of 40 samples (two row tiles): stage-wise against the
+    oracle at the head bar, and grouped == isolated bitwise (the split depends
+    on K only)."""
+    ten = (W.TenantSpec(3, 0, 1, 30, 40, (512, 600, 1030, 6), 3, 2),
+           W.TenantSpec(40, 0, 1, 30, 40, (512, 1030, 6), 3, 2),
+           W.TenantSpec(5, 0, 1, 30, 40, (512, 64, 6), 3, 2))
+    spec = W.WorkloadSpec(96, W.BackboneSpec(1, 512, 4, 256, False), ten, 0, "head k split")
+    wl = W.make_workload(spec)
+    _say("heads with ragged K ranges: 3 + 40 + 5 samples")
+    st = run_group(wl)
+    check_heads_stagewise(wl, st)
+    _grouped_equals_isolated(wl)
+
+
 def _grouped_equals_isolated(wl):
     from paper_2607_16074_amd import step as jstep
     model, reqs, targets = jstep.from_workload(wl)
