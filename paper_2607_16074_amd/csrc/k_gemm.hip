@@ -23,9 +23,10 @@
 // fills 1 KB = 8 rows; the lane -> source-chunk assignment applies the
 // swizzle.
 //
-// Loops: the 256x256 tile (8 wavefronts) runs a ring-buffered ping-pong loop
-// (gemm_ring_kernel); the smaller tiles of short launches and of the grouped
-// per-tenant launches run an interleaved double-buffered loop (gemm_tile).
+// Loops: the 256x256 tile (4 wavefronts, one per SIMD) runs a ring-buffered
+// loop (gemm_ring_kernel, gemm_grouped_ring_kernel); the smaller tiles of
+// short launches and of small grouped problems run an interleaved
+// double-buffered loop (gemm_tile).
 //
 // Launch order: tiles are walked in groups of 32 token-tiles (token tile
 // fastest).  Workgroups are dealt round-robin to the 8 XCDs, so the 32 tiles
@@ -108,6 +109,53 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x4 (&a
   const int64_t ldc = g.ldc;
   const int32_t M = g.M, N = g.N;
   const int q4 = (lane >> 4) * 4;
+  if constexpr (EPI == EPI_RESID_F32 || EPI == EPI_GELUGRAD_BF16) {
+    // Read-modify epilogues: the fp32 operands (residual rows, or saved
+    // pre-activations) of JB token-row blocks are all requested before the
+    // first store of the batch, so a batch costs one memory round trip
+    // instead of one per block.  Lanes outside the output read element (0, 0)
+    // of the operand and store nothing.
+    constexpr int JB = TM < 32 / TN ? TM : 32 / TN;
+    static_assert(TM % JB == 0, "batch of token-row blocks");
+    const float* src = EPI == EPI_RESID_F32 ? reinterpret_cast<const float*>(C) : g.aux;
+    const int64_t ldr = EPI == EPI_RESID_F32 ? ldc : g.ldaux;
+#pragma unroll
+    for (int j0 = 0; j0 < TM; j0 += JB) {
+      float4 r[JB][TN];
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        const int32_t m = tm * BM + wm * WM + (j0 + jj) * 16 + (lane & 15);
+        const int32_t mr = m < M ? m : 0;
+#pragma unroll
+        for (int i = 0; i < TN; ++i) {
+          const int32_t n = tn * BN + wn * WN + i * 16 + q4;
+          const int32_t nr = n < N ? n : 0;
+          r[jj][i] = *reinterpret_cast<const float4*>(src + (int64_t)mr * ldr + nr);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        const int32_t m = tm * BM + wm * WM + (j0 + jj) * 16 + (lane & 15);
+        if (m >= M) continue;
+#pragma unroll
+        for (int i = 0; i < TN; ++i) {
+          const int32_t n = tn * BN + wn * WN + i * 16 + q4;
+          if (n >= N) continue;
+          const f32x4 a = acc[i][j0 + jj];
+          const float4 z = r[jj][i];
+          if constexpr (EPI == EPI_RESID_F32) {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n) =
+                make_float4(z.x + a[0], z.y + a[1], z.z + a[2], z.w + a[3]);
+          } else {
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+                make_uint2(pack_bf2(a[0] * gelu_grad_f(z.x), a[1] * gelu_grad_f(z.y)),
+                           pack_bf2(a[2] * gelu_grad_f(z.z), a[3] * gelu_grad_f(z.w)));
+          }
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int32_t m = tm * BM + wm * WM + j * 16 + (lane & 15);
@@ -131,29 +179,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x4 (&a
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e];
-        if constexpr (EPI == EPI_RESID_F32) {
-          float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n);
-          float4 o = *p;
-          o.x += v[0];
-          o.y += v[1];
-          o.z += v[2];
-          o.w += v[3];
-          *p = o;
-        } else if constexpr (EPI == EPI_F32) {
+        if constexpr (EPI == EPI_F32) {
           *reinterpret_cast<float4*>(reinterpret_cast<float*>(C) + (int64_t)m * ldc + n) =
               make_float4(v[0], v[1], v[2], v[3]);
         } else if constexpr (EPI == EPI_GELU_SAVE) {
           *reinterpret_cast<float4*>(g.aux + (int64_t)m * g.ldaux + n) = make_float4(v[0], v[1], v[2], v[3]);
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = gelu_f(v[e]);
-          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
-              make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-        } else if constexpr (EPI == EPI_GELUGRAD_BF16) {
-          const float4 z = *reinterpret_cast<const float4*>(g.aux + (int64_t)m * g.ldaux + n);
-          v[0] *= gelu_grad_f(z.x);
-          v[1] *= gelu_grad_f(z.y);
-          v[2] *= gelu_grad_f(z.z);
-          v[3] *= gelu_grad_f(z.w);
           *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
               make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
         } else {
