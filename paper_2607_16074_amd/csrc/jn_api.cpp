@@ -1329,8 +1329,16 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     if (tiles < 0) rec.bad_gemm = true;
     const size_t at = rec.add(probs.data(), sizeof(GemmArgs) * probs.size());
     const int32_t n = (int32_t)probs.size();
-    rec.ops.push_back([=](char* a) { return launch_gemm_grouped(s, epi, (const GemmArgs*)(a + at), n, tiles, shape); });
+    const int trans = probs.empty() ? 0 : probs[0].trans;
+    rec.ops.push_back(
+        [=](char* a) { return launch_gemm_grouped(s, epi, (const GemmArgs*)(a + at), n, tiles, shape, trans); });
     rec.opcode.push_back(JN_OP_EXPERT_GEMM);
+  };
+  // Transposed-operand problems run only on the 256x256 tiles; elsewhere
+  // (offsets beyond the loop's 32-bit ones) the caller materialises the
+  // transposes instead.  Both give the same MFMA sequence per output element.
+  auto trans_ok = [&](const std::vector<GemmArgs>& probs) {
+    return gemm_grouped_tile_shape(probs.data(), (int32_t)probs.size()) == 0;
   };
   auto per_tenant_gemm = [&](int epi, std::function<GemmArgs(int32_t)> fn) {
     std::vector<GemmArgs> v;
@@ -1467,6 +1475,65 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       a.K = K;
       return a;
     });
+  };
+  // weight gradient C_g[out][in] = dY_g^T X_g over the tenant's rows of two
+  // row buffers (dY [rows][out], X [rows][in]; prefix: the tenant's prefix
+  // rows), read transposed by the GEMM -- or from zero-padded transposes
+  auto wgrad_rows = [&](const uint16_t* dy, int64_t out, const uint16_t* xin, int64_t in,
+                        std::function<float*(int32_t)> Csel, bool prefix) {
+    std::vector<GemmArgs> v;
+    for (int32_t g = 0; g < G; ++g) {
+      GemmArgs a{};
+      const int64_t r0 = prefix ? P.zoff[g] : P.roff[g];
+      a.X = dy + r0 * out;
+      a.ldx = out;
+      a.W = xin + r0 * in;
+      a.ldw = in;
+      a.C = Csel(g);
+      a.ldc = in;
+      a.M = (int32_t)out;
+      a.N = (int32_t)in;
+      a.K = prefix ? (int32_t)P.Pz[g] : P.rows[g];
+      a.trans = GEMM_TRANS_X | GEMM_TRANS_W;
+      v.push_back(a);
+    }
+    if (trans_ok(v)) {
+      gemm(EPI_F32, v);
+      return;
+    }
+    trans_rows(dy, out, B(Ly.TA), prefix);
+    trans_rows(xin, in, B(Ly.TB), prefix);
+    wgrad(out, in, Csel, prefix);
+  };
+  // data gradient C[rows][in] = epi(dY[rows][out] W_g[out][in]) per tenant,
+  // the weight read transposed by the GEMM -- or from a transposed copy
+  auto dgrad_rows = [&](int epi, const uint16_t* dy, int64_t out, std::function<const void*(int32_t)> wsel, int64_t in,
+                        void* C, bool cfp32, float* aux = nullptr) {
+    std::vector<GemmArgs> v;
+    for (int32_t g = 0; g < G; ++g) {
+      GemmArgs a{};
+      a.X = dy + (int64_t)P.roff[g] * out;
+      a.ldx = out;
+      a.W = (const uint16_t*)wsel(g);
+      a.ldw = in;
+      a.C = cfp32 ? (void*)((float*)C + (int64_t)P.roff[g] * in) : (void*)((uint16_t*)C + (int64_t)P.roff[g] * in);
+      a.ldc = in;
+      if (aux) {
+        a.aux = aux + (int64_t)P.roff[g] * in;
+        a.ldaux = in;
+      }
+      a.M = P.rows[g];
+      a.N = (int32_t)in;
+      a.K = (int32_t)out;
+      a.trans = GEMM_TRANS_W;
+      v.push_back(a);
+    }
+    if (trans_ok(v)) {
+      gemm(epi, v);
+      return;
+    }
+    trans_w(wsel, out, in);
+    rows_gemm(epi, dy, out, [&](int32_t g) { return (const uint16_t*)WTg(g, out, in); }, in, C, in, cfp32, aux);
   };
   auto Wl = [&](int l, const void* jn_expert_layer::*m) {
     return [=](int32_t g) { return (const uint16_t*)(ex[g].layers[l].*m); };
@@ -1614,9 +1681,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
 
   // --------------------------------------------------------------- backward
   rows_copy(F(Ly.dpred), false, B(Ly.dpredb), true, P.Na, kAP);
-  trans_rows(B(Ly.dpredb), kAP, B(Ly.TA), false);
-  trans_rows(B(Ly.yb), d, B(Ly.TB), false);
-  wgrad(kAP, d, [&](int32_t g) { return F(Ly.dwoutp) + (int64_t)g * kAP * d; }, false);
+  wgrad_rows(B(Ly.dpredb), kAP, B(Ly.yb), d, [&](int32_t g) { return F(Ly.dwoutp) + (int64_t)g * kAP * d; }, false);
   rows_gemm(EPI_F32, B(Ly.dpredb), kAP, [&](int32_t g) { return B(Ly.woutpT) + (int64_t)g * d * kAP; }, d, F(Ly.tf),
             d, true);
   rows_copy(nullptr, false, F(Ly.dx), false, P.Na, d);  // dx = 0
@@ -1627,25 +1692,16 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     const size_t g3 = ptr_table([&](int32_t g) { return ex[g].layers[l].g3; });
     // MLP block: x += m W_down^T, m = gelu(h3 W_up^T)
     rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
-    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-    trans_rows(B(Ly.mb[l]), f, B(Ly.TB), false);
-    wgrad(d, f, Gl(l, &jn_expert_layer_grads::w_down), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].w_down; }, d, f);
-    rows_gemm(EPI_GELUGRAD_BF16, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, f); }, f, B(Ly.tb), f,
-              false, F(Ly.pre[l]));
-    trans_rows(B(Ly.tb), f, B(Ly.TA), false);
-    trans_rows(B(Ly.h3[l]), d, B(Ly.TB), false);
-    wgrad(f, d, Gl(l, &jn_expert_layer_grads::w_up), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].w_up; }, f, d);
-    rows_gemm(EPI_F32, B(Ly.tb), f, [&](int32_t g) { return (const uint16_t*)WTg(g, f, d); }, d, F(Ly.tf), d, true);
+    wgrad_rows(B(Ly.dxb), d, B(Ly.mb[l]), f, Gl(l, &jn_expert_layer_grads::w_down), false);
+    dgrad_rows(EPI_GELUGRAD_BF16, B(Ly.dxb), d, [&](int32_t g) { return ex[g].layers[l].w_down; }, f, B(Ly.tb), false,
+               F(Ly.pre[l]));
+    wgrad_rows(B(Ly.tb), f, B(Ly.h3[l]), d, Gl(l, &jn_expert_layer_grads::w_up), false);
+    dgrad_rows(EPI_F32, B(Ly.tb), f, [&](int32_t g) { return ex[g].layers[l].w_up; }, d, F(Ly.tf), true);
     rms_bwd(Ly.x3[l], g3, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g3; }));
     // cross-attention block
     rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
-    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-    trans_rows(B(Ly.ocb[l]), d, B(Ly.TB), false);
-    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wo_c), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].wo_c; }, d, d);
-    rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
+    wgrad_rows(B(Ly.dxb), d, B(Ly.ocb[l]), d, Gl(l, &jn_expert_layer_grads::wo_c), false);
+    dgrad_rows(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return ex[g].layers[l].wo_c; }, d, F(Ly.tf), true);
     {
       AttnArgs A{};
       A.Q = B(Ly.qc[l]);
@@ -1676,22 +1732,14 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, true);
     }
-    trans_rows(B(Ly.tb), d, B(Ly.TA), false);
-    trans_rows(B(Ly.h2[l]), d, B(Ly.TB), false);
-    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wq_c), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].wq_c; }, d, d);
-    rows_gemm(EPI_F32, B(Ly.tb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
-    trans_rows(B(Ly.dkvb), 2 * d, B(Ly.TA), true);
-    trans_rows(B(Ly.z), dp, B(Ly.TB), true);
-    wgrad(2 * d, dp, Gl(l, &jn_expert_layer_grads::wkv_c), true);
+    wgrad_rows(B(Ly.tb), d, B(Ly.h2[l]), d, Gl(l, &jn_expert_layer_grads::wq_c), false);
+    dgrad_rows(EPI_F32, B(Ly.tb), d, [&](int32_t g) { return ex[g].layers[l].wq_c; }, d, F(Ly.tf), true);
+    wgrad_rows(B(Ly.dkvb), 2 * d, B(Ly.z), dp, Gl(l, &jn_expert_layer_grads::wkv_c), true);
     rms_bwd(Ly.x2[l], g2, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g2; }));
     // self-attention block
     rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
-    trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-    trans_rows(B(Ly.osb[l]), d, B(Ly.TB), false);
-    wgrad(d, d, Gl(l, &jn_expert_layer_grads::wo_s), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].wo_s; }, d, d);
-    rows_gemm(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return (const uint16_t*)WTg(g, d, d); }, d, F(Ly.tf), d, true);
+    wgrad_rows(B(Ly.dxb), d, B(Ly.osb[l]), d, Gl(l, &jn_expert_layer_grads::wo_s), false);
+    dgrad_rows(EPI_F32, B(Ly.dxb), d, [&](int32_t g) { return ex[g].layers[l].wo_s; }, d, F(Ly.tf), true);
     {
       AttnArgs A{};
       A.Q = B(Ly.qkv[l]);
@@ -1720,19 +1768,13 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       A.scale = scale;
       attn(A, true);
     }
-    trans_rows(B(Ly.tb), 3 * d, B(Ly.TA), false);
-    trans_rows(B(Ly.h1[l]), d, B(Ly.TB), false);
-    wgrad(3 * d, d, Gl(l, &jn_expert_layer_grads::wqkv_s), false);
-    trans_w([&](int32_t g) { return ex[g].layers[l].wqkv_s; }, 3 * d, d);
-    rows_gemm(EPI_F32, B(Ly.tb), 3 * d, [&](int32_t g) { return (const uint16_t*)WTg(g, 3 * d, d); }, d, F(Ly.tf), d,
-              true);
+    wgrad_rows(B(Ly.tb), 3 * d, B(Ly.h1[l]), d, Gl(l, &jn_expert_layer_grads::wqkv_s), false);
+    dgrad_rows(EPI_F32, B(Ly.tb), 3 * d, [&](int32_t g) { return ex[g].layers[l].wqkv_s; }, d, F(Ly.tf), true);
     rms_bwd(Ly.x1[l], g1, ptr_table([&](int32_t g) { return (const void*)io[g].layers[l].g1; }));
   }
   // input projection and the padded output-projection gradient
   rows_copy(F(Ly.dx), false, B(Ly.dxb), true, P.Na, d);
-  trans_rows(B(Ly.dxb), d, B(Ly.TA), false);
-  trans_rows(B(Ly.ub), KI, B(Ly.TB), false);
-  wgrad(d, KI, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * KI; }, false);
+  wgrad_rows(B(Ly.dxb), d, B(Ly.ub), KI, [&](int32_t g) { return F(Ly.dwinp) + (int64_t)g * d * KI; }, false);
   {
     std::vector<CopyDesc> v;
     for (int32_t g = 0; g < G; ++g) {

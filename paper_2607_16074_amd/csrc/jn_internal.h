@@ -51,7 +51,12 @@ enum GemmEpi : int32_t {
   EPI_GELUGRAD_BF16 = 6  // C bf16 = acc * gelu'(aux fp32)
 };
 
-// One GEMM problem: C[M][N] (+)= epi(X[M][K] W[N][K]^T); bf16 X, W row-major.
+// Operand layouts of a grouped problem (GemmArgs::trans): X stored [K][M]
+// (element (m, k) at X[k * ldx + m]), W stored [K][N].
+constexpr int GEMM_TRANS_X = 1, GEMM_TRANS_W = 2;
+
+// One GEMM problem: C[M][N] (+)= epi(X[M][K] W[N][K]^T); bf16 X, W row-major
+// unless `trans` says otherwise.
 struct GemmArgs {
   const uint16_t* X;
   const uint16_t* W;
@@ -61,6 +66,7 @@ struct GemmArgs {
   int64_t ldx, ldw, ldc, ldaux;
   int32_t M, N, K;
   int32_t tiles_m, tiles_n, tile_start;  // filled by the launchers
+  int32_t trans;        // GEMM_TRANS_* bits (grouped launches on 256x256 tiles only)
   int64_t split_c;      // split-K: elements between the fp32 partial outputs of
                         // consecutive K ranges (blockIdx.y); 0 when unsplit
 };
@@ -69,10 +75,15 @@ struct GemmArgs {
 // the problems, calls gemm_grouped_prepare (tile ranges, returns the tile
 // total, or -1 if a problem is not M, N, K > 0 with K % 64 == 0 and
 // N % 32 == 0), uploads them and launches.  shape from gemm_grouped_tile_shape.
+// Problems with transposed operands (all of one launch alike) run on the
+// 256x256 tiles (shape 0, which gemm_grouped_tile_shape returns for them, or
+// -1 where their offsets do not fit the loop's 32-bit ones); with both
+// operands transposed K need not be a multiple of 64.  Combinations launched:
+// EPI_F32 with GEMM_TRANS_W or both, EPI_GELUGRAD_BF16 with GEMM_TRANS_W.
 int gemm_grouped_tile_shape(const GemmArgs* probs, int32_t nprob);
 int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape);
 hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
-                               int shape);
+                               int shape, int trans = 0);
 
 // C[M][N] (+)= epi(A[M][K] * B[N][K]^T); A, B bf16 row-major with leading
 // dims lda, ldb (elements); for EPI_GEGLU_BF16, B is w_gate and B2 is w_up,

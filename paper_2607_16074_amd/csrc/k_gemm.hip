@@ -51,6 +51,7 @@ namespace jnx {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 #define JN_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
@@ -312,6 +313,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   }
   wait_lgkmcnt<0>();
   wait_vmcnt<0>();  // the repeated slab's DMA lands before the LDS is released
+  // accumulators pinned to the accumulation registers (as in ring_tile)
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) asm volatile("" : "+a"(acc[i][j]));
 
   gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
 }
@@ -434,6 +440,26 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const uint16_t* bas
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, n, 0x00020000);
 }
 
+// ds_read_b64_tr_b16 at LDS address p + OFF bytes, issued as inline assembly:
+// the compiler's wait insertion treats the builtin as a read that may alias
+// any LDS DMA in flight and puts a vmcnt(0) before it, which drains the
+// ring's prefetch on every fragment.  The asm is invisible to that pass, so
+// the caller waits (lgkmcnt) before using the result; the loops below wait
+// for all LDS reads at every phase boundary.
+template <int OFF>
+__device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint16_t*)p;
+  uint64_t r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
+// Chunk position swizzle of k-line k of a transposed operand's half-slab
+// (32 chunks of 16 bytes per line): the 16 k-lines one ds_read_b64_tr_b16
+// touches (8 per half-wave, 2 chunks each) cover every LDS bank once per
+// half-wave (checked with a bank model on the CPU).
+__device__ __forceinline__ int tswz(int k) { return 2 * ((k & 3) | ((k & 8) >> 1)); }
+
 // Ring-buffered loop of the 256x256 tile on 4 wavefronts, one per SIMD, each
 // 128 weight rows x 128 tokens (64 accumulator blocks, kept in the
 // accumulation registers).  Per K=64 slab kt, phase 0 runs the first k-half's
@@ -454,8 +480,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const uint16_t* bas
 // in the MFMA stream cost 30-50 cycles of issue, and global_load_lds with a
 // 64-bit address computed per instruction cost more than the buffer form.
 // Tile pid of problem g; lds holds 5 x 32 KB.
-template <int EPI>
+//
+// TR: operands stored transposed (GEMM_TRANS_X: X is [K][M], element (m, k)
+// at X[k * ldx + m]; GEMM_TRANS_W: W is [K][N]).  A transposed operand's
+// half-slab is 64 k-lines of 256 rows (512 B per line, 2 lines per DMA
+// instruction), its 16-byte chunks at position chunk ^ tswz(k); a fragment
+// is two ds_read_b64_tr_b16 (k-slots 0..3 and 4..7 of the lane's k block), so
+// the MFMA sequence per output element is the one of the row-major layout.
+// Loads past line K of a transposed operand return zero (buffer range), so
+// with both operands transposed K need not be a multiple of 64.
+template <int EPI, int TR>
 __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16_t* __restrict__ lds) {
+  constexpr bool TX = (TR & GEMM_TRANS_X) != 0, TW = (TR & GEMM_TRANS_W) != 0;
   constexpr int BN = 256, BM = 256, WGN = 2, WGM = 2;
   constexpr int WN = BN / WGN, WM = BM / WGM;
   constexpr int TN = WN / 16, TM = WM / 16;
@@ -474,22 +510,40 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   // columns tn*128..) -- rows past the end are clamped to the last one
   const int32_t m0 = tm * BM;
   const int32_t c0 = GLU ? tn * (BN / 2) : tn * BN;
-  const uint16_t* const xb = g.X + (int64_t)m0 * g.ldx;
-  const uint16_t* const wb = g.W + (int64_t)c0 * g.ldw;
+  static_assert(!(GLU && TW), "GeGLU weights are row-major");
+  const uint16_t* const xb = TX ? g.X + m0 : g.X + (int64_t)m0 * g.ldx;
+  const uint16_t* const wb = TW ? g.W + c0 : g.W + (int64_t)c0 * g.ldw;
   const uint16_t* const wb2 = GLU ? g.W2 + (int64_t)c0 * g.ldw : wb;
-  const __amdgpu_buffer_rsrc_t xr = panel_rsrc(xb, (int64_t)(M - m0) * g.ldx * 2);
-  const __amdgpu_buffer_rsrc_t wr = panel_rsrc(wb, (int64_t)(g.N - c0) * g.ldw * 2);
+  const __amdgpu_buffer_rsrc_t xr =
+      panel_rsrc(xb, TX ? ((int64_t)K * g.ldx - m0) * 2 : (int64_t)(M - m0) * g.ldx * 2);
+  const __amdgpu_buffer_rsrc_t wr =
+      panel_rsrc(wb, TW ? ((int64_t)K * g.ldw - c0) * 2 : (int64_t)(g.N - c0) * g.ldw * 2);
   const __amdgpu_buffer_rsrc_t wr2 = panel_rsrc(wb2, (int64_t)(g.N - c0) * g.ldw * 2);
-  // wave w fetches rows 64w .. 64w+63 of both halves, 8 rows per instruction
+  // row-major operand: wave w fetches rows 64w .. 64w+63 of the half-slab, 8
+  // rows per instruction; transposed: k-lines 16w .. 16w+15, 2 per instruction
   uint32_t xo[NI], wo[NI];
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int r = 64 * wave + 8 * i + (lane >> 3);
     const int chunk = (lane & 7) ^ lds_swz(r);
-    xo[i] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * g.ldx + chunk * 8) * 2);
-    const int32_t col = GLU ? min(c0 + (r >> 5) * 16 + (r & 15), g.N - 1) : min(c0 + r, g.N - 1);
-    wo[i] = (uint32_t)(((int64_t)(col - c0) * g.ldw + chunk * 8) * 2);
+    const int kl = 16 * wave + 2 * i + (lane >> 5);
+    const int tchunk = (lane & 31) ^ tswz(kl);
+    if constexpr (TX)
+      xo[i] = (uint32_t)(((int64_t)kl * g.ldx + tchunk * 8) * 2);
+    else
+      xo[i] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * g.ldx + chunk * 8) * 2);
+    if constexpr (TW) {
+      wo[i] = (uint32_t)(((int64_t)kl * g.ldw + tchunk * 8) * 2);
+    } else {
+      const int32_t col = GLU ? min(c0 + (r >> 5) * 16 + (r & 15), g.N - 1) : min(c0 + r, g.N - 1);
+      wo[i] = (uint32_t)(((int64_t)(col - c0) * g.ldw + chunk * 8) * 2);
+    }
   }
+  // byte step between slabs: one 128-byte row segment (in the scalar offset),
+  // or 64 k-lines of a transposed operand (in the lane offset, which the
+  // buffer range check covers, so lines past K read zero)
+  const int32_t xso = TX ? (int32_t)(kBK * 2 * g.ldx) : kBK * 2;
+  const int32_t wso = TW ? (int32_t)(kBK * 2 * g.ldw) : kBK * 2;
   const int dro = wave * NI * 512;         // this wave's 1 KB blocks inside a slot
   uint16_t* const ring2 = lds;             // weight slabs, slot kt % 2
   uint16_t* const ring3 = lds + 2 * SLOT;  // token slabs, slot kt % 3
@@ -497,11 +551,12 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   // weight rows of one 16-row block, all gate (W) or all up (W2)
 #define JN_DMA_W(i, slab, slot)                                                                                  \
   __builtin_amdgcn_raw_ptr_buffer_load_lds((GLU && (((i) >> 1) & 1)) ? wr2 : wr,                                \
-                                           JN_LPTR(ring2 + (slot) * SLOT + dro + (i) * 512), 16, wo[i],         \
-                                           (slab) * (kBK * 2), 0, 0)
+                                           JN_LPTR(ring2 + (slot) * SLOT + dro + (i) * 512), 16,                \
+                                           TW ? wo[i] + (uint32_t)((slab) * wso) : wo[i], TW ? 0 : (slab) * wso, 0, 0)
 #define JN_DMA_X(i, slab, slot)                                                                                  \
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, JN_LPTR(ring3 + (slot) * SLOT + dro + (i) * 512), 16, xo[i],      \
-                                           (slab) * (kBK * 2), 0, 0)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, JN_LPTR(ring3 + (slot) * SLOT + dro + (i) * 512), 16,            \
+                                           TX ? xo[i] + (uint32_t)((slab) * xso) : xo[i], TX ? 0 : (slab) * xso, 0, \
+                                           0)
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -509,9 +564,34 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = K / kBK;
+  const int KT = (K + kBK - 1) / kBK;
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = wm * WM + (lane & 15);
+  // transposed reads: lane (quad, e = (lane & 15) / 4, c = lane & 3) reads k-line
+  // 8 quad + e (+4) at rows rbase + 4c; tr_base(part) | 16 ts, XORed with 16 f
+  // per fragment f, addresses the swizzled chunk (bits 4-6 are free below)
+  const int te = (lane & 15) >> 2, tc = lane & 3;
+  const int tlane = (8 * quad + te) * 256 + 8 * (tc >> 1) + 4 * (tc & 1) + 16 * ((te & 3) | ((quad & 1) << 2));
+  const int twl = tlane + 128 * wn, txl = tlane + 128 * wm;
+  // fragment f (16 rows) of k-half h of a half-slab slot
+  auto frag_w = [&](const uint16_t* slot, int f, int h) -> bf16x8 {
+    if constexpr (TW) {
+      const uint16_t* p = slot + 8192 * h + (twl ^ (16 * f));
+      const bf16x4 lo = lds_read_tr<0>(p), hi = lds_read_tr<2048>(p);
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    } else {
+      return *reinterpret_cast<const bf16x8*>(slot + (wrow + 16 * f) * kBK + ((4 * h + quad) ^ sw) * 8);
+    }
+  };
+  auto frag_x = [&](const uint16_t* slot, int f, int h) -> bf16x8 {
+    if constexpr (TX) {
+      const uint16_t* p = slot + 8192 * h + (txl ^ (16 * f));
+      const bf16x4 lo = lds_read_tr<0>(p), hi = lds_read_tr<2048>(p);
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    } else {
+      return *reinterpret_cast<const bf16x8*>(slot + (xrow + 16 * f) * kBK + ((4 * h + quad) ^ sw) * 8);
+    }
+  };
 
   // prologue: slabs 0 and 1 (both halves), then slab 0's first-half fragments
   {
@@ -528,13 +608,10 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   }
   __builtin_amdgcn_s_barrier();
   bf16x8 fa[TN + TM], fb[TN + TM];  // first-half / second-half fragments: weights, then tokens
-  {
-    const int pos = quad ^ sw;
 #pragma unroll
-    for (int i = 0; i < TN; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(ring2 + (wrow + 16 * i) * kBK + pos * 8);
+  for (int i = 0; i < TN; ++i) fa[i] = frag_w(ring2, i, 0);
 #pragma unroll
-    for (int j = 0; j < TM; ++j) fa[TN + j] = *reinterpret_cast<const bf16x8*>(ring3 + (xrow + 16 * j) * kBK + pos * 8);
-  }
+  for (int j = 0; j < TM; ++j) fa[TN + j] = frag_x(ring3, j, 0);
   wait_lgkmcnt<0>();
 
   int slot3 = 0;  // kt % 3
@@ -547,7 +624,6 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
     {
       const uint16_t* cw = ring2 + slot2 * SLOT;
       const uint16_t* cx = ring3 + slot3 * SLOT;
-      const int pos = (4 + quad) ^ sw;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int q = 0; q < TN * TM; ++q) {
@@ -556,9 +632,9 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
         if ((q & 3) == 0) {
           const int f = q >> 2;
           if (f < TN)
-            fb[f] = *reinterpret_cast<const bf16x8*>(cw + (wrow + 16 * f) * kBK + pos * 8);
+            fb[f] = frag_w(cw, f, 1);
           else
-            fb[f] = *reinterpret_cast<const bf16x8*>(cx + (xrow + 16 * (f - TN)) * kBK + pos * 8);
+            fb[f] = frag_x(cx, f - TN, 1);
         }
         if ((q & 7) == 6) JN_DMA_X(q >> 3, sf, prev3);
         __builtin_amdgcn_sched_barrier(0);
@@ -574,7 +650,6 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
     {
       const uint16_t* nw = ring2 + (slot2 ^ 1) * SLOT;
       const uint16_t* nx = ring3 + next3 * SLOT;
-      const int pos = quad ^ sw;
 #pragma unroll
       for (int q = 0; q < TN * TM; ++q) {
         const int i = q / TM, j = q % TM;
@@ -582,9 +657,9 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
         if ((q & 3) == 0) {
           const int f = q >> 2;
           if (f < TN)
-            fa[f] = *reinterpret_cast<const bf16x8*>(nw + (wrow + 16 * f) * kBK + pos * 8);
+            fa[f] = frag_w(nw, f, 0);
           else
-            fa[f] = *reinterpret_cast<const bf16x8*>(nx + (xrow + 16 * (f - TN)) * kBK + pos * 8);
+            fa[f] = frag_x(nx, f - TN, 0);
         }
         if ((q & 7) == 6) JN_DMA_W(q >> 3, sf, slot2);
         __builtin_amdgcn_sched_barrier(0);
@@ -596,6 +671,16 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
 #undef JN_DMA_W
 #undef JN_DMA_X
   wait_vmcnt<0>();  // the repeated slabs' DMAs land before the LDS is reused or released
+  // Pin the accumulators to the accumulation registers where the loop ends.
+  // Left to itself, the register allocator placed some accumulators of the
+  // epilogues that can store straight from either register file (fp32 store,
+  // fp32 pre-activation save) in vector registers and copied them into
+  // accumulation registers before every MFMA of the loop (with spills to
+  // scratch in the grouped variants).
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) asm volatile("" : "+a"(acc[i][j]));
 
   if constexpr (EPI == EPI_BF16 || EPI == EPI_GELU_BF16) {
     __builtin_amdgcn_s_barrier();
@@ -610,18 +695,18 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
 template <int EPI>
 __global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * 256 * kBK];
-  ring_tile<EPI>(split_range(g0), blockIdx.x, lds);
+  ring_tile<EPI, 0>(split_range(g0), blockIdx.x, lds);
 }
 
 // Grouped ring tiles: problem p owns tiles [tile_start, tile_start + tiles).
-template <int EPI>
+template <int EPI, int TR>
 __global__ __launch_bounds__(256, 1) void gemm_grouped_ring_kernel(const GemmArgs* __restrict__ probs, int32_t nprob) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * 256 * kBK];
   const int32_t b = blockIdx.x;
   int32_t p = 0;
   while (p + 1 < nprob && probs[p + 1].tile_start <= b) ++p;
   const GemmArgs g = probs[p];
-  ring_tile<EPI>(g, b - g.tile_start, lds);
+  ring_tile<EPI, TR>(g, b - g.tile_start, lds);
 }
 
 template <int BN, int BM, int WGN, int WGM>
@@ -674,16 +759,19 @@ static hipError_t launch_tile(hipStream_t s, int epi, GemmArgs g, int32_t splits
 }
 
 static hipError_t launch_grouped_ring(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob,
-                                      int32_t total_tiles) {
+                                      int32_t total_tiles, int trans) {
   dim3 grid(total_tiles), block(256);
-#define JN_GEMM_CASE(E) \
-  case E: gemm_grouped_ring_kernel<E><<<grid, block, 0, s>>>(dprobs, nprob); break;
-  switch (epi) {
-    JN_GEMM_CASE(EPI_BF16)
-    JN_GEMM_CASE(EPI_RESID_F32)
-    JN_GEMM_CASE(EPI_F32)
-    JN_GEMM_CASE(EPI_GELU_SAVE)
-    JN_GEMM_CASE(EPI_GELUGRAD_BF16)
+#define JN_GEMM_CASE(E, T) \
+  case E * 4 + T: gemm_grouped_ring_kernel<E, T><<<grid, block, 0, s>>>(dprobs, nprob); break;
+  switch (epi * 4 + trans) {
+    JN_GEMM_CASE(EPI_BF16, 0)
+    JN_GEMM_CASE(EPI_RESID_F32, 0)
+    JN_GEMM_CASE(EPI_F32, 0)
+    JN_GEMM_CASE(EPI_GELU_SAVE, 0)
+    JN_GEMM_CASE(EPI_GELUGRAD_BF16, 0)
+    JN_GEMM_CASE(EPI_F32, GEMM_TRANS_W)
+    JN_GEMM_CASE(EPI_GELUGRAD_BF16, GEMM_TRANS_W)
+    JN_GEMM_CASE(EPI_F32, GEMM_TRANS_X | GEMM_TRANS_W)
     default:
       return hipErrorInvalidValue;
   }
@@ -946,21 +1034,32 @@ constexpr int32_t kGroupedRingRows = 512;
 
 int gemm_grouped_tile_shape(const GemmArgs* probs, int32_t nprob) {
   int32_t max_m = 0;
-  bool ring_ok = true;
+  bool ring_ok = true, trans = false;
+  constexpr int64_t kMax = 0x7fffffff;
   for (int32_t p = 0; p < nprob; ++p) {
-    max_m = std::max(max_m, probs[p].M);
-    if ((int64_t)256 * std::max(probs[p].ldx, probs[p].ldw) * 2 > (int64_t)0x7fffffff) ring_ok = false;
+    const GemmArgs& g = probs[p];
+    max_m = std::max(max_m, g.M);
+    // per-lane panel offsets: 256 rows of a row-major operand, or its whole
+    // K lines (plus one slab) for a transposed one
+    const int64_t kx = (int64_t)g.K + kBK, span_x = (g.trans & GEMM_TRANS_X) ? kx * g.ldx : 256 * g.ldx;
+    const int64_t span_w = (g.trans & GEMM_TRANS_W) ? kx * g.ldw : 256 * g.ldw;
+    if (2 * std::max(span_x, span_w) > kMax) ring_ok = false;
+    trans = trans || g.trans != 0;
   }
+  if (trans) return ring_ok ? 0 : -1;
   if (ring_ok && max_m >= kGroupedRingRows) return 0;
   return max_m >= 1024 ? 1 : 2;
 }
 
 int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
+  if (shape < 0 || shape > 2 || nprob <= 0) return -1;
   const int BN = shape == 2 ? 128 : 256, BM = shape == 0 ? 256 : 128;
   int32_t total = 0;
   for (int32_t p = 0; p < nprob; ++p) {
     const GemmArgs& g = probs[p];
-    if (g.M <= 0 || g.N <= 0 || g.K <= 0 || g.K % kBK != 0 || g.N % 32 != 0) return -1;
+    const bool ragged_ok = g.trans == (GEMM_TRANS_X | GEMM_TRANS_W);
+    if (g.trans != probs[0].trans || g.trans < 0 || g.trans > 3 || (g.trans && shape != 0)) return -1;
+    if (g.M <= 0 || g.N <= 0 || g.K <= 0 || (!ragged_ok && g.K % kBK != 0) || g.N % 32 != 0) return -1;
     probs[p].tiles_m = (probs[p].M + BM - 1) / BM;
     probs[p].tiles_n = (probs[p].N + BN - 1) / BN;
     probs[p].tile_start = total;
@@ -970,9 +1069,9 @@ int32_t gemm_grouped_prepare(GemmArgs* probs, int32_t nprob, int shape) {
 }
 
 hipError_t launch_gemm_grouped(hipStream_t s, int epi, const GemmArgs* dprobs, int32_t nprob, int32_t total_tiles,
-                               int shape) {
-  if (nprob <= 0 || total_tiles <= 0) return hipErrorInvalidValue;
-  if (shape == 0) return launch_grouped_ring(s, epi, dprobs, nprob, total_tiles);
+                               int shape, int trans) {
+  if (nprob <= 0 || total_tiles <= 0 || (trans && shape != 0)) return hipErrorInvalidValue;
+  if (shape == 0) return launch_grouped_ring(s, epi, dprobs, nprob, total_tiles, trans);
   if (shape == 1) return launch_grouped_tile<256, 128, 4, 2>(s, epi, dprobs, nprob, total_tiles);
   return launch_grouped_tile<128, 128, 2, 2>(s, epi, dprobs, nprob, total_tiles);
 }
