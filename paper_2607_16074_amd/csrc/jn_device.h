@@ -18,6 +18,21 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
   return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
 }
 
+// ds_read_b64_tr_b16 at LDS address p + OFF bytes (in each 16-lane group,
+// lane i receives element i % 4 of the 8-byte chunks that lanes 4e + i / 4
+// address, e = 0..3), issued as inline assembly.  The compiler's wait
+// insertion treats the builtin form as a read that may alias any LDS DMA in
+// flight and puts a vmcnt(0) before it, which drains every prefetch that is
+// in flight; the asm is invisible to that pass, so the caller waits
+// (lgkmcnt) before it uses the result.
+template <int OFF>
+__device__ __forceinline__ uint64_t lds_read_tr_b16(const void* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+  uint64_t r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+  return r;
+}
+
 // v together with the value lane l ^ 16 (v_permlane16_swap) or l ^ 32
 // (v_permlane32_swap) holds, without an LDS round trip.  The two come back
 // in an order that differs between the lanes of a pair, so only commutative

@@ -440,20 +440,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const uint16_t* bas
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, n, 0x00020000);
 }
 
-// ds_read_b64_tr_b16 at LDS address p + OFF bytes, issued as inline assembly:
-// the compiler's wait insertion treats the builtin as a read that may alias
-// any LDS DMA in flight and puts a vmcnt(0) before it, which drains the
-// ring's prefetch on every fragment.  The asm is invisible to that pass, so
-// the caller waits (lgkmcnt) before using the result; the loops below wait
-// for all LDS reads at every phase boundary.
-template <int OFF>
-__device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
-  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint16_t*)p;
-  uint64_t r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
-  return __builtin_bit_cast(bf16x4, r);
-}
-
 // Chunk position swizzle of k-line k of a transposed operand's half-slab
 // (32 chunks of 16 bytes per line): the 16 k-lines one ds_read_b64_tr_b16
 // touches (8 per half-wave, 2 chunks each) cover every LDS bank once per
@@ -567,7 +553,8 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   const int KT = (K + kBK - 1) / kBK;
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = wm * WM + (lane & 15);
-  // transposed reads: lane (quad, e = (lane & 15) / 4, c = lane & 3) reads k-line
+  // transposed reads (inline assembly, covered by the loop's LDS waits at
+  // every phase boundary): lane (quad, e = (lane & 15) / 4, c = lane & 3) reads k-line
   // 8 quad + e (+4) at rows rbase + 4c; tr_base(part) | 16 ts, XORed with 16 f
   // per fragment f, addresses the swizzled chunk (bits 4-6 are free below)
   const int te = (lane & 15) >> 2, tc = lane & 3;
@@ -577,7 +564,8 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   auto frag_w = [&](const uint16_t* slot, int f, int h) -> bf16x8 {
     if constexpr (TW) {
       const uint16_t* p = slot + 8192 * h + (twl ^ (16 * f));
-      const bf16x4 lo = lds_read_tr<0>(p), hi = lds_read_tr<2048>(p);
+      const bf16x4 lo = __builtin_bit_cast(bf16x4, lds_read_tr_b16<0>(p));
+      const bf16x4 hi = __builtin_bit_cast(bf16x4, lds_read_tr_b16<2048>(p));
       return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     } else {
       return *reinterpret_cast<const bf16x8*>(slot + (wrow + 16 * f) * kBK + ((4 * h + quad) ^ sw) * 8);
@@ -586,7 +574,8 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
   auto frag_x = [&](const uint16_t* slot, int f, int h) -> bf16x8 {
     if constexpr (TX) {
       const uint16_t* p = slot + 8192 * h + (txl ^ (16 * f));
-      const bf16x4 lo = lds_read_tr<0>(p), hi = lds_read_tr<2048>(p);
+      const bf16x4 lo = __builtin_bit_cast(bf16x4, lds_read_tr_b16<0>(p));
+      const bf16x4 hi = __builtin_bit_cast(bf16x4, lds_read_tr_b16<2048>(p));
       return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     } else {
       return *reinterpret_cast<const bf16x8*>(slot + (xrow + 16 * f) * kBK + ((4 * h + quad) ^ sw) * 8);
