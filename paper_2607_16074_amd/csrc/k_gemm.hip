@@ -57,7 +57,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 #define JN_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 constexpr int kBK = 64;       // K per slab (128-byte rows)
-constexpr int kStages = 2;    // double buffer of the interleaved loop
+constexpr int kStages = 3;    // LDS stages of the interleaved loop (prefetch distance 2)
 constexpr int kGroupM = 32;   // token tiles per L2 group
 
 __device__ __forceinline__ int lds_swz(int r) { return (r >> 1) & 7; }
@@ -263,23 +263,33 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   const int sw = lds_swz(lane & 15), quad = lane >> 4;
   const int wrow = wn * WN + (lane & 15), xrow = BN + wm * WM + (lane & 15);
 
-  // prologue: slab 0; slab kt+1 is fetched during slab kt's first half
+  // prologue: slabs 0 .. kStages-2; slab kt+kStages-1 is fetched during slab
+  // kt's first half into the stage slab kt-1 used
+  static_assert(kStages == 3, "prefetch distance 2");
 #pragma unroll
   for (int i = 0; i < NI; ++i)
     __builtin_amdgcn_global_load_lds(JN_GPTR(src[i]), JN_LPTR(dst0 + i * 512), 16, 0, 0);
-  wait_vmcnt<0>();
+  {
+    const int s1 = min(1, KT - 1);
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      __builtin_amdgcn_global_load_lds(JN_GPTR(src[i] + s1 * kBK), JN_LPTR(dst0 + STAGE + i * 512), 16, 0, 0);
+  }
+  wait_vmcnt<NI>();  // slab 0 landed
   __builtin_amdgcn_s_barrier();
 
   // The loop body has no branches (each one in the MFMA stream costs tens of
-  // cycles of issue): the last slab's fetch repeats slab KT-1 into the free
-  // buffer, and its next-slab fragment reads read that buffer.
+  // cycles of issue): past the last slab the fetches repeat slab KT-1 into a
+  // free stage, and the last next-slab fragment reads read a free stage.
   bf16x8 fw[2][TN], fx[2][TM];
   gemm_frags<TN>(fw[0], lds, wrow, quad ^ sw);
   gemm_frags<TM>(fx[0], lds, xrow, quad ^ sw);
+  int st = 0;  // kt % 3
   for (int kt = 0; kt < KT; ++kt) {
-    const uint16_t* cur = lds + (kt & 1) * STAGE;
-    const int sf = min(kt + 1, KT - 1);  // slab fetched into the buffer slab kt-1 used
-    uint16_t* const fdst = dst0 + ((kt + 1) & 1) * STAGE;
+    const int st1 = st == 2 ? 0 : st + 1, st2 = st == 0 ? 2 : st - 1;  // (kt + 1) % 3, (kt + 2) % 3
+    const uint16_t* cur = lds + st * STAGE;
+    const int sf = min(kt + 2, KT - 1);  // slab fetched into the stage slab kt-1 used
+    uint16_t* const fdst = dst0 + st2 * STAGE;
 #pragma unroll
     for (int step = 0; step < 2; ++step) {
       if (step == 0) {
@@ -287,10 +297,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
         gemm_frags<TN>(fw[1], cur, wrow, pos);
         gemm_frags<TM>(fx[1], cur, xrow, pos);
       } else {
-        wait_vmcnt<0>();
+        wait_vmcnt<NI>();  // slab kt+1 landed; slab kt+2's fetch may stay in flight
         wait_lgkmcnt<0>();
         __builtin_amdgcn_s_barrier();
-        const uint16_t* nxt = lds + ((kt + 1) & 1) * STAGE;
+        const uint16_t* nxt = lds + st1 * STAGE;
         gemm_frags<TN>(fw[0], nxt, wrow, quad ^ sw);
         gemm_frags<TM>(fx[0], nxt, xrow, quad ^ sw);
       }
@@ -310,9 +320,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    st = st1;
   }
   wait_lgkmcnt<0>();
-  wait_vmcnt<0>();  // the repeated slab's DMA lands before the LDS is released
+  wait_vmcnt<0>();  // the repeated slabs' DMAs land before the LDS is released
   // accumulators pinned to the accumulation registers (as in ring_tile)
 #pragma unroll
   for (int i = 0; i < TN; ++i)
