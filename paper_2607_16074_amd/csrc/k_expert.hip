@@ -424,7 +424,10 @@ __device__ __forceinline__ int xa_swz(int r) {
     const int x = (r >> 1) & 7;  // 2 rows per 256-byte bank row: bit-reversed row pair
     return ((x & 1) << 2) | (x & 2) | (x >> 2);
   } else {
-    return ((r & 3) << 2) | ((r >> 2) & 3);
+    // one row per bank row; a transposed read is served 32 lanes at a time,
+    // and this keeps its 8 rows x 2 chunks (and a fragment read's 16 rows) on
+    // 16 distinct 16-byte bank slots
+    return ((r & 7) << 1) | ((r >> 3) & 1);
   }
 }
 
