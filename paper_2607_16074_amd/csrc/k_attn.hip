@@ -60,11 +60,15 @@ constexpr int kKeys = 64;    // keys per step (64 measured best for head widths 
 //   HD 32  (4 rows per 256-byte bank row): (r >> 2) & 3
 //   HD 64  (2 rows per bank row):          bit-reversed ((r >> 1) & 7)
 //   HD 128:                                4 * (r & 3) + ((r >> 2) & 3)
-//   HD 256:                                2 * (r & 7) + ((r >> 3) & 1)
-// At head width 256 the hardware serves a transposed read 32 lanes at a
-// time (the bank-conflict counter showed 19% of the kernel's cycles with the
-// HD 128 rule, whose two 16-lane halves collide): the rule used keeps the 8
-// rows x 2 chunks of a half-wave on 16 distinct slots as well.
+//   HD 256 (r = 4 q + e):                  2 * (e + 4 * ((q ^ q / 2) & 1)) + q / 2
+// At head width 256 a transposed read (16 lanes = 4 rows x 2 chunks) is
+// served together with a second 16-lane group, and the bank-conflict
+// counter located the pairs: groups q and q ^ 1 and groups q and q ^ 2.
+// The HD 128 rule puts rows r and r ^ 4 on one bank slot pair (19% of the
+// kernel's cycles in conflicts), 2 * (r & 7) + r / 8 rows r and r ^ 8 (9.5%);
+// this rule pairs rows r and r ^ 12 only, which no served pair holds
+// together (0 conflict cycles, and still 16 distinct slots for the 16 rows of
+// a K fragment read).
 template <int HD>
 __device__ __forceinline__ int attn_swz(int r) {
   if constexpr (HD == 32) {
@@ -75,7 +79,8 @@ __device__ __forceinline__ int attn_swz(int r) {
   } else if constexpr (HD == 128) {
     return ((r & 3) << 2) | ((r >> 2) & 3);
   } else {
-    return ((r & 7) << 1) | ((r >> 3) & 1);
+    const int q = (r >> 2) & 3, e = r & 3;
+    return ((e | (((q ^ (q >> 1)) & 1) << 2)) << 1) | ((q >> 1) & 1);
   }
 }
 
