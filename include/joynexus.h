@@ -99,6 +99,21 @@ jn_status jn_ctx_set_trace(jn_ctx* ctx, int32_t enable);
  * trace.  Synchronizes with the context stream. */
 jn_status jn_ctx_trace_read(jn_ctx* ctx, jn_trace_entry* out, int32_t cap, int32_t* n);
 
+/* Context options (jn_ctx_set_option), for verification; a context starts
+ * with every option 0.
+ *   JN_OPT_EXPERT_TRANSPOSES: 1 = the action-expert gradient GEMMs (the
+ *     weight gradients dY^T X over a tenant's rows, the data gradients dY W)
+ *     read materialised, zero-padded transposes of their operands -- the
+ *     path the library takes by itself only where a problem's offsets exceed
+ *     the 32-bit ones of its transposed operand loads; 0 = they read the row
+ *     buffers and weights transposed inside the GEMM.  Both issue the same
+ *     MFMA sequence per output element, so results are bitwise identical.
+ * Sec. 5.2 (tenant-private backward of the action modules).  Returns
+ * JN_EINVAL for an unknown option or a value other than 0 / 1; takes effect
+ * for calls enqueued after it. */
+#define JN_OPT_EXPERT_TRANSPOSES 1
+jn_status jn_ctx_set_option(jn_ctx* ctx, int32_t option, int32_t value);
+
 /* ---------------------------------------------------------------- pack --- */
 
 /* One inference / training request of one tenant (App. A.3: a request carries

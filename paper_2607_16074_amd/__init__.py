@@ -71,6 +71,10 @@ class Context:
         """Bracket every kernel this context launches with timing events."""
         _check(_lib.jn_ctx_set_trace(self.handle, 1 if enable else 0), self)
 
+    def set_option(self, option: int, value: int):
+        """jn_ctx_set_option: e.g. ``_abi.JN_OPT_EXPERT_TRANSPOSES``."""
+        _check(_lib.jn_ctx_set_option(self.handle, int(option), int(value)), self)
+
     def trace_read(self, cap: int = 1 << 16) -> list:
         """[(op name, M, N, K, ms)] of the traced launches, in launch order."""
         buf = (_abi.jn_trace_entry * cap)()

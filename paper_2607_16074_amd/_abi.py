@@ -14,12 +14,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("JN_LIB_PATH") or os.path.join(_HERE, "libjoynexus.so")
 
 JN_OK, JN_EINVAL, JN_EINCOMPAT, JN_ESHAPE, JN_ENOSPACE, JN_EHIP, JN_EUNSUPPORTED = range(7)
+JN_OPT_EXPERT_TRANSPOSES = 1  # jn_ctx_set_option: expert gradient GEMMs on materialised transposes
 STATUS_NAMES = {0: "JN_OK", 1: "JN_EINVAL", 2: "JN_EINCOMPAT", 3: "JN_ESHAPE", 4: "JN_ENOSPACE",
                 5: "JN_EHIP", 6: "JN_EUNSUPPORTED"}
 
 EXPORTS = (
     "jn_ctx_create", "jn_ctx_destroy", "jn_ctx_set_stream", "jn_last_error", "jn_ctx_set_trace",
-    "jn_ctx_trace_read",
+    "jn_ctx_trace_read", "jn_ctx_set_option",
     "jn_pack_plan", "jn_pack_maps_host", "jn_pack_group",
     "jn_backbone_workspace_size", "jn_backbone_forward",
     "jn_heads_workspace_size", "jn_tenant_heads_fwd_bwd", "jn_tenant_heads_fwd_bwd_noalloc",
@@ -154,6 +155,7 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "jn_ctx_set_stream": (C.c_int, [V, V]),
         "jn_last_error": (C.c_char_p, [V]),
         "jn_ctx_set_trace": (C.c_int, [V, C.c_int32]),
+        "jn_ctx_set_option": (C.c_int, [V, C.c_int32, C.c_int32]),
         "jn_ctx_trace_read": (C.c_int, [V, P(jn_trace_entry), C.c_int32, P(C.c_int32)]),
         "jn_pack_plan": (C.c_int, [P(jn_request), C.c_int32, P(jn_tenant), C.c_int32, P(jn_pack_opts),
                                    P(jn_pack_sizes)]),

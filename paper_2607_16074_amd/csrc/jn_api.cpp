@@ -94,6 +94,8 @@ struct jn_ctx {
   void* fixed_host = nullptr;
   hipEvent_t fixed_ev = nullptr;
   bool fixed_pending = false;
+  // JN_OPT_EXPERT_TRANSPOSES
+  bool expert_transposes = false;
 };
 
 namespace {
@@ -445,6 +447,15 @@ jn_status jn_ctx_set_trace(jn_ctx* c, int32_t enable) {
   c->recs.clear();
   c->pool_used = 0;
   return JN_OK;
+}
+
+jn_status jn_ctx_set_option(jn_ctx* c, int32_t option, int32_t value) {
+  if (!c) return JN_EINVAL;
+  if (value != 0 && value != 1) return fail(c, JN_EINVAL, "option %d: value %d is not 0 or 1", option, value);
+  switch (option) {
+    case JN_OPT_EXPERT_TRANSPOSES: c->expert_transposes = value != 0; return JN_OK;
+    default: return fail(c, JN_EINVAL, "unknown option %d", option);
+  }
 }
 
 jn_status jn_ctx_trace_read(jn_ctx* c, jn_trace_entry* out, int32_t cap, int32_t* n) {
@@ -1338,7 +1349,7 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
   // (offsets beyond the loop's 32-bit ones) the caller materialises the
   // transposes instead.  Both give the same MFMA sequence per output element.
   auto trans_ok = [&](const std::vector<GemmArgs>& probs) {
-    return gemm_grouped_tile_shape(probs.data(), (int32_t)probs.size()) == 0;
+    return !c->expert_transposes && gemm_grouped_tile_shape(probs.data(), (int32_t)probs.size()) == 0;
   };
   auto per_tenant_gemm = [&](int epi, std::function<GemmArgs(int32_t)> fn) {
     std::vector<GemmArgs> v;

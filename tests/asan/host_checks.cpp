@@ -464,6 +464,13 @@ void check_experts(jn_ctx* c, bool flow) {
   void* w = dev(ws);
   void* hidden = dev((size_t)k.p.T * dp * 2);
   CHECK(jn_tenant_experts_fwd_bwd(c, &k.p, hidden, ex.data(), io.data(), G, w, ws) == JN_OK);
+  // the materialised-transpose path of the gradient GEMMs plans within the same workspace
+  CHECK(jn_ctx_set_option(c, JN_OPT_EXPERT_TRANSPOSES, 1) == JN_OK);
+  CHECK(jn_tenant_experts_fwd_bwd(c, &k.p, hidden, ex.data(), io.data(), G, w, ws) == JN_OK);
+  CHECK(jn_ctx_set_option(c, JN_OPT_EXPERT_TRANSPOSES, 0) == JN_OK);
+  CHECK(jn_ctx_set_option(c, JN_OPT_EXPERT_TRANSPOSES, 2) == JN_EINVAL);
+  CHECK(jn_ctx_set_option(c, 99, 0) == JN_EINVAL);
+  CHECK(jn_ctx_set_option(nullptr, JN_OPT_EXPERT_TRANSPOSES, 0) == JN_EINVAL);
   CHECK(jn_tenant_experts_fwd_bwd(c, &k.p, hidden, ex.data(), io.data(), G, w, ws - 1) == JN_ENOSPACE);
   ex[0].chunk = 65;
   CHECK(jn_tenant_experts_fwd_bwd(c, &k.p, hidden, ex.data(), io.data(), G, w, ws) == JN_EUNSUPPORTED);

@@ -232,6 +232,44 @@ def test_expert_grouped_equals_isolated_bitwise(jn, flow):
                 assert torch.equal(la[name], lb[name]), (g, name)
 
 
+def _expert_outputs_equal(a, b, tag):
+    assert torch.equal(a.pred, b.pred) and torch.equal(a.loss, b.loss), tag
+    assert torch.equal(a.dw_in, b.dw_in) and torch.equal(a.dw_out, b.dw_out) and torch.equal(a.dgf, b.dgf), tag
+    if a.dw_time is not None:
+        assert torch.equal(a.dw_time, b.dw_time), tag
+    for la, lb in zip(a.layers, b.layers):
+        for name in la:
+            assert torch.equal(la[name], lb[name]), (tag, name)
+
+
+@pytest.mark.parametrize("case", ["small", "small-flow", "config4-3"])
+def test_expert_transposed_operands_equal_materialised_transposes(jn, case):
+    """The gradient GEMMs read their operands transposed inside the GEMM
+    (ragged per-tenant K zero-filled by the load's range check); with
+    JN_OPT_EXPERT_TRANSPOSES they read zero-padded transposed copies instead.
+    Both issue the same MFMA sequence per output element: every prediction,
+    loss and gradient must agree bitwise."""
+    from paper_2607_16074_amd import _abi
+    from paper_2607_16074_amd import step as jstep
+    if case == "config4-3":
+        full = W.config_spec(4, 0)
+        order = sorted(range(full.G), key=lambda g: (full.tenants[g].n_samples, g))[:3]
+        spec = dataclasses.replace(full, tenants=tuple(full.tenants[g] for g in order))
+    else:
+        spec = expert_spec((2, 256, 4, 512), 10, [(3, 7), (5, 14), (2, 32)], flow=64 if case == "small-flow" else 0)
+    wl = W.make_workload(spec)
+    _say(f"expert gradients, transposed loads vs materialised transposes: {case}")
+    st, targets, noisy = run_experts(wl)
+    ctx = jn.Context()
+    ctx.set_option(_abi.JN_OPT_EXPERT_TRANSPOSES, 1)
+    model, reqs = st.model, jstep.from_workload(wl)[1]
+    alt = jstep.GroupStep(model, reqs, targets, st.tenants, 1, ctx=ctx, noisy=noisy, flow_t=jstep.flow_times(wl))
+    alt.run()
+    torch.cuda.synchronize()
+    for k, g in enumerate(st.tenants):
+        _expert_outputs_equal(st.ios[k], alt.ios[k], g)
+
+
 def test_expert_errors_enqueue_nothing(jn):
     spec = expert_spec((1, 256, 4, 512), 10, [(2, 7), (2, 14)])
     wl = W.make_workload(spec)
