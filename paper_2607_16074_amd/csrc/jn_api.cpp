@@ -1085,6 +1085,19 @@ namespace {
 constexpr int kAP = 64;
 constexpr int kKP = 64;
 
+// K ranges of an expert weight gradient contracted over K rows (a tenant's
+// action rows or its samples' prefix rows): S = round(K / 6144) ranges, 1..8,
+// of ceil(K / S) rows rounded up to 64 (the last one shorter), their fp32
+// partials added in range order.  A function of K only, so a tenant's
+// gradient bits do not depend on the batch it runs in.  The cross-attention
+// key/value weight gradient contracts over ~12K prefix rows per tenant of the
+// 16-tenant workload, 1.5 waves of 256x256 tiles unsplit.
+constexpr int64_t kWgradRange = 6144;
+int32_t wgrad_splits(int64_t K) {
+  return (int32_t)std::min<int64_t>(8, std::max<int64_t>(1, (K + kWgradRange / 2) / kWgradRange));
+}
+int64_t wgrad_range_rows(int64_t K, int32_t S) { return ((K + S - 1) / S + 63) / 64 * 64; }
+
 struct ExpShape {
   int32_t L, d, H, f, chunk, dp;
   float eps;
@@ -1105,7 +1118,7 @@ struct ExpPlan {
 struct ExpLayout {
   size_t arena = 0, arena_bytes = 0;
   size_t x, xf, yb, ub, vel, predp, dpred, dpredb, z, zoff, winp, woutp, woutpT, dx, dxb, tf, dsum, tb, dkvb, gx, part,
-      TA, TB, WT, dwinp, dwoutp;
+      TA, TB, WT, kpart, dwinp, dwoutp;
   std::vector<size_t> x1, x2, x3, h1, h2, h3, qkv, os, osb, lses, qc, kv, oc, ocb, lsec, pre, mb;
   size_t total = 0;
 };
@@ -1231,6 +1244,18 @@ ExpLayout exp_layout(const ExpPlan& P) {
   Ly.TA = take(2 * std::max<int64_t>(wmax * P.KaT, 2 * d * P.KzT));
   Ly.TB = take(2 * std::max<int64_t>(std::max<int64_t>(wmax, KI) * P.KaT, (int64_t)s.dp * P.KzT));
   Ly.WT = take(2 * G * std::max<int64_t>(f * d, 3 * d * d) + 2 * G * 2 * d * s.dp);
+  {
+    // partials of split weight gradients: action-row ones (any weight shape)
+    // and prefix-row ones (the key/value weights), never live together
+    const int64_t apair = std::max<int64_t>(std::max<int64_t>(f * d, 3 * d * d), std::max<int64_t>(d * KI, kAP * d));
+    int64_t ka = 0, kz = 0;
+    for (int32_t g = 0; g < G; ++g) {
+      const int32_t Sa = wgrad_splits(P.rows[g]), Sz = wgrad_splits(P.Pz[g]);
+      if (Sa > 1) ka += Sa * apair;
+      if (Sz > 1) kz += Sz * 2 * d * s.dp;
+    }
+    Ly.kpart = take(4 * std::max(ka, kz));
+  }
   Ly.dwinp = take(4 * G * d * KI);
   Ly.dwoutp = take(4 * G * kAP * d);
   for (int l = 0; l < s.L; ++l) {
@@ -1370,6 +1395,14 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
     rec.ops.push_back([=](char* a) { return launch_transpose(s, (const TransDesc*)(a + at), n, blocks); });
     rec.opcode.push_back(JN_OP_EXPERT_OTHER);
   };
+  auto ksum = [&](std::vector<KSumDesc> dv) {
+    const int32_t blocks = ksum_prepare(dv.data(), (int32_t)dv.size());
+    if (blocks < 0) rec.bad_gemm = true;
+    const size_t at = rec.add(dv.data(), sizeof(KSumDesc) * dv.size());
+    const int32_t n = (int32_t)dv.size();
+    rec.ops.push_back([=](char* a) { return launch_ksum(s, (const KSumDesc*)(a + at), n, blocks); });
+    rec.opcode.push_back(JN_OP_EXPERT_OTHER);
+  };
   auto ptr_table = [&](std::function<const void*(int32_t)> fn) {
     std::vector<const void*> v(G);
     for (int32_t g = 0; g < G; ++g) v[g] = fn(g);
@@ -1469,52 +1502,59 @@ jn_status jn_tenant_experts_fwd_bwd(jn_ctx* c, const jn_packed* p, const void* h
       return a;
     });
   };
-  // weight-gradient GEMM: C[out][in] = TA_g [out][K_g] . TB_g [in][K_g]^T
-  auto wgrad = [&](int64_t out, int64_t in, std::function<float*(int32_t)> Csel, bool prefix) {
-    per_tenant_gemm(EPI_F32, [&](int32_t g) {
-      GemmArgs a{};
-      const int64_t k0 = prefix ? P.kzoff[g] : P.kaoff[g];
-      const int32_t K = prefix ? P.Kz[g] : P.Ka[g];
-      a.X = B(Ly.TA) + out * k0;
-      a.ldx = K;
-      a.W = B(Ly.TB) + in * k0;
-      a.ldw = K;
-      a.C = Csel(g);
-      a.ldc = in;
-      a.M = (int32_t)out;
-      a.N = (int32_t)in;
-      a.K = K;
-      return a;
-    });
-  };
   // weight gradient C_g[out][in] = dY_g^T X_g over the tenant's rows of two
   // row buffers (dY [rows][out], X [rows][in]; prefix: the tenant's prefix
   // rows), read transposed by the GEMM -- or from zero-padded transposes
+  // (TA_g [out][K_g], TB_g [in][K_g]) -- in the K ranges of wgrad_splits
   auto wgrad_rows = [&](const uint16_t* dy, int64_t out, const uint16_t* xin, int64_t in,
                         std::function<float*(int32_t)> Csel, bool prefix) {
-    std::vector<GemmArgs> v;
+    std::vector<GemmArgs> vt, vm;  // transposed loads / materialised transposes
+    std::vector<KSumDesc> sums;
+    int64_t planes = 0;  // partial planes handed out
     for (int32_t g = 0; g < G; ++g) {
-      GemmArgs a{};
+      const int64_t K = prefix ? P.Pz[g] : P.rows[g];
       const int64_t r0 = prefix ? P.zoff[g] : P.roff[g];
-      a.X = dy + r0 * out;
-      a.ldx = out;
-      a.W = xin + r0 * in;
-      a.ldw = in;
-      a.C = Csel(g);
-      a.ldc = in;
-      a.M = (int32_t)out;
-      a.N = (int32_t)in;
-      a.K = prefix ? (int32_t)P.Pz[g] : P.rows[g];
-      a.trans = GEMM_TRANS_X | GEMM_TRANS_W;
-      v.push_back(a);
+      const int64_t kz0 = prefix ? P.kzoff[g] : P.kaoff[g];
+      const int64_t Kp = prefix ? P.Kz[g] : P.Ka[g];
+      const int32_t S = wgrad_splits(K);
+      const int64_t len = S > 1 ? wgrad_range_rows(K, S) : K;
+      float* part = F(Ly.kpart) + planes * out * in;
+      for (int32_t r = 0; r < S; ++r) {
+        const int64_t k0 = r * len, k1 = r == S - 1 ? K : (r + 1) * len;
+        GemmArgs a{};
+        a.C = S > 1 ? (void*)(part + r * out * in) : (void*)Csel(g);
+        a.ldc = in;
+        a.M = (int32_t)out;
+        a.N = (int32_t)in;
+        a.X = dy + (r0 + k0) * out;
+        a.ldx = out;
+        a.W = xin + (r0 + k0) * in;
+        a.ldw = in;
+        a.K = (int32_t)(k1 - k0);
+        a.trans = GEMM_TRANS_X | GEMM_TRANS_W;
+        vt.push_back(a);
+        GemmArgs m = a;  // columns k0.. of the tenant's [out][Kp] / [in][Kp] transposed blocks
+        m.trans = 0;
+        m.X = B(Ly.TA) + out * kz0 + k0;
+        m.ldx = Kp;
+        m.W = B(Ly.TB) + in * kz0 + k0;
+        m.ldw = Kp;
+        m.K = (int32_t)((r == S - 1 ? Kp : k1) - k0);
+        vm.push_back(m);
+      }
+      if (S > 1) {
+        sums.push_back(KSumDesc{part, Csel(g), out * in, S, 0});
+        planes += S;
+      }
     }
-    if (trans_ok(v)) {
-      gemm(EPI_F32, v);
-      return;
+    if (trans_ok(vt)) {
+      gemm(EPI_F32, vt);
+    } else {
+      trans_rows(dy, out, B(Ly.TA), prefix);
+      trans_rows(xin, in, B(Ly.TB), prefix);
+      gemm(EPI_F32, vm);
     }
-    trans_rows(dy, out, B(Ly.TA), prefix);
-    trans_rows(xin, in, B(Ly.TB), prefix);
-    wgrad(out, in, Csel, prefix);
+    if (!sums.empty()) ksum(sums);
   };
   // data gradient C[rows][in] = epi(dY[rows][out] W_g[out][in]) per tenant,
   // the weight read transposed by the GEMM -- or from a transposed copy

@@ -193,6 +193,19 @@ struct CopyDesc {
   int32_t block_start, vec;  // filled by copy2d_prepare
 };
 int32_t copy2d_prepare(CopyDesc* d, int32_t n);
+
+// dst[i] = ((src[0][i] + src[1][i]) + ...) + src[S-1][i], i < n (parts
+// n elements apart, fp32; n % 4 == 0, 16-byte aligned): the K ranges of a
+// split weight gradient added in range order.
+struct KSumDesc {
+  const float* src;
+  float* dst;
+  int64_t n;
+  int32_t S;
+  int32_t block_start;  // filled by ksum_prepare
+};
+int32_t ksum_prepare(KSumDesc* d, int32_t n);
+hipError_t launch_ksum(hipStream_t s, const KSumDesc* d, int32_t n, int32_t blocks);
 hipError_t launch_copy2d(hipStream_t s, const CopyDesc* d, int32_t n, int32_t blocks);
 
 // bf16 dst[c][r] = src[r][c] (r < rows), 0 for rows <= r < rows_pad; c < cols.

@@ -3,8 +3,10 @@
 // holds the rest:
 //   copy2d       grouped strided 2-D copy with zero padding and fp32 <-> bf16
 //                conversion (operand padding, bf16 rounding points, saves)
+//   ksum         ordered sum of the K-range partials of a split weight gradient
 //   transpose    grouped bf16 transpose with zero-padded columns (operands of
-//                the data- and weight-gradient GEMMs)
+//                the data- and weight-gradient GEMMs where they cannot be read
+//                transposed in place)
 //   prefix       tenant-ordered copy of every sample's valid backbone rows
 //   rmsnorm      per-tenant-gain RMSNorm forward (fp32 -> bf16) and backward
 //                (fp32), gain gradients by fixed-order column sums
@@ -102,6 +104,48 @@ int32_t copy2d_prepare(CopyDesc* d, int32_t n) {
 hipError_t launch_copy2d(hipStream_t s, const CopyDesc* d, int32_t n, int32_t blocks) {
   if (blocks <= 0) return hipSuccess;
   copy2d_kernel<<<blocks, 256, 0, s>>>(d, n);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ ksum ---
+// One block per 4096 elements of a descriptor (a thread sums 4 x 4 columns).
+__global__ __launch_bounds__(256) void ksum_kernel(const KSumDesc* __restrict__ descs, int32_t ndesc) {
+  const int32_t b = blockIdx.x;
+  int32_t i = 0;
+  while (i + 1 < ndesc && descs[i + 1].block_start <= b) ++i;
+  const KSumDesc D = descs[i];
+  const int64_t base = (int64_t)(b - D.block_start) * 4096;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t e = base + ((int64_t)k * 256 + threadIdx.x) * 4;
+    if (e >= D.n) break;
+    float4 acc = *reinterpret_cast<const float4*>(D.src + e);
+    for (int32_t r = 1; r < D.S; ++r) {
+      const float4 v = *reinterpret_cast<const float4*>(D.src + r * D.n + e);
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    *reinterpret_cast<float4*>(D.dst + e) = acc;
+  }
+}
+
+int32_t ksum_prepare(KSumDesc* d, int32_t n) {
+  int32_t total = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (d[i].n <= 0 || d[i].n % 4 != 0 || d[i].S < 1 || reinterpret_cast<uintptr_t>(d[i].src) % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(d[i].dst) % 16 != 0)
+      return -1;
+    d[i].block_start = total;
+    total += (int32_t)((d[i].n + 4095) / 4096);
+  }
+  return total;
+}
+
+hipError_t launch_ksum(hipStream_t s, const KSumDesc* d, int32_t n, int32_t blocks) {
+  if (blocks <= 0 || n <= 0) return hipSuccess;
+  ksum_kernel<<<blocks, 256, 0, s>>>(d, n);
   return hipGetLastError();
 }
 

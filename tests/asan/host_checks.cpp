@@ -10,6 +10,7 @@
 // ASan against the buffer it belongs to, through every entry point and its
 // error paths.  Test infrastructure only.  Prints "host checks ok" at the end.
 #include <cstdint>
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -82,6 +83,26 @@ Group make_group(Rng& r, int G, int d, int max_reqs_per_tenant, int max_n, int m
     g.req.push_back(q);
   }
   for (size_t i = 0; i < g.req.size(); ++i) g.req[i].lengths = g.lens[i].data();
+  return g;
+}
+
+// G tenants, one request each of n samples of exactly len rows.
+Group long_group(int d, int G, int n, int len) {
+  Group g;
+  g.opts.d_model = d;
+  g.opts.align = 1;
+  g.ten.assign(G, jn_tenant{0x1234, d, 0});
+  g.lens.resize(G);
+  for (int t = 0; t < G; ++t) {
+    jn_request q{};
+    q.tenant = t;
+    q.n_samples = n;
+    q.max_len = len;
+    g.lens[t].assign(n, len);
+    q.embeds = dev((size_t)n * len * d * 2);
+    g.req.push_back(q);
+  }
+  for (int t = 0; t < G; ++t) g.req[t].lengths = g.lens[t].data();
   return g;
 }
 
@@ -385,16 +406,23 @@ void check_heads(jn_ctx* c) {
 
 // ------------------------------------------------------------ experts ---
 
-void check_experts(jn_ctx* c, bool flow) {
+void check_experts(jn_ctx* c, bool flow, bool long_prefix = false) {
   Rng r(flow ? 6 : 5);
   const int dp = 128, d = 256, H = 4, f = 512, L = 2, chunk = 10, dt = 64;
-  Group g = make_group(r, 3, dp, 2, 4, 40, 16);
+  // long prefixes: tenants with over 9K prefix rows, whose key/value weight
+  // gradients run split into K ranges
+  Group g = long_prefix ? long_group(dp, 3, 8, 1500) : make_group(r, 3, dp, 2, 4, 40, 16);
   Packed k = pack(c, g);
   const int G = 3;
   std::vector<int32_t> ns(G);
   std::vector<int64_t> rows(G);
   CHECK(jn_pack_tenant_sizes(g.req.data(), (int)g.req.size(), g.ten.data(), G, &g.opts, ns.data(), rows.data()) ==
         JN_OK);
+  if (long_prefix) {
+    int64_t most = 0;
+    for (int t = 0; t < G; ++t) most = std::max(most, rows[t]);
+    CHECK(most >= 9216);  // at least one tenant's prefix gradient is split
+  }
   std::vector<jn_expert> ex(G);
   std::vector<jn_expert_io> io(G);
   std::vector<std::vector<jn_expert_layer>> xl(G);
@@ -556,6 +584,7 @@ int main() {
   check_heads(c);
   check_experts(c, false);
   check_experts(c, true);
+  check_experts(c, false, true);
   check_adamw(c);
   int stream_token = 0;
   check_infer(c, &stream_token);
