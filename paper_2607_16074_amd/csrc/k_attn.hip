@@ -99,6 +99,7 @@ struct AttnShape {
   int32_t group;    // query heads per key/value head
   int32_t qtiles;   // 128-query tiles per sample (of the longest sample)
   int32_t total;    // (sample, key/value head) groups
+  int32_t nblocks;  // work-item slots (blocks of the one-item-per-workgroup mapping)
   float scale_log2;
 };
 
@@ -347,6 +348,16 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
 // 15-23% faster on 300-3000-token samples; at head width 128 the same layout
 // was no faster on 300-token samples and 9% slower on 1000-token ones, so
 // that width keeps attn_fwd_kernel.
+// Its 128 KB of K/V stages leave room for one workgroup per compute unit, so
+// a workgroup that fetched its Q rows and first stage only after starting
+// left the compute unit idle for that fetch, and between workgroups: timer
+// stamps on the 2B-shaped batch put ~13K of a work item's ~38K cycles
+// outside the key loop.  The grid is therefore one workgroup per compute
+// unit, each running a fixed list of work items, with the next item's first
+// K/V stage and Q rows fetched under the current item's last key step
+// (8.1 -> 7.1 ms per 18-layer step).  The output is written 16 bytes per
+// lane after a lane swap (8.1 -> 6.5 ms with both).  The work of an item,
+// hence every output bit, is unchanged.
 //   S^T = K Q^T: A = K (16 keys x 32 dims), B = Q (32 dims x 16 queries);
 //     lane l holds query l % 16 and keys 4 (l / 16) .. +3 of each 16-key block.
 //   O^T += V^T P^T over a 32-key chunk (blocks 2c, 2c+1): B slot 8 q + e of
@@ -371,39 +382,53 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
   static_assert(NDMA % NW == 0, "tile shape");
   __shared__ __attribute__((aligned(1024))) uint16_t lds[2][2 * TILE];
 
-  // work mapping as in attn_fwd_kernel
-  const int32_t b = blockIdx.x;
-  const int32_t slot = b >> 3;
-  const int32_t units = sh.group * sh.qtiles;
-  const int32_t kg = (slot / units) * 8 + (b & 7);
-  if (kg >= sh.total) return;
-  const int32_t r_in = slot % units;
-  const int32_t qt = r_in % sh.qtiles;
-  const int32_t i = kg / sh.n_kv, kvh = kg % sh.n_kv;
-  const int32_t h = kvh * sh.group + r_in / sh.qtiles;
-  const int32_t d = sh.d;
-  const int32_t L = seqlens[i];
-  const int32_t base = cu_seqlens[i];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-
-  if (qt == 0) {  // alignment rows of this sample: zero output
-    const int32_t pad = cu_seqlens[i + 1] - base - L;
-    for (int32_t e = tid; e < pad * (HD / 8); e += 512) {
-      const int32_t row = base + L + e / (HD / 8);
-      *reinterpret_cast<uint4*>(out + (int64_t)row * d + h * HD + (e % (HD / 8)) * 8) = make_uint4(0, 0, 0, 0);
-    }
-  }
-  const int32_t q0 = qt * kQRows;
-  if (q0 >= L) return;
-
+  const int j16 = lane & 15, quad = lane >> 4;
+  const int32_t d = sh.d;
   const int64_t ld = sh.ld;
   const float scale_log2 = sh.scale_log2;
-  const uint16_t* Qg = qkv + h * HD;
-  const uint16_t* Kg = qkv + sh.kv_col + kvh * HD;
-  const uint16_t* Vg = qkv + sh.v_col + kvh * HD;
+  const int32_t units = sh.group * sh.qtiles;
 
-  auto issue_stage = [&](int32_t kb, int stage) {
+  // A workgroup runs the work items of blocks blockIdx.x, + gridDim.x, ...
+  // (block b: the mapping of attn_fwd_kernel, so b % 8 still names the XCD
+  // when gridDim.x % 8 == 0).  The first K/V stage and the Q rows of the
+  // next item are fetched under the last key step of the current one.
+  struct Item {
+    int32_t h, kvh, L, base, q0, nsteps;
+  };
+  auto decode = [&](int32_t b, Item& it) -> bool {  // false: the block has no work
+    const int32_t slot = b >> 3;
+    const int32_t kg = (slot / units) * 8 + (b & 7);
+    if (kg >= sh.total) return false;
+    const int32_t r_in = slot % units;
+    const int32_t qt = r_in % sh.qtiles;
+    const int32_t i = kg / sh.n_kv;
+    it.kvh = kg % sh.n_kv;
+    it.h = it.kvh * sh.group + r_in / sh.qtiles;
+    it.L = seqlens[i];
+    it.base = cu_seqlens[i];
+    if (qt == 0) {  // alignment rows of this sample: zero output
+      const int32_t pad = cu_seqlens[i + 1] - it.base - it.L;
+      for (int32_t e = tid; e < pad * (HD / 8); e += 512) {
+        const int32_t row = it.base + it.L + e / (HD / 8);
+        *reinterpret_cast<uint4*>(out + (int64_t)row * d + it.h * HD + (e % (HD / 8)) * 8) = make_uint4(0, 0, 0, 0);
+      }
+    }
+    it.q0 = qt * kQRows;
+    if (it.q0 >= it.L) return false;
+    const int32_t kend = CAUSAL ? min(it.L, it.q0 + kQRows) : it.L;
+    it.nsteps = (kend + KB - 1) / KB;
+    return true;
+  };
+  auto next_item = [&](int32_t b, Item& it) -> int32_t {  // first block >= b (same residue) with work
+    for (; b < sh.nblocks; b += gridDim.x)
+      if (decode(b, it)) return b;
+    return sh.nblocks;
+  };
+  auto issue_stage = [&](const Item& it, int32_t kb, int stage) {
+    const uint16_t* Kg = qkv + sh.kv_col + it.kvh * HD;
+    const uint16_t* Vg = qkv + sh.v_col + it.kvh * HD;
 #pragma unroll
     for (int k = 0; k < DPW; ++k) {
       const int u = wave * DPW + k;
@@ -411,20 +436,24 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
       const int v = isv ? u - NDMA / 2 : u;
       const int r = v * RPI + lane / CPR;
       const int c = (lane % CPR) ^ attn_swz<HD>(r);
-      const int32_t key = min(kb + r, L - 1);
-      const uint16_t* src = (isv ? Vg : Kg) + (int64_t)(base + key) * ld + c * 8;
+      const int32_t key = min(kb + r, it.L - 1);
+      const uint16_t* src = (isv ? Vg : Kg) + (int64_t)(it.base + key) * ld + c * 8;
       __builtin_amdgcn_global_load_lds(JN_GPTR(src), JN_LPTR(&lds[stage][u * 512]), 16, 0, 0);
     }
   };
-
-  const int32_t qw = q0 + wave * 16;  // this wave's first query row
-  const bool active = qw < L;
-  const int j16 = lane & 15, quad = lane >> 4;
-  const int32_t qrow = min(qw + j16, L - 1);
   bf16x8 qf[NQC];
+  auto load_q = [&](const Item& it) {
+    const int32_t qrow = min(it.q0 + wave * 16 + j16, it.L - 1);
+    const uint16_t* Qg = qkv + it.h * HD + (int64_t)(it.base + qrow) * ld + quad * 8;
 #pragma unroll
-  for (int c = 0; c < NQC; ++c)
-    qf[c] = *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(base + qrow) * ld + c * 32 + quad * 8);
+    for (int c = 0; c < NQC; ++c) qf[c] = *reinterpret_cast<const bf16x8*>(Qg + c * 32);
+  };
+
+  Item cur, nxt;
+  int32_t b = next_item(blockIdx.x, cur);
+  if (b >= sh.nblocks) return;
+  load_q(cur);
+  issue_stage(cur, 0, 0);
 
   // K fragment of 16-key block kb16, dim chunk c: row 16 kb16 + j16, logical
   // 16-byte chunk 4 c + quad; rows 16 kb16 + j share the swizzle of row j
@@ -435,134 +464,172 @@ __global__ __launch_bounds__(512, 1) void attn16_fwd_kernel(const uint16_t* __re
   const int vrow = 4 * quad + (j16 >> 2);
   const int vswz = attn_swz<HD>(vrow);
 
-  f32x4 o[NOT];
+  int par = 0;  // buffer of the current item's first step
+  while (true) {
+    const int32_t qw = cur.q0 + wave * 16;  // this wave's first query row
+    const bool active = qw < cur.L;
+    f32x4 o[NOT];
 #pragma unroll
-  for (int t = 0; t < NOT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int t = 0; t < NOT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+    int32_t bn = sh.nblocks;  // next block with work, found in the last step
+    for (int32_t jstep = 0; jstep < cur.nsteps; ++jstep) {
+      const int32_t kb = jstep * KB;
+      const int stage = (par + jstep) & 1;
+      attn_wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();  // step j's tiles landed; step j-1's buffer is free
+      const bool last = jstep + 1 == cur.nsteps;
+      if (!last) {
+        issue_stage(cur, kb + KB, stage ^ 1);
+      } else {
+        bn = next_item(b + gridDim.x, nxt);
+        if (bn < sh.nblocks) issue_stage(nxt, 0, stage ^ 1);
+      }
+      // every key of the step later than the wave's queries: nothing to do
+      const bool work = active && !(CAUSAL && kb > qw + 15);
+      const uint16_t* Ks = &lds[stage][0];
+      const uint16_t* Vs = &lds[stage][TILE];
 
-  issue_stage(0, 0);
-  const int32_t kend = CAUSAL ? min(L, q0 + kQRows) : L;
-  const int32_t nsteps = (kend + KB - 1) / KB;
-  for (int32_t jstep = 0; jstep < nsteps; ++jstep) {
-    const int32_t kb = jstep * KB;
-    attn_wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();  // step j's tiles landed; step j-1's buffer is free
-    if (jstep + 1 < nsteps) issue_stage(kb + KB, (jstep + 1) & 1);
-    if (!active) continue;
-    if (CAUSAL && kb > qw + 15) continue;  // every key of the step is later than the wave's queries
-    const uint16_t* Ks = &lds[jstep & 1][0];
-    const uint16_t* Vs = &lds[jstep & 1][TILE];
-
-    // scores: dim chunk c outer, so the four 16-key blocks' accumulators
-    // alternate; the K fragments of chunk c+1 are read before the MFMAs of
-    // chunk c (each accumulator still sums c = 0..NQC-1 in order)
-    f32x4 s[4];
-    bf16x8 kf[2][4];
+      // scores: dim chunk c outer, so the four 16-key blocks' accumulators
+      // alternate; the K fragments of chunk c+1 are read before the MFMAs of
+      // chunk c (each accumulator still sums c = 0..NQC-1 in order)
+      f32x4 s[4];
+      if (work) {
+        bf16x8 kf[2][4];
 #pragma unroll
-    for (int kb16 = 0; kb16 < 4; ++kb16) {
-      s[kb16] = f32x4{0.f, 0.f, 0.f, 0.f};
-      kf[0][kb16] = *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + ((quad ^ kswz) * 8));
-    }
+        for (int kb16 = 0; kb16 < 4; ++kb16) {
+          s[kb16] = f32x4{0.f, 0.f, 0.f, 0.f};
+          kf[0][kb16] = *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + ((quad ^ kswz) * 8));
+        }
 #pragma unroll
-    for (int c = 0; c < NQC; ++c) {
-      if (c + 1 < NQC) {
+        for (int c = 0; c < NQC; ++c) {
+          if (c + 1 < NQC) {
+#pragma unroll
+            for (int kb16 = 0; kb16 < 4; ++kb16)
+              kf[(c + 1) & 1][kb16] = *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD +
+                                                                       (((4 * (c + 1) + quad) ^ kswz) * 8));
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int kb16 = 0; kb16 < 4; ++kb16)
+            s[kb16] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c & 1][kb16], qf[c], s[kb16], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      if (last && bn < sh.nblocks) load_q(nxt);  // Q is not read again in this item
+      if (!work) continue;
+      // online softmax (see attn_fwd_kernel); the four lanes of a query are
+      // lane ^ 16 and lane ^ 32 apart
+      float mloc = -INFINITY;
+      if (kb + KB > cur.L || (CAUSAL && kb + KB - 1 > qw)) {
+        const int32_t qlane = qw + j16;
 #pragma unroll
         for (int kb16 = 0; kb16 < 4; ++kb16)
-          kf[(c + 1) & 1][kb16] =
-              *reinterpret_cast<const bf16x8*>(Ks + (kb16 * 16 + j16) * HD + (((4 * (c + 1) + quad) ^ kswz) * 8));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int32_t key = kb + kb16 * 16 + quad * 4 + e;
+            if (key >= cur.L || (CAUSAL && key > qlane)) s[kb16][e] = -INFINITY;
+          }
       }
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int kb16 = 0; kb16 < 4; ++kb16)
-        s[kb16] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c & 1][kb16], qf[c], s[kb16], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // online softmax (see attn_fwd_kernel); the four lanes of a query are
-    // lane ^ 16 and lane ^ 32 apart
-    float mloc = -INFINITY;
-    if (kb + KB > L || (CAUSAL && kb + KB - 1 > qw)) {
-      const int32_t qlane = qw + j16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, s[kb16][e]);
+      mloc = max_xor32(max_xor16(mloc)) * scale_log2;
+      if (__any(mloc > m_run + kRescale)) {
+        const float m_new = fmaxf(m_run, mloc);
+        if (__all(m_run == -INFINITY)) {
+          m_run = m_new;  // first update: O and l are still zero
+        } else {
+          const float alpha = exp2f(m_run - m_new);
+          l_run *= alpha;
+          m_run = m_new;
+#pragma unroll
+          for (int t = 0; t < NOT; ++t) o[t] *= alpha;
+        }
+      }
+      float lsum = 0.f;
 #pragma unroll
       for (int kb16 = 0; kb16 < 4; ++kb16)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int32_t key = kb + kb16 * 16 + quad * 4 + e;
-          if (key >= L || (CAUSAL && key > qlane)) s[kb16][e] = -INFINITY;
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb16][e], scale_log2, -m_run));
+          s[kb16][e] = p;
+          lsum += p;
         }
-    }
-#pragma unroll
-    for (int kb16 = 0; kb16 < 4; ++kb16)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) mloc = fmaxf(mloc, s[kb16][e]);
-    mloc = max_xor32(max_xor16(mloc)) * scale_log2;
-    if (__any(mloc > m_run + kRescale)) {
-      const float m_new = fmaxf(m_run, mloc);
-      if (__all(m_run == -INFINITY)) {
-        m_run = m_new;  // first update: O and l are still zero
-      } else {
-        const float alpha = exp2f(m_run - m_new);
-        l_run *= alpha;
-        m_run = m_new;
-#pragma unroll
-        for (int t = 0; t < NOT; ++t) o[t] *= alpha;
-      }
-    }
-    float lsum = 0.f;
-#pragma unroll
-    for (int kb16 = 0; kb16 < 4; ++kb16)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb16][e], scale_log2, -m_run));
-        s[kb16][e] = p;
-        lsum += p;
-      }
-    lsum = sum_xor32(sum_xor16(lsum));
-    l_run += lsum;
+      lsum = sum_xor32(sum_xor16(lsum));
+      l_run += lsum;
 
-    bf16x8 pf[2];
+      bf16x8 pf[2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pf[c][e] = (__bf16)s[2 * c][e];
-        pf[c][4 + e] = (__bf16)s[2 * c + 1][e];
+        for (int e = 0; e < 4; ++e) {
+          pf[c][e] = (__bf16)s[2 * c][e];
+          pf[c][4 + e] = (__bf16)s[2 * c + 1][e];
+        }
+      // P.V: the V^T fragments of head-dim block t+2 are read before the
+      // MFMAs of block t
+      auto read_v = [&](int t, bf16x8 (&vf)[2]) {
+        const int col = t * 16 + 4 * (j16 & 3);
+        const int pos = (((col >> 3) ^ vswz) * 8) + (col & 7);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int r0 = c * 32 + vrow;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4*)(Vs + r0 * HD + pos));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4*)(Vs + (r0 + 16) * HD + pos));
+          vf[c] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+      };
+      bf16x8 vb[2][2];
+      read_v(0, vb[0]);
+#pragma unroll
+      for (int t = 0; t < NOT; ++t) {
+        if (t + 1 < NOT) read_v(t + 1, vb[(t + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[t & 1][c], pf[c], o[t], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-    // P.V: the V^T fragments of head-dim block t+2 are read before the
-    // MFMAs of block t
-    auto read_v = [&](int t, bf16x8 (&vf)[2]) {
-      const int col = t * 16 + 4 * (j16 & 3);
-      const int pos = (((col >> 3) ^ vswz) * 8) + (col & 7);
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const int r0 = c * 32 + vrow;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4*)(Vs + r0 * HD + pos));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4*)(Vs + (r0 + 16) * HD + pos));
-        vf[c] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
-    };
-    bf16x8 vb[2][2];
-    read_v(0, vb[0]);
-#pragma unroll
-    for (int t = 0; t < NOT; ++t) {
-      if (t + 1 < NOT) read_v(t + 1, vb[(t + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int c = 0; c < 2; ++c) o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[t & 1][c], pf[c], o[t], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
     }
+
+    if (active) {
+      // lane (j16, quad) holds head-dim columns 16 t + 4 quad .. +3 of query
+      // j16; swapping the packed blocks t+1 of quads 0, 2 with the blocks t
+      // of quads 1, 3 leaves each lane 8 consecutive columns: 16 t (quad 0),
+      // 16 t + 16 (1), 16 t + 8 (2), 16 t + 24 (3), one 16-byte store each
+      const int32_t q = qw + j16;
+      const float inv = 1.0f / l_run;
+      uint16_t* orow = out + (int64_t)(cur.base + q) * d + cur.h * HD + 16 * (quad & 1) + 8 * (quad >> 1);
+#pragma unroll
+      for (int t = 0; t < NOT; t += 2) {
+        const auto a = __builtin_amdgcn_permlane16_swap(pack_bf2(o[t][0] * inv, o[t][1] * inv),
+                                                        pack_bf2(o[t + 1][0] * inv, o[t + 1][1] * inv), false, false);
+        const auto c = __builtin_amdgcn_permlane16_swap(pack_bf2(o[t][2] * inv, o[t][3] * inv),
+                                                        pack_bf2(o[t + 1][2] * inv, o[t + 1][3] * inv), false, false);
+        if (q < cur.L) *reinterpret_cast<uint4*>(orow + t * 16) = make_uint4(a[0], c[0], a[1], c[1]);
+      }
+    }
+    if (bn >= sh.nblocks) break;
+    par = (par + cur.nsteps) & 1;
+    cur = nxt;
+    b = bn;
   }
+}
 
-  if (!active) return;
-  const int32_t q = qw + j16;
-  if (q >= L) return;
-  const float inv = 1.0f / l_run;
-  uint16_t* orow = out + (int64_t)(base + q) * d + h * HD + quad * 4;
-#pragma unroll
-  for (int t = 0; t < NOT; ++t)
-    *reinterpret_cast<uint2*>(orow + t * 16) =
-        make_uint2(pack_bf2(o[t][0] * inv, o[t][1] * inv), pack_bf2(o[t][2] * inv, o[t][3] * inv));
+// compute units of the current device (cached per device)
+static int attn_compute_units() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cached[dev] = n;
+  }
+  return cached[dev];
 }
 
 hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int32_t* seqlens,
@@ -584,8 +651,14 @@ hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int
   const int64_t blocks = (total + 7) / 8 * 8 * sh.group * sh.qtiles;
   if (total <= 0 || blocks > (1LL << 30)) return hipErrorInvalidValue;
   sh.total = (int32_t)total;
+  sh.nblocks = (int32_t)blocks;
   sh.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   const dim3 grid((unsigned)blocks);
+  // head width 256: one workgroup per compute unit (its LDS and registers
+  // allow no second), each running every gridDim.x-th block
+  int cus = attn_compute_units();
+  cus -= cus % 8;
+  const dim3 grid16((unsigned)(cus >= 8 && blocks > cus ? cus : blocks));
   auto Q = reinterpret_cast<const uint16_t*>(qkv);
   auto O = reinterpret_cast<uint16_t*>(out);
 #define JN_ATTN(HDV)                                                                        \
@@ -598,9 +671,9 @@ hipError_t launch_attention(hipStream_t s, const void* qkv, void* out, const int
 #define JN_ATTN16(HDV)                                                                          \
   case HDV:                                                                                     \
     if (causal)                                                                                 \
-      attn16_fwd_kernel<HDV, true><<<grid, 512, 0, s>>>(Q, O, seqlens, cu_seqlens, sh);        \
+      attn16_fwd_kernel<HDV, true><<<grid16, 512, 0, s>>>(Q, O, seqlens, cu_seqlens, sh);        \
     else                                                                                        \
-      attn16_fwd_kernel<HDV, false><<<grid, 512, 0, s>>>(Q, O, seqlens, cu_seqlens, sh);       \
+      attn16_fwd_kernel<HDV, false><<<grid16, 512, 0, s>>>(Q, O, seqlens, cu_seqlens, sh);       \
     break;
   switch (hd) {
     JN_ATTN(32)

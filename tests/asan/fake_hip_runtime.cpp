@@ -69,6 +69,10 @@ hipError_t hipGetDevice(int* dev) {
   *dev = 0;
   return hipSuccess;
 }
+hipError_t hipDeviceGetAttribute(int* value, hipDeviceAttribute_t attr, int) {
+  *value = attr == hipDeviceAttributeMultiprocessorCount ? 256 : 0;  // MI355X
+  return hipSuccess;
+}
 hipError_t hipGetLastError(void) { return hipSuccess; }
 const char* hipGetErrorString(hipError_t) { return "fake runtime error"; }
 
