@@ -69,6 +69,7 @@ struct GemmArgs {
   int32_t trans;        // GEMM_TRANS_* bits (grouped launches on 256x256 tiles only)
   int64_t split_c;      // split-K: elements between the fp32 partial outputs of
                         // consecutive K ranges (blockIdx.y); 0 when unsplit
+  int32_t xcd_ranges;   // split-K ring launches: K ranges dealt to XCD groups (set by the launcher)
 };
 
 // Grouped launch over nprob problems sharing one epilogue: the host fills

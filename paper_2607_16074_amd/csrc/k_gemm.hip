@@ -344,10 +344,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int32_t pid, uint16
   gemm_epilogue<BN, BM, WGN, WGM, EPI>(g, acc, tm, tn, wn, wm, lane);
 }
 
-// Split-K: K range blockIdx.y of a launch whose g.K is the per-range length.
-__device__ __forceinline__ GemmArgs split_range(const GemmArgs& g) {
+// Split-K: K range s of a launch whose g.K is the per-range length.
+__device__ __forceinline__ GemmArgs split_range(const GemmArgs& g, int32_t s) {
   GemmArgs r = g;
-  const int32_t s = blockIdx.y;
   if (s) {
     r.X += (int64_t)s * g.K;
     r.W += (int64_t)s * g.K;
@@ -359,7 +358,7 @@ __device__ __forceinline__ GemmArgs split_range(const GemmArgs& g) {
 template <int BN, int BM, int WGN, int WGM, int EPI>
 __global__ __launch_bounds__(64 * WGN * WGM, 1) void gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds[kStages * (BN + BM) * kBK];
-  gemm_tile<BN, BM, WGN, WGM, EPI>(split_range(g), blockIdx.x, lds);
+  gemm_tile<BN, BM, WGN, WGM, EPI>(split_range(g, blockIdx.y), blockIdx.x, lds);
 }
 
 // Sum of the split-K partials in range order, then the epilogue.  Thread =
@@ -702,11 +701,28 @@ __device__ __forceinline__ void ring_tile(const GemmArgs& g, int32_t pid, uint16
 }
 
 // One launch of ring tiles over g (split-K ranges from blockIdx.y as in
-// gemm_kernel).
+// gemm_kernel).  With g.xcd_ranges (S = gridDim.y ranges, S | 8, at most
+// kGroupM token tiles, 8 / S | tiles_n) workgroup b + gridDim.x y, which the
+// hardware places on XCD x = (b + gridDim.x y) % 8, takes K range
+// x / (8 / S) and, of that range, the tiles of one block of tiles_n / (8 / S)
+// weight tiles over all token tiles.  In the grouped walk every XCD held one
+// token tile over all K ranges and all weight tiles, so each of the 8 L2s
+// fetched the whole weight matrix; now an XCD fetches one range's token rows
+// and a 1/(8/S) share of that range's weight columns.  Which workgroup
+// computes a (range, tile) changes nothing else.
 template <int EPI>
 __global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g0) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds[5 * 256 * kBK];
-  ring_tile<EPI, 0>(split_range(g0), blockIdx.x, lds);
+  int32_t pid = blockIdx.x, s = blockIdx.y;
+  if (g0.xcd_ranges) {
+    const int32_t lin = blockIdx.x + blockIdx.y * gridDim.x;
+    const int32_t x = lin & 7, slot = lin >> 3, nx = 8 / gridDim.y;
+    s = x / nx;
+    const int32_t tm = slot % g0.tiles_m;
+    const int32_t tn = (x % nx) * (g0.tiles_n / nx) + slot / g0.tiles_m;
+    pid = tn * g0.tiles_m + tm;  // tile_of's inverse for tiles_m <= kGroupM
+  }
+  ring_tile<EPI, 0>(split_range(g0, s), pid, lds);
 }
 
 // Grouped ring tiles: problem p owns tiles [tile_start, tile_start + tiles).
@@ -733,6 +749,7 @@ static hipError_t launch_ring(hipStream_t s, int epi, GemmArgs g, int32_t splits
   g.tiles_m = (g.M + 255) / 256;
   g.tiles_n = (NL + 255) / 256;
   g.tile_start = 0;
+  g.xcd_ranges = splits > 1 && 8 % splits == 0 && g.tiles_m <= kGroupM && g.tiles_n % (8 / splits) == 0;
   const dim3 grid(g.tiles_m * g.tiles_n, splits), block(256);
   switch (epi) {
     case EPI_BF16: gemm_ring_kernel<EPI_BF16><<<grid, block, 0, s>>>(g); break;
