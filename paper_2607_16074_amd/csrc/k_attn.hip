@@ -323,25 +323,39 @@ __global__ __launch_bounds__(256, (HD >= 256 && KB >= 64) ? 1 : 2) void attn_fwd
   }
 
   if (!active) return;
-  // lane (query l % 32, half l / 32) holds head-dim columns 32 t + 8 rr +
-  // 4 (l / 32) .. +3; swapping the packed blocks rr+1 of the low half with
-  // the blocks rr of the high half (rr even) leaves each lane 8 consecutive
-  // columns, 32 t + 8 rr + 8 (l / 32), for one 16-byte store
   const int32_t q = qw + (lane & 31);
-  const float inv = 1.0f / l_run;
-  uint16_t* orow = out + (int64_t)(base + q) * d + h * HD + 2 * hi4;
+  if constexpr (HD <= 64) {
+    const float inv = 1.0f / l_run;
+    // lane (query l % 32, half l / 32) holds head-dim columns 32 t + 8 rr +
+    // 4 (l / 32) .. +3; swapping the packed blocks rr+1 of the low half with
+    // the blocks rr of the high half (rr even) leaves each lane 8 consecutive
+    // columns, 32 t + 8 rr + 8 (l / 32), for one 16-byte store (at head width
+    // 128 the causal kernel then spilled registers, so it keeps 8-byte stores)
+    uint16_t* orow = out + (int64_t)(base + q) * d + h * HD + 2 * hi4;
 #pragma unroll
-  for (int t = 0; t < NOT; ++t)
+    for (int t = 0; t < NOT; ++t)
 #pragma unroll
-    for (int rr = 0; rr < 4; rr += 2) {
-      const auto a = __builtin_amdgcn_permlane32_swap(pack_bf2(o[t][rr * 4] * inv, o[t][rr * 4 + 1] * inv),
-                                                      pack_bf2(o[t][rr * 4 + 4] * inv, o[t][rr * 4 + 5] * inv), false,
-                                                      false);
-      const auto c = __builtin_amdgcn_permlane32_swap(pack_bf2(o[t][rr * 4 + 2] * inv, o[t][rr * 4 + 3] * inv),
-                                                      pack_bf2(o[t][rr * 4 + 6] * inv, o[t][rr * 4 + 7] * inv), false,
-                                                      false);
-      if (q < L) *reinterpret_cast<uint4*>(orow + t * 32 + rr * 8) = make_uint4(a[0], c[0], a[1], c[1]);
-    }
+      for (int rr = 0; rr < 4; rr += 2) {
+        const auto a = __builtin_amdgcn_permlane32_swap(pack_bf2(o[t][rr * 4] * inv, o[t][rr * 4 + 1] * inv),
+                                                        pack_bf2(o[t][rr * 4 + 4] * inv, o[t][rr * 4 + 5] * inv),
+                                                        false, false);
+        const auto c = __builtin_amdgcn_permlane32_swap(pack_bf2(o[t][rr * 4 + 2] * inv, o[t][rr * 4 + 3] * inv),
+                                                        pack_bf2(o[t][rr * 4 + 6] * inv, o[t][rr * 4 + 7] * inv),
+                                                        false, false);
+        if (q < L) *reinterpret_cast<uint4*>(orow + t * 32 + rr * 8) = make_uint4(a[0], c[0], a[1], c[1]);
+      }
+  } else {
+    if (q >= L) return;
+    const float inv = 1.0f / l_run;
+    uint16_t* orow = out + (int64_t)(base + q) * d + h * HD;
+#pragma unroll
+    for (int t = 0; t < NOT; ++t)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+        *reinterpret_cast<uint2*>(orow + t * 32 + rr * 8 + hi4) =
+            make_uint2(pack_bf2(o[t][rr * 4] * inv, o[t][rr * 4 + 1] * inv),
+                       pack_bf2(o[t][rr * 4 + 2] * inv, o[t][rr * 4 + 3] * inv));
+  }
 }
 
 
