@@ -132,6 +132,35 @@ def test_variant_wide_and_long(jn, case):
     _say(f"  hidden max-rel {worst:.3e}")
 
 
+MANY_ITEMS = [(1, False), (2, True)]  # kv heads, causal (d 512, 2 query heads of width 256)
+
+
+@pytest.mark.parametrize("case", MANY_ITEMS, ids=[f"kv{c[0]}{'c' if c[1] else 'b'}" for c in MANY_ITEMS])
+def test_attention_hd256_many_items_per_workgroup(jn, case):
+    """Head width 256 with more (sample, head, query tile) work items than
+    compute units, so each persistent workgroup runs several items and
+    fetches the next one's first K/V stage and Q rows under the current
+    item's last key step; ragged lengths 1 .. 400 (one to four query tiles,
+    one to seven key steps) and 16-row alignment, whose padding rows are
+    zeroed by the items decoded in the middle of another item.  Every sample
+    against the oracle."""
+    kv, causal = case
+    ns = (14, 12, 12, 10)
+    wl = W.make_workload(spec_of(512, 2, kv, causal, 10000.0 if causal else 0.0, ns=ns, lo=1, hi=400, max_len=400,
+                                 layers=1))
+    wl.requests[0].lengths[0] = 1
+    wl.requests[-1].lengths[-1] = 400
+    lens = [int(x) for q in wl.requests for x in q.lengths]
+    qtiles = (max(lens) + 127) // 128
+    items = (len(lens) * kv + 7) // 8 * 8 * (2 // kv) * qtiles
+    _say(f"hd256 persistent kv={kv} causal={causal}: {len(lens)} samples, {items} work-item slots, "
+         f"{torch.cuda.get_device_properties(0).multi_processor_count} compute units")
+    assert items > torch.cuda.get_device_properties(0).multi_processor_count
+    st = run(wl, align=16)
+    worst = check(wl, st)
+    _say(f"  hidden max-rel {worst:.3e}")
+
+
 def test_variant_grouped_equals_isolated_bitwise(jn):
     """Rotary positions come from each sample's own rows, so a sample's
     result does not depend on where the pack put it."""
